@@ -1,0 +1,10 @@
+"""Float64 CPU oracle of the InertiaKV decode-step eviction path.
+
+Test infrastructure only: the test-suite, the smoke check and the benchmark's CPU-baseline leg import it;
+the HIP library and its binding never do, and the two share no code.
+"""
+from .inertiakv import (  # noqa: F401
+    BF16, CUMULATIVE, EMA, F32, SINGLE_STEP, Cache, Params, StepResult, budget_from_ratio, compact_rows,
+    evict_step, fold_layers, head_attention, holefill_moves, layer_scores, new_token_prior, refresh_due,
+    select_keep, to_f64,
+)

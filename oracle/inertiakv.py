@@ -1,0 +1,296 @@
+"""Plain, slow, float64 CPU oracle of the InertiaKV / InertiaKV-Lazy decode-step eviction path.
+
+THIS IS TEST INFRASTRUCTURE. Only the test-suite, the smoke check and the benchmark's CPU-baseline leg may
+import it. The product (the HIP library and its Python binding) never calls it and shares no code with it.
+
+Paper: "What Matters for Aggressive Decoding-Time KV Eviction? Temporal Aggregation and Ranking Preservation".
+Each function names the passage it follows:
+
+* Sec. 3 (problem statement): budget B = floor((1 - rho) L0); eviction is irreversible; whenever the cache
+  holds more than B tokens the lowest-utility tokens are evicted.
+* Eq. 1: s_t(i) = (1/H) sum_h a_t^(h)(i), the last-query attention of every head, mean-pooled over the H
+  query heads.  Appendix "Implementation Details / Per-step scoring": under GQA each KV head's attention is
+  shared by its query-head group before pooling.
+* Eq. 2 / 3 / 4: single-step, cumulative and EMA aggregation rules.
+* Appendix "Implementation Details / Layer scoring": the EMA state is updated after every eligible layer,
+  m_{t,l} = alpha m_{t,l-1} + (1 - alpha) s_{t,l}, l = 1..K, m_{t,0} = m_{t-1,K}.
+* Appendix "Implementation Details / Momentum initialization": m_0 = 0 for every prefill position.
+* Eq. 5 and Sec. 3.2 "Lazy refresh": refresh set R_r = {t >= 1 : (t - 1) mod r = 0}; off the refresh set the
+  utility is carried unchanged and eviction still runs on the stale ranking (Appendix "Eviction on
+  non-refresh steps").
+* Appendix "New token insertion during non-refresh steps": the new token starts at the mean utility of the
+  L_t - 1 existing tokens and may be evicted on the same step.
+* Sec. 3.2 "Score-Free decoding" box: score once at decode step 1, freeze, new tokens take the current mean
+  momentum, evict whenever the cache exceeds B.
+
+Readings where the paper is silent (the same list is kept in the design notes):
+* H in Eq. 1 is the number of query heads; every query head gets its own softmax over its KV head's keys.
+* The logit is the scaled dot product q.k / sqrt(d), with an optional additive recency bias on the
+  `window` most recent absolute positions (a workload knob, 0 = off).
+* One retention set per sequence per step, taken after the last layer's fold and applied to every layer
+  and KV head.
+* A new token's prior at a refresh step is 0, like m_0 (the paper only fixes the non-refresh case).
+* Ties in utility are broken by keeping the lower absolute position.
+* Compaction is "hole-fill": with k = min(B, n), kept rows in slots >= k move, in ascending order, into the
+  evicted slots < k, in ascending order.  Attention is invariant to row order, so any layout is faithful;
+  this one moves the fewest rows.
+* Non-refresh initialisation policy "min" (lowest existing utility) is offered beside the paper's "mean".
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+F32 = "f32"
+BF16 = "bf16"
+
+
+# ----------------------------------------------------------------------------------------------------------
+# element handling
+# ----------------------------------------------------------------------------------------------------------
+def to_f64(raw: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact up-conversion of stored elements to float64.
+
+    bf16 elements are carried as their uint16 bit patterns; a bf16 value is the float32 whose upper 16 bits
+    are those bits, so the conversion is exact.
+    """
+    if dtype == F32:
+        return np.asarray(raw, dtype=np.float32).astype(np.float64)
+    if dtype == BF16:
+        bits = np.asarray(raw, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+        return bits.view(np.float32).astype(np.float64)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+# ----------------------------------------------------------------------------------------------------------
+# Sec. 3: budget, Eq. 5: refresh schedule
+# ----------------------------------------------------------------------------------------------------------
+def budget_from_ratio(prefill_len: int, compression_ratio: float) -> int:
+    """Sec. 3: B = floor((1 - rho) * L0)."""
+    return int(math.floor((1.0 - compression_ratio) * prefill_len + 1e-9))
+
+
+def refresh_due(t: int, period: int, score_free: bool) -> bool:
+    """Eq. 5: t is in R_r = {t >= 1 : (t-1) mod r == 0}.  Score-Free refreshes only at t = 1 (Sec. 3.2 box)."""
+    if t < 1:
+        raise ValueError("decode steps are numbered from 1")
+    if score_free:
+        return t == 1
+    return (t - 1) % period == 0
+
+
+# ----------------------------------------------------------------------------------------------------------
+# Eq. 1: last-query attention, mean-pooled over query heads (GQA-shared)
+# ----------------------------------------------------------------------------------------------------------
+def head_attention(q_h: np.ndarray, keys_g: np.ndarray, pos: np.ndarray | None = None, cur_pos: int = 0,
+                   recency_bias: float = 0.0, recency_window: int = 0) -> np.ndarray:
+    """a^(h)(i) = softmax_i(q_h . k_i / sqrt(d) [+ bias if pos_i is among the `window` newest positions])."""
+    d = q_h.shape[-1]
+    z = keys_g @ q_h / math.sqrt(d)
+    if recency_bias != 0.0 and recency_window > 0:
+        recent = np.asarray(pos) >= (cur_pos - (recency_window - 1))
+        z = z + recency_bias * recent
+    z = z - z.max()
+    e = np.exp(z)
+    return e / e.sum()
+
+
+def layer_scores(q_l: np.ndarray, keys_l: np.ndarray, pos: np.ndarray | None = None, cur_pos: int = 0,
+                 recency_bias: float = 0.0, recency_window: int = 0) -> np.ndarray:
+    """Eq. 1 for one layer and one sequence.
+
+    q_l:    [H_q, d]       float64, the current (last) query of every query head
+    keys_l: [H_kv, n, d]   float64, the cached keys of every KV head
+    returns s: [n] = (1/H_q) sum_h a^(h), query head h reading KV head h // (H_q / H_kv).
+    """
+    hq, hkv = q_l.shape[0], keys_l.shape[0]
+    if hq % hkv:
+        raise ValueError("query heads must be a multiple of KV heads")
+    group = hq // hkv
+    s = np.zeros(keys_l.shape[1], dtype=np.float64)
+    for h in range(hq):
+        s += head_attention(q_l[h], keys_l[h // group], pos, cur_pos, recency_bias, recency_window)
+    return s / hq
+
+
+# ----------------------------------------------------------------------------------------------------------
+# Eq. 2-4 + Appendix "Layer scoring": per-layer sequential aggregation
+# ----------------------------------------------------------------------------------------------------------
+EMA, SINGLE_STEP, CUMULATIVE = "ema", "single", "cumulative"
+
+
+def fold_layers(u: np.ndarray, s_layers, alpha: float, rule: str = EMA) -> np.ndarray:
+    """Fold the layer scores s_1..s_K (in ascending layer order) into the running utility.
+
+    EMA (Eq. 4, Appendix "Layer scoring"):  u <- alpha u + (1 - alpha) s_l for l = 1..K.
+    Single-step (Eq. 2):                    u <- s_l (only the last processed layer survives).
+    Cumulative (Eq. 3):                     u <- u + s_l.
+    """
+    u = np.array(u, dtype=np.float64, copy=True)
+    for s in s_layers:
+        if rule == EMA:
+            u = alpha * u + (1.0 - alpha) * np.asarray(s, dtype=np.float64)
+        elif rule == SINGLE_STEP:
+            u = np.array(s, dtype=np.float64, copy=True)
+        elif rule == CUMULATIVE:
+            u = u + np.asarray(s, dtype=np.float64)
+        else:
+            raise ValueError(f"unknown aggregation rule {rule!r}")
+    return u
+
+
+# ----------------------------------------------------------------------------------------------------------
+# Sec. 3 eviction rule: keep the B highest utilities (ties: lower position kept)
+# ----------------------------------------------------------------------------------------------------------
+def select_keep(u: np.ndarray, pos: np.ndarray, budget: int) -> np.ndarray:
+    """Boolean mask over the n cached tokens: the first min(B, n) under (u descending, position ascending)."""
+    n = len(u)
+    keep = np.zeros(n, dtype=bool)
+    if n <= budget:
+        keep[:] = True
+        return keep
+    order = np.lexsort((np.asarray(pos), -np.asarray(u, dtype=np.float64)))
+    keep[order[:budget]] = True
+    return keep
+
+
+def holefill_moves(keep: np.ndarray, budget: int):
+    """Hole-fill compaction plan.  k = min(B, n); holes = ascending evicted slots < k; tails = ascending kept
+    slots >= k; row tails[j] moves to holes[j].  Returns (dst, src) index arrays of equal length."""
+    n = len(keep)
+    k = min(budget, n)
+    holes = np.nonzero(~keep[:k])[0]
+    tails = np.nonzero(keep[k:])[0] + k
+    if len(holes) != len(tails):
+        raise ValueError("keep mask must retain exactly min(B, n) tokens")
+    return holes, tails
+
+
+# ----------------------------------------------------------------------------------------------------------
+# cache state and one decode step
+# ----------------------------------------------------------------------------------------------------------
+@dataclass
+class Params:
+    alpha: float
+    budget: int
+    refresh_period: int = 1
+    score_free: bool = False
+    nonrefresh_init: str = "mean"      # "mean" (Appendix, new-token insertion) or "min"
+    recency_bias: float = 0.0
+    recency_window: int = 0
+    rule: str = EMA
+
+
+@dataclass
+class Cache:
+    """One batch of sequences.  k, v: [K, b, H_kv, cap, d] raw elements (uint16 bf16 bits or float32);
+    u: [b, cap] float64 utility; pos: [b, cap] int64 absolute positions; n: rows in use (same for all b)."""
+    k: np.ndarray
+    v: np.ndarray
+    u: np.ndarray
+    pos: np.ndarray
+    n: int
+    dtype: str
+
+    def copy(self) -> "Cache":
+        return Cache(self.k.copy(), self.v.copy(), self.u.copy(), self.pos.copy(), self.n, self.dtype)
+
+
+@dataclass
+class StepResult:
+    refreshed: bool
+    n_scored: int                              # tokens in the cache after the append
+    keep: np.ndarray                           # [b, n_scored] bool, the retention decision
+    u_pre: np.ndarray                          # [b, n_scored] utility on which the decision was taken
+    s_layers: np.ndarray | None = None         # [K, b, n_scored] per-layer scores (refresh steps)
+    moves: list = field(default_factory=list)  # per sequence (dst, src)
+    n_out: int = 0
+
+
+def new_token_prior(u_existing: np.ndarray, refresh: bool, policy: str) -> float:
+    """Prior utility of the token appended at this step.
+
+    Refresh steps: 0, like m_0 (reading; the paper fixes only the non-refresh case).
+    Non-refresh steps: mean of the existing utilities (Appendix, new-token insertion; Score-Free box:
+    'current mean momentum'), or their minimum under the "min" policy.
+    """
+    if refresh or len(u_existing) == 0:
+        return 0.0
+    if policy == "mean":
+        return float(np.mean(u_existing))
+    if policy == "min":
+        return float(np.min(u_existing))
+    raise ValueError(f"unknown init policy {policy!r}")
+
+
+def evict_step(cache: Cache, q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray, t: int, new_pos: int,
+               params: Params, keep_override: np.ndarray | None = None) -> StepResult:
+    """One decode step, mutating `cache` in place.
+
+    q: [K, b, H_q, d] raw; k_new, v_new: [K, b, H_kv, d] raw.
+    1. append the new token (K/V row at slot n, its position and prior utility);
+    2. on refresh steps, score every cached token layer by layer (Eq. 1) and fold (Eq. 4, layer-sequential);
+    3. if more than B tokens are cached, keep the top B (ties: lower position);
+    4. hole-fill compaction of K, V, u and pos.
+    `keep_override` lets a caller replace the selection by an equally valid one (used only to keep two
+    implementations in lockstep after a tie inside the rounding band); it must keep exactly min(B, n) tokens.
+    """
+    nl, nb, hkv, cap, d = cache.k.shape
+    n = cache.n
+    if n + 1 > cap:
+        raise ValueError("cache capacity exceeded")
+    refresh = refresh_due(t, params.refresh_period, params.score_free)
+
+    # 1. append
+    for b in range(nb):
+        cache.u[b, n] = new_token_prior(cache.u[b, :n], refresh, params.nonrefresh_init)
+        cache.pos[b, n] = new_pos
+    cache.k[:, :, :, n, :] = k_new
+    cache.v[:, :, :, n, :] = v_new
+    n += 1
+    cache.n = n
+
+    # 2. score + fold
+    s_all = None
+    if refresh:
+        s_all = np.zeros((nl, nb, n), dtype=np.float64)
+        for b in range(nb):
+            for l in range(nl):
+                keys = to_f64(cache.k[l, b, :, :n, :], cache.dtype)
+                ql = to_f64(q[l, b], cache.dtype)
+                s_all[l, b] = layer_scores(ql, keys, cache.pos[b, :n], new_pos,
+                                           params.recency_bias, params.recency_window)
+            cache.u[b, :n] = fold_layers(cache.u[b, :n], s_all[:, b], params.alpha, params.rule)
+    u_pre = cache.u[:, :n].copy()
+
+    # 3. select
+    keep = np.zeros((nb, n), dtype=bool)
+    for b in range(nb):
+        keep[b] = select_keep(cache.u[b, :n], cache.pos[b, :n], params.budget)
+    if keep_override is not None:
+        keep_override = np.asarray(keep_override, dtype=bool)[:, :n]
+        if not np.all(keep_override.sum(axis=1) == min(params.budget, n)):
+            raise ValueError("override must keep exactly min(B, n) tokens per sequence")
+        keep = keep_override
+
+    # 4. compact
+    moves = []
+    for b in range(nb):
+        dst, src = holefill_moves(keep[b], params.budget)
+        cache.k[:, b, :, dst, :] = cache.k[:, b, :, src, :]
+        cache.v[:, b, :, dst, :] = cache.v[:, b, :, src, :]
+        cache.u[b, dst] = cache.u[b, src]
+        cache.pos[b, dst] = cache.pos[b, src]
+        moves.append((dst, src))
+    cache.n = min(params.budget, n)
+    return StepResult(refresh, n, keep, u_pre, s_all, moves, cache.n)
+
+
+def compact_rows(rows: np.ndarray, keep: np.ndarray, budget: int) -> np.ndarray:
+    """Hole-fill applied to one [n_slots, ...] array (e.g. a K slab); returns a new array."""
+    out = np.array(rows, copy=True)
+    dst, src = holefill_moves(keep, budget)
+    out[dst] = rows[src]
+    return out
