@@ -1,0 +1,136 @@
+/*
+ * inertiakv.h - C ABI of the InertiaKV / InertiaKV-Lazy decode-step KV-eviction path on one MI355X (gfx950).
+ *
+ * Method: "What Matters for Aggressive Decoding-Time KV Eviction? Temporal Aggregation and Ranking
+ * Preservation".  Every decode step appends one token to a KV cache; on refresh steps every cached token is
+ * scored by the last query's softmax attention, mean-pooled over query heads (Eq. 1; GQA groups share their KV
+ * head, implementation appendix "Per-step scoring"), and the scores of layers 1..K are folded in order into one
+ * utility per token, u <- alpha u + (1 - alpha) s_l (Eq. 4 and appendix "Layer scoring").  Whenever the cache
+ * holds more than B tokens the lowest utilities are evicted (Sec. 3), ties going to the higher position, and the
+ * retained K/V rows are compacted.  Lazy refresh (Eq. 5) scores only on steps t with (t - 1) mod R == 0;
+ * Score-Free (Sec. 3.2) scores only at t = 1.  Off the refresh set the new token starts at the mean (or, as an
+ * option, the minimum) of the existing utilities (appendix "New token insertion") and eviction uses the stale
+ * ranking (appendix "Eviction on non-refresh steps").
+ *
+ * Conventions for every call
+ *  - Buffer pointers are DEVICE pointers owned by the caller; the library never allocates, frees or
+ *    synchronises device memory and never reads them on the host.  Scratch comes from a caller workspace of
+ *    at least kv_workspace_bytes() bytes, 256-byte aligned.
+ *  - Work is queued asynchronously on `stream` (a hipStream_t; NULL = the default stream) in stream order.
+ *  - Arguments are validated on the host before anything is queued; an invalid call returns a negative
+ *    kv_status and queues nothing.  KV_ERR_HIP reports a failed launch (hipGetLastError).
+ *  - Layouts (row-major, innermost last; d = head_dim, cap = capacity):
+ *      K, V cache  [layers][batch][n_kv_heads][cap][d]   dtype (f32 or bf16), rows [0, n) in use
+ *      q           [layers][batch][n_q_heads][d]         dtype, the current query of every head and layer
+ *      k_new,v_new [layers][batch][n_kv_heads][d]        dtype, the token appended at this step
+ *      u           [batch][cap] float                    utility per cached token
+ *      pos         [batch][cap] int32                    absolute position per cached token (unique, >= 0)
+ *      keep        [batch][cap] uint8                    1 = retained (first n entries written)
+ *      s_out       [layers][batch][n] float              per-layer pooled score s_l (optional, may be NULL)
+ *    Query head h reads KV head h / (n_q_heads / n_kv_heads).  Every sequence holds the same n tokens.
+ *  - Preconditions not checked on the device: keys, queries and utilities are finite; utilities are >= 0
+ *    when produced by this library; positions are unique within a sequence.
+ *  - The calls are stateless and may run concurrently on different streams with disjoint buffers.
+ */
+#ifndef INERTIAKV_H
+#define INERTIAKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    KV_OK = 0,
+    KV_ERR_INVALID_ARG = -1, /* null pointer, bad size, n out of range, alpha outside [0, 1), ...        */
+    KV_ERR_UNSUPPORTED = -2, /* head_dim not 64/128, group size > 16, dtype not f32/bf16, misalignment   */
+    KV_ERR_WORKSPACE = -3,   /* workspace missing or smaller than kv_workspace_bytes()                   */
+    KV_ERR_HIP = -4          /* a kernel launch failed                                                    */
+} kv_status;
+
+typedef enum { KV_F32 = 0, KV_BF16 = 1 } kv_dtype;
+
+/* Prior utility of the token appended on a NON-refresh step (appendix "New token insertion": MEAN). */
+typedef enum { KV_INIT_MEAN = 0, KV_INIT_MIN = 1 } kv_init;
+
+/* Aggregation rule (Eq. 2-4), applied layer by layer: EMA u <- alpha u + (1-alpha) s_l; single-step u <- s_l;
+ * cumulative u <- u + s_l. */
+typedef enum { KV_RULE_EMA = 0, KV_RULE_SINGLE_STEP = 1, KV_RULE_CUMULATIVE = 2 } kv_rule;
+
+typedef struct {
+    int32_t batch;      /* sequences                                   >= 1              */
+    int32_t layers;     /* eligible layers K, folded in ascending order 1..256           */
+    int32_t n_q_heads;  /* query heads H (Eq. 1)                       multiple of n_kv  */
+    int32_t n_kv_heads; /* KV heads; group size n_q/n_kv <= 16                           */
+    int32_t head_dim;   /* 64 or 128                                                     */
+    int32_t capacity;   /* rows per (layer, sequence, KV head) slab                      */
+    int32_t dtype;      /* kv_dtype of q, K, V, k_new, v_new                              */
+} kv_shape;
+
+typedef struct {
+    float alpha;            /* EMA coefficient, 0 <= alpha < 1 (alpha = 0: last layer only)        */
+    int32_t budget;         /* B >= 1: tokens kept whenever more are cached                         */
+    int32_t refresh_period; /* R >= 1: refresh iff (t - 1) mod R == 0 (Eq. 5); 1 = full refresh     */
+    int32_t score_free;     /* nonzero: refresh only at t = 1 (Score-Free)                          */
+    int32_t nonrefresh_init;/* kv_init                                                             */
+    float recency_bias;     /* added to logits of the `recency_window` newest positions; 0 = off    */
+    int32_t recency_window; /* positions p >= new_pos - (window - 1) get the bias                   */
+    int32_t rule;           /* kv_rule                                                             */
+} kv_params;
+
+/* Optional timing hooks: when an entry is non-NULL, kv_evict_step records that hipEvent_t on its stream
+ * immediately before (begin) / after (end) the kernels of the phase.  Phases: 0 append, 1 score, 2 fold,
+ * 3 select, 4 compact. */
+#define KV_PHASES 5
+typedef struct {
+    void* begin[KV_PHASES];
+    void* end[KV_PHASES];
+} kv_trace;
+
+/* Bytes of workspace needed by every call below for any n <= n_max cached tokens (host only). */
+kv_status kv_workspace_bytes(const kv_shape* shape, int32_t n_max, size_t* bytes);
+
+/* Scoring + fold (Eq. 1 and Eq. 4, layer-sequential).  For every layer l = 1..K, query head h and cached
+ * token i < n: z_h(i) = q_h . k_i / sqrt(d) (+ recency_bias if pos[i] >= cur_pos - (recency_window - 1)),
+ * a_h = softmax over the n tokens, s_l(i) = (1/H) sum_h a_h(i); then u <- alpha u + (1 - alpha) s_l for
+ * l = 1..K in order (u updated in place for i < n; entries >= n untouched).  s_out (nullable) receives s_l. */
+kv_status kv_score_ema(const kv_shape* shape, int32_t n, const void* q, const void* k, const int32_t* pos,
+                       int32_t cur_pos, float alpha, float recency_bias, int32_t recency_window, float* u,
+                       float* s_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Top-B selection (Sec. 3): keep[b][i] = 1 for the min(B, n) tokens first under (u descending, position
+ * ascending), 0 for the others, for i < n. */
+kv_status kv_topk_select(const kv_shape* shape, int32_t n, int32_t budget, const float* u, const int32_t* pos,
+                         uint8_t* keep, void* ws, size_t ws_bytes, void* stream);
+
+/* Hole-fill compaction of a retention decision (which must keep exactly min(B, n) tokens per sequence):
+ * with k = min(B, n), the kept rows in slots >= k move, in ascending order, into the dropped slots < k, in
+ * ascending order, for every layer and KV head of K and V, and for u and pos.  Rows [0, k) then hold exactly
+ * the retained tokens; rows >= k are left as they were.  A mask that keeps a different count is rejected on
+ * the device by moving nothing beyond the smaller of the two lists. */
+kv_status kv_compact(const kv_shape* shape, int32_t n, int32_t budget, const uint8_t* keep, void* k, void* v,
+                     float* u, int32_t* pos, void* ws, size_t ws_bytes, void* stream);
+
+/* One decode step t >= 1 on a cache of n_in tokens (n_in + 1 <= capacity):
+ *  1. append k_new/v_new at slot n_in, pos = new_pos, u = 0 on refresh steps, else the mean (or min) of the
+ *     n_in existing utilities;
+ *  2. refresh steps only: kv_score_ema over the n_in + 1 tokens with q, cur_pos = new_pos;
+ *  3. if n_in + 1 > B: select the top B (stale utilities on non-refresh steps) and compact as kv_compact.
+ * *n_out (HOST pointer) receives min(B, n_in + 1).  keep_out (nullable) receives the decision over the
+ * n_in + 1 slots before compaction; s_out (nullable) the per-layer scores of a refresh step; trace (nullable)
+ * timing events. */
+kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in,
+                        int32_t new_pos, const void* q, const void* k_new, const void* v_new, void* k, void* v,
+                        float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
+                        const kv_trace* trace, void* ws, size_t ws_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* kv_status_string(kv_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* INERTIAKV_H */

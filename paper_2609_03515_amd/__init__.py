@@ -1,0 +1,6 @@
+"""InertiaKV / InertiaKV-Lazy decode-step KV eviction on MI355X (gfx950): HIP kernels behind a C ABI.
+
+`binding` wraps the C entry points of libinertiakv.so (kv_score_ema, kv_topk_select, kv_compact,
+kv_evict_step); `build` compiles the library with hipcc.  The library is loaded on first use and its absence
+is an error.
+"""

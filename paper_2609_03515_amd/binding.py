@@ -1,0 +1,213 @@
+"""ctypes binding of libinertiakv.so: argument marshalling only.
+
+Every function carries the name of the C entry point it calls and takes torch tensors for device buffers;
+it passes their device pointers and the current HIP stream, and raises KVError on a non-zero status.  All
+computation happens in the HIP kernels behind the C ABI; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libinertiakv.so")
+
+KV_OK, KV_ERR_INVALID_ARG, KV_ERR_UNSUPPORTED, KV_ERR_WORKSPACE, KV_ERR_HIP = 0, -1, -2, -3, -4
+KV_F32, KV_BF16 = 0, 1
+KV_INIT_MEAN, KV_INIT_MIN = 0, 1
+KV_RULE_EMA, KV_RULE_SINGLE_STEP, KV_RULE_CUMULATIVE = 0, 1, 2
+KV_PHASES = 5
+PHASES = ("append", "score", "fold", "select", "compact")
+
+EXPORTED = ("kv_workspace_bytes", "kv_score_ema", "kv_topk_select", "kv_compact", "kv_evict_step",
+            "kv_status_string")
+
+
+class KVError(RuntimeError):
+    def __init__(self, fn, status):
+        super().__init__(f"{fn} failed: {status_string(status)} ({status})")
+        self.status = status
+
+
+class KvShape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("capacity", ctypes.c_int32),
+                ("dtype", ctypes.c_int32)]
+
+
+class KvParams(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_float), ("budget", ctypes.c_int32), ("refresh_period", ctypes.c_int32),
+                ("score_free", ctypes.c_int32), ("nonrefresh_init", ctypes.c_int32),
+                ("recency_bias", ctypes.c_float), ("recency_window", ctypes.c_int32), ("rule", ctypes.c_int32)]
+
+
+class KvTrace(ctypes.Structure):
+    _fields_ = [("begin", ctypes.c_void_p * KV_PHASES), ("end", ctypes.c_void_p * KV_PHASES)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Loads the built library; raises if it is missing (there is no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2609_03515_amd.build.build()")
+    lib = ctypes.CDLL(path)
+    vp, i32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+    shp, prm, trc = ctypes.POINTER(KvShape), ctypes.POINTER(KvParams), ctypes.POINTER(KvTrace)
+    lib.kv_workspace_bytes.argtypes = [shp, i32, ctypes.POINTER(sz)]
+    lib.kv_score_ema.argtypes = [shp, i32, vp, vp, vp, i32, f32, f32, i32, vp, vp, vp, sz, vp]
+    lib.kv_topk_select.argtypes = [shp, i32, i32, vp, vp, vp, vp, sz, vp]
+    lib.kv_compact.argtypes = [shp, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.kv_evict_step.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+                                  ctypes.POINTER(i32), vp, vp, trc, vp, sz, vp]
+    for fn in EXPORTED[:-1]:
+        getattr(lib, fn).restype = i32
+    lib.kv_status_string.argtypes = [i32]
+    lib.kv_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().kv_status_string(int(status)).decode()
+
+
+def _check(fn, status):
+    if status != KV_OK:
+        raise KVError(fn, status)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def make_shape(batch, layers, n_q_heads, n_kv_heads, head_dim, capacity, dtype) -> KvShape:
+    if isinstance(dtype, str):
+        dtype = {"f32": KV_F32, "bf16": KV_BF16}[dtype]
+    elif dtype in (torch.float32, torch.bfloat16):
+        dtype = KV_F32 if dtype == torch.float32 else KV_BF16
+    return KvShape(batch, layers, n_q_heads, n_kv_heads, head_dim, capacity, dtype)
+
+
+def make_params(alpha, budget, refresh_period=1, score_free=False, nonrefresh_init="mean", recency_bias=0.0,
+                recency_window=0, rule="ema") -> KvParams:
+    init = {"mean": KV_INIT_MEAN, "min": KV_INIT_MIN}[nonrefresh_init] if isinstance(nonrefresh_init, str) \
+        else int(nonrefresh_init)
+    rl = {"ema": KV_RULE_EMA, "single": KV_RULE_SINGLE_STEP, "cumulative": KV_RULE_CUMULATIVE}[rule] \
+        if isinstance(rule, str) else int(rule)
+    return KvParams(float(alpha), int(budget), int(refresh_period), int(bool(score_free)), init,
+                    float(recency_bias), int(recency_window), rl)
+
+
+def kv_workspace_bytes(shape: KvShape, n_max: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check("kv_workspace_bytes", load_library().kv_workspace_bytes(ctypes.byref(shape), int(n_max),
+                                                                    ctypes.byref(out)))
+    return out.value
+
+
+def kv_score_ema(shape, n, q, k, pos, cur_pos, alpha, recency_bias, recency_window, u, s_out, ws, stream=None):
+    _check("kv_score_ema", load_library().kv_score_ema(
+        ctypes.byref(shape), int(n), _ptr(q), _ptr(k), _ptr(pos), int(cur_pos), float(alpha),
+        float(recency_bias), int(recency_window), _ptr(u), _ptr(s_out), _ptr(ws),
+        ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+
+
+def kv_topk_select(shape, n, budget, u, pos, keep, ws, stream=None):
+    _check("kv_topk_select", load_library().kv_topk_select(
+        ctypes.byref(shape), int(n), int(budget), _ptr(u), _ptr(pos), _ptr(keep), _ptr(ws),
+        ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+
+
+def kv_compact(shape, n, budget, keep, k, v, u, pos, ws, stream=None):
+    _check("kv_compact", load_library().kv_compact(
+        ctypes.byref(shape), int(n), int(budget), _ptr(keep), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), _ptr(ws),
+        ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+
+
+def kv_evict_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, ws, keep_out=None,
+                  s_out=None, trace: KvTrace | None = None, stream=None) -> int:
+    """Returns n_out = min(B, n_in + 1)."""
+    n_out = ctypes.c_int32(-1)
+    _check("kv_evict_step", load_library().kv_evict_step(
+        ctypes.byref(shape), ctypes.byref(params), int(t), int(n_in), int(new_pos), _ptr(q), _ptr(k_new),
+        _ptr(v_new), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out),
+        ctypes.byref(trace) if trace is not None else None, _ptr(ws),
+        ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+    return n_out.value
+
+
+def workspace(shape: KvShape, n_max: int, device="cuda") -> torch.Tensor:
+    """A caller-owned workspace tensor of kv_workspace_bytes() bytes (256-byte aligned by the allocator)."""
+    nbytes = kv_workspace_bytes(shape, n_max)
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+# --- HIP events for the timing hooks (runtime plumbing, no computation) -------------------------------------
+_hip = None
+
+
+def _hip_runtime():
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+        _hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        _hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        _hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        _hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        _hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    return _hip
+
+
+class HipEvent:
+    def __init__(self):
+        self.handle = ctypes.c_void_p()
+        rc = _hip_runtime().hipEventCreate(ctypes.byref(self.handle))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreate failed ({rc})")
+
+    def record(self, stream=None):
+        rc = _hip_runtime().hipEventRecord(self.handle, _stream(stream))
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def elapsed_ms(self, later: "HipEvent") -> float:
+        _hip_runtime().hipEventSynchronize(later.handle)
+        out = ctypes.c_float(0)
+        rc = _hip_runtime().hipEventElapsedTime(ctypes.byref(out), self.handle, later.handle)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return out.value
+
+    def __del__(self):
+        if _hip is not None and self.handle:
+            _hip.hipEventDestroy(self.handle)
+            self.handle = ctypes.c_void_p()
+
+
+def make_trace(pairs: dict) -> KvTrace:
+    """pairs: phase name -> (begin HipEvent, end HipEvent)."""
+    tr = KvTrace()
+    for i, name in enumerate(PHASES):
+        if name in pairs:
+            tr.begin[i] = pairs[name][0].handle.value
+            tr.end[i] = pairs[name][1].handle.value
+    return tr

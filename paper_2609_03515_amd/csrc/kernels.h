@@ -1,0 +1,98 @@
+// Host-side launchers of the eviction-path kernels (implemented in the .hip files beside this header).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace ikv {
+
+constexpr int kMaxLayers = 256;
+constexpr int kMaxGroup = 16;
+
+// Scoring of one step (Eq. 1).  Fast path: one workgroup streams a whole (layer, sequence, KV head) slab
+// and keeps its logits in LDS, writing the group probability sums r.  Split path: several workgroups per
+// slab write logits z and per-head partial (max, sum) pairs; a finish kernel turns them into r.
+struct ScoreArgs {
+    const void* q;
+    const void* k;
+    const int32_t* pos;
+    float* r;       // [layers][batch][n_kv][n_stride]
+    float* z;       // split: [layers][batch][n_q][n_stride]
+    float2* part;   // split: [layers][batch][n_q][nchunk] (max, sum)
+    int batch, layers, hq, hkv, group, cap, n, n_stride;
+    int recent_from;  // positions >= recent_from receive `bias`
+    float bias;
+    float scale;      // 1 / sqrt(d)
+    int chunk_rows, nchunk;
+};
+
+struct ScorePlan {
+    bool split;
+    int group_pad;     // group size rounded up to a power of two
+    int waves;         // waves per workgroup
+    int rows_per_iter; // rows one workgroup covers per loop iteration
+    int chunk_rows;    // rows per workgroup
+    int nchunk;        // workgroups per slab
+    size_t lds_bytes;  // dynamic LDS per workgroup (fast path)
+    int grid;
+};
+
+bool score_plan(int dtype, int head_dim, int group, int n, ScorePlan* plan);
+hipError_t launch_score(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s);
+hipError_t launch_split_finish(const ScoreArgs& a, hipStream_t s);
+
+// Layer fold (Eq. 2-4): u <- prior_w * u + sum_l w_l s_l with s_l = (1/H) sum_g r_{l,g}.
+struct FoldArgs {
+    const float* r;
+    float* u;
+    float* s_out;  // nullable [layers][batch][n]
+    int batch, layers, hkv, n, n_stride, cap;
+    float inv_hq;
+    float prior_w;
+    float w[kMaxLayers];
+};
+hipError_t launch_fold(const FoldArgs& a, hipStream_t s);
+
+// Selection + compaction plan, one workgroup per sequence.
+struct SelectArgs {
+    const float* u;
+    const int32_t* pos;
+    const uint8_t* keep_in;  // plan-only mode: the retention decision to compact
+    uint8_t* keep_out;       // nullable: decision written here ([batch][cap])
+    int32_t* pair_dst;       // [batch][max_pairs]
+    int32_t* pair_src;
+    int32_t* npairs;         // [batch]
+    int batch, cap, n, budget, max_pairs;
+};
+hipError_t launch_select(const SelectArgs& a, bool plan_only, hipStream_t s);
+
+// Row moves of the compaction plan for K, V, u and pos.
+struct MoveArgs {
+    void* k;
+    void* v;
+    float* u;
+    int32_t* pos;
+    const int32_t* pair_dst;
+    const int32_t* pair_src;
+    const int32_t* npairs;
+    int batch, layers, hkv, cap, row_bytes;
+    int max_pairs;    // loop bound on pairs per sequence
+    int pair_stride;  // row stride of pair_dst / pair_src
+};
+hipError_t launch_move(const MoveArgs& a, hipStream_t s);
+
+// Append of the new token's K/V rows, position and prior utility.
+struct AppendArgs {
+    void* k;
+    void* v;
+    const void* k_new;
+    const void* v_new;
+    float* u;
+    int32_t* pos;
+    int batch, layers, hkv, cap, row_bytes, n_in, new_pos;
+    int init_mode;  // 0: zero (refresh step), 1: mean, 2: min of u[0, n_in)
+};
+hipError_t launch_append(const AppendArgs& a, hipStream_t s);
+
+}  // namespace ikv

@@ -1,0 +1,137 @@
+// Device helpers shared by the eviction-path kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ikv {
+
+constexpr int kWave = 64;
+
+typedef __bf16 __attribute__((ext_vector_type(2))) bf16x2;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Cross-lane exchange inside a 16-lane DPP row.  Controls used here:
+//   0xB1 quad_perm [1,0,3,2] (lane ^ 1)     0x4E quad_perm [2,3,0,1] (lane ^ 2)
+//   0x141 row_half_mirror (lane ^ 7 inside each 8-lane half)      0x128 row_ror:8 (lane ^ 8 inside 16)
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+    return __builtin_amdgcn_update_dpp(0.0f, x, CTRL, 0xF, 0xF, true);
+}
+constexpr int kXor1 = 0xB1;
+constexpr int kXor2 = 0x4E;
+constexpr int kMirror8 = 0x141;
+constexpr int kRor8 = 0x128;
+
+// Partner control for the butterfly step that separates lanes by bit `mask` (1, 2, 4, 8) of the lane
+// index inside its aligned group; the partner differs in that bit and agrees on all higher bits.
+template <int MASK>
+struct StepCtrl;
+template <> struct StepCtrl<1> { static constexpr int v = kXor1; };
+template <> struct StepCtrl<2> { static constexpr int v = kXor2; };
+template <> struct StepCtrl<4> { static constexpr int v = kMirror8; };
+template <> struct StepCtrl<8> { static constexpr int v = kRor8; };
+
+// Sum over the aligned group of W lanes (W in 1, 2, 4, 8, 16); every lane of the group gets the total.
+template <int W>
+__device__ __forceinline__ float group_allsum(float x) {
+    if constexpr (W >= 2) x += dpp<kXor1>(x);
+    if constexpr (W >= 4) x += dpp<kXor2>(x);
+    if constexpr (W >= 8) x += dpp<kMirror8>(x);
+    if constexpr (W >= 16) x += dpp<kRor8>(x);
+    return x;
+}
+
+// Reduce-scatter of V = W values over an aligned group of W lanes: afterwards v[0] of the lane with in-group
+// index p holds the group total of value index p.  At each step the lane keeps the half of the remaining
+// indices selected by its own bit and adds the partner's copy of the same indices.
+template <int W, int HALF>
+__device__ __forceinline__ void scatter_step(float (&v)[W], int p) {
+    const bool upper = (p & HALF) != 0;
+#pragma unroll
+    for (int i = 0; i < HALF; ++i) {
+        const float lo = v[i], hi = v[i + HALF];
+        const float keep = upper ? hi : lo;
+        const float send = upper ? lo : hi;
+        v[i] = keep + dpp<StepCtrl<HALF>::v>(send);
+    }
+}
+template <int W>
+__device__ __forceinline__ float reduce_scatter(float (&v)[W], int p) {
+    if constexpr (W >= 16) scatter_step<W, 8>(v, p);
+    if constexpr (W >= 8) scatter_step<W, 4>(v, p);
+    if constexpr (W >= 4) scatter_step<W, 2>(v, p);
+    if constexpr (W >= 2) scatter_step<W, 1>(v, p);
+    return v[0];
+}
+
+// Online-softmax pair (running max, sum of exp(z - max)).
+struct MaxSum {
+    float m, s;
+};
+__device__ __forceinline__ MaxSum ms_combine(MaxSum a, MaxSum b) {
+    const float m = fmaxf(a.m, b.m);
+    if (m == -INFINITY) return {m, 0.0f};
+    return {m, a.s * __expf(a.m - m) + b.s * __expf(b.m - m)};
+}
+
+// Order-preserving map of a float onto uint32 (larger float -> larger key; -0 < +0).
+__device__ __forceinline__ uint32_t float_key(float x) {
+    const uint32_t b = __float_as_uint(x);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, kWave));
+    return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, kWave);
+    return x;
+}
+
+// Element traits: 16-byte chunk of a K row and of a query, and the dot product of two chunks.
+template <typename T>
+struct Elem;
+
+template <>
+struct Elem<float> {
+    static constexpr int kPerChunk = 4;
+    typedef f32x4 chunk_t;
+    __device__ __forceinline__ static float dot(const chunk_t& k, const chunk_t& q, float acc) {
+        acc = fmaf(k.x, q.x, acc);
+        acc = fmaf(k.y, q.y, acc);
+        acc = fmaf(k.z, q.z, acc);
+        acc = fmaf(k.w, q.w, acc);
+        return acc;
+    }
+};
+
+struct bf16_t {
+    uint16_t bits;
+};
+
+template <>
+struct Elem<bf16_t> {
+    static constexpr int kPerChunk = 8;
+    typedef u32x4 chunk_t;  // 8 bf16 as 4 packed pairs
+    __device__ __forceinline__ static float dot2(uint32_t a, uint32_t b, float acc) {
+        return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a), __builtin_bit_cast(bf16x2, b),
+                                               acc, false);
+    }
+    __device__ __forceinline__ static float dot(const chunk_t& k, const chunk_t& q, float acc) {
+        acc = dot2(k.x, q.x, acc);
+        acc = dot2(k.y, q.y, acc);
+        acc = dot2(k.z, q.z, acc);
+        acc = dot2(k.w, q.w, acc);
+        return acc;
+    }
+};
+
+__host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x >> 1); }
+__host__ __device__ constexpr size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+}  // namespace ikv

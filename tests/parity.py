@@ -1,0 +1,60 @@
+"""Helpers for GPU-vs-oracle parity tests: moving the same seeded inputs to both sides and comparing."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from oracle import Cache, Params
+from workload import raw_numpy
+
+REL_TOL = 1e-3        # scores and utilities
+ABS_TOL = 1e-12
+BAND = 1e-4           # retention sets may differ only for utilities this close to the B-th value
+
+
+def oracle_cache(st: dict, dtype: str) -> Cache:
+    return Cache(raw_numpy(st["k"]), raw_numpy(st["v"]), st["u"].detach().cpu().numpy().astype(np.float64),
+                 st["pos"].detach().cpu().numpy().astype(np.int64), int(st["n"]), dtype)
+
+
+def oracle_params(cfg, **kw) -> Params:
+    base = dict(alpha=cfg.alpha, budget=cfg.budget, refresh_period=cfg.refresh_period,
+                score_free=cfg.score_free, nonrefresh_init=cfg.nonrefresh_init,
+                recency_bias=cfg.recency_bias, recency_window=cfg.recency_window)
+    base.update(kw)
+    return Params(**base)
+
+
+def to_device(st: dict, device="cuda") -> dict:
+    return {k: (v.to(device).contiguous() if isinstance(v, torch.Tensor) else v) for k, v in st.items()}
+
+
+def assert_close(gpu, ref, what, rel=REL_TOL, abs_=ABS_TOL):
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert gpu.shape == ref.shape, (what, gpu.shape, ref.shape)
+    err = np.abs(gpu - ref)
+    lim = rel * np.abs(ref) + abs_
+    bad = np.nonzero(err > lim)
+    assert len(bad[0]) == 0, (f"{what}: {len(bad[0])} of {err.size} outside tolerance; worst rel "
+                              f"{np.max(err / (np.abs(ref) + 1e-30)):.3e} at {tuple(b[0] for b in bad)}")
+
+
+def band_mask(u_ref: np.ndarray, budget: int) -> np.ndarray:
+    """Tokens whose reference utility lies within BAND (relative) of the B-th value."""
+    n = len(u_ref)
+    if n <= budget:
+        return np.zeros(n, dtype=bool)
+    tau = np.sort(u_ref)[::-1][budget - 1]
+    return np.abs(u_ref - tau) <= BAND * abs(tau)
+
+
+def check_keep(keep_gpu: np.ndarray, keep_ref: np.ndarray, u_ref: np.ndarray, budget: int, what: str) -> int:
+    """Exact count; equality outside the rounding band.  Returns the number of in-band differences."""
+    keep_gpu = np.asarray(keep_gpu, dtype=bool)
+    keep_ref = np.asarray(keep_ref, dtype=bool)
+    assert keep_gpu.sum() == keep_ref.sum() == min(budget, len(keep_ref)), (what, keep_gpu.sum(), keep_ref.sum())
+    band = band_mask(u_ref, budget)
+    diff = keep_gpu != keep_ref
+    assert not np.any(diff & ~band), f"{what}: {int((diff & ~band).sum())} retention differences outside the band"
+    return int(diff.sum())

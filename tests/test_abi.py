@@ -1,0 +1,147 @@
+"""The C ABI library loads on a machine without a GPU, exports every declared entry point, and rejects bad
+arguments on the host before any HIP call (every call here is invalid, so nothing is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_03515_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "inertiakv.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:kv_status|const char\*)\s+(kv_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2609_03515_amd import build
+        build.build()
+    return B.load_library()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert names == sorted(B.EXPORTED)
+    for name in names:
+        assert hasattr(lib, name), name
+    assert ctypes.CDLL(B.LIB_PATH).kv_evict_step is not None
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4):
+        assert B.status_string(code)
+    assert B.status_string(-99) == "unknown status"
+
+
+GOOD = dict(batch=2, layers=3, n_q_heads=8, n_kv_heads=2, head_dim=128, capacity=100, dtype="bf16")
+
+
+def shape(**kw):
+    d = dict(GOOD)
+    d.update(kw)
+    return B.make_shape(**d)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=96), B.KV_ERR_UNSUPPORTED),
+    (dict(n_q_heads=7), B.KV_ERR_INVALID_ARG),
+    (dict(n_q_heads=64, n_kv_heads=2), B.KV_ERR_UNSUPPORTED),          # group 32 > 16
+    (dict(n_q_heads=32, n_kv_heads=2, head_dim=64), B.KV_ERR_UNSUPPORTED),  # group 16 > 8 lanes of a d64 bf16 row
+    (dict(dtype=7), B.KV_ERR_UNSUPPORTED),
+    (dict(batch=0), B.KV_ERR_INVALID_ARG),
+    (dict(layers=300), B.KV_ERR_UNSUPPORTED),
+])
+def test_bad_shapes(lib, kw, status):
+    with pytest.raises(B.KVError) as e:
+        B.kv_workspace_bytes(shape(**kw), 10)
+    assert e.value.status == status
+
+
+def test_workspace_monotone(lib):
+    s = shape(capacity=40000)
+    sizes = [B.kv_workspace_bytes(s, n) for n in (1, 100, 3278, 5000, 6000, 40000)]
+    assert sizes == sorted(sizes)
+    with pytest.raises(B.KVError):
+        B.kv_workspace_bytes(s, 40001)
+
+
+FAKE = 1 << 20   # a host-side stand-in address, never dereferenced: every call below fails validation
+
+
+def _score(s, n=10, alpha=0.9, ws=None, ws_bytes=0, q=FAKE, window=0):
+    return lib_().kv_score_ema(ctypes.byref(s), n, q, FAKE, FAKE, 0, alpha, 0.0, window, FAKE, None, ws,
+                               ws_bytes, None)
+
+
+def lib_():
+    return B.load_library()
+
+
+def test_score_validation(lib):
+    s = shape()
+    assert _score(s, n=0) == B.KV_ERR_INVALID_ARG
+    assert _score(s, n=101) == B.KV_ERR_INVALID_ARG
+    assert _score(s, alpha=1.0) == B.KV_ERR_INVALID_ARG
+    assert _score(s, alpha=-0.1) == B.KV_ERR_INVALID_ARG
+    assert _score(s, alpha=float("nan")) == B.KV_ERR_INVALID_ARG
+    assert _score(s, q=None) == B.KV_ERR_INVALID_ARG
+    assert _score(s, q=FAKE + 4) == B.KV_ERR_UNSUPPORTED      # misaligned rows
+    assert _score(s, window=-1) == B.KV_ERR_INVALID_ARG
+    assert _score(s) == B.KV_ERR_WORKSPACE                  # no workspace
+    need = B.kv_workspace_bytes(s, 10)
+    assert _score(s, ws=FAKE, ws_bytes=need - 1) == B.KV_ERR_WORKSPACE
+    assert _score(s, ws=FAKE + 16, ws_bytes=need) == B.KV_ERR_INVALID_ARG   # workspace not 256-aligned
+
+
+def test_select_compact_validation(lib):
+    s = shape()
+    L = lib_()
+    assert L.kv_topk_select(ctypes.byref(s), 10, 0, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == B.KV_ERR_INVALID_ARG
+    assert L.kv_topk_select(ctypes.byref(s), 10, 5, None, FAKE, FAKE, FAKE, 1 << 30, None) == B.KV_ERR_INVALID_ARG
+    assert L.kv_topk_select(ctypes.byref(s), 10, 5, FAKE, FAKE, FAKE, None, 0, None) == B.KV_ERR_WORKSPACE
+    assert L.kv_compact(ctypes.byref(s), 10, 5, None, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == \
+        B.KV_ERR_INVALID_ARG
+    assert L.kv_compact(ctypes.byref(s), 10, 5, FAKE, FAKE + 8, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == \
+        B.KV_ERR_UNSUPPORTED
+    # n <= B is a no-op that still validates the workspace
+    assert L.kv_compact(ctypes.byref(s), 10, 50, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == B.KV_ERR_WORKSPACE
+
+
+def _step(s, p, t=1, n_in=10, n_out=True, **kw):
+    args = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k=FAKE, v=FAKE, u=FAKE, pos=FAKE, ws=None, ws_bytes=0)
+    args.update(kw)
+    out = ctypes.c_int32(-7)
+    rc = lib_().kv_evict_step(ctypes.byref(s), ctypes.byref(p) if p is not None else None, t, n_in, 5,
+                              args["q"], args["k_new"], args["v_new"], args["k"], args["v"], args["u"], args["pos"],
+                              ctypes.byref(out) if n_out else None, None, None, None, args["ws"], args["ws_bytes"],
+                              None)
+    return rc, out.value
+
+
+def test_step_validation(lib):
+    s = shape()
+    good = B.make_params(0.9, 20)
+    assert _step(s, None)[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, good, n_out=False)[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, good, t=0)[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, good, n_in=100)[0] == B.KV_ERR_INVALID_ARG          # n_in + 1 > capacity
+    assert _step(s, good, n_in=-1)[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, B.make_params(1.0, 20))[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, B.make_params(0.9, 0))[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, B.make_params(0.9, 20, refresh_period=0))[0] == B.KV_ERR_INVALID_ARG
+    bad_init = B.make_params(0.9, 20)
+    bad_init.nonrefresh_init = 5
+    assert _step(s, bad_init)[0] == B.KV_ERR_INVALID_ARG
+    bad_rule = B.make_params(0.9, 20)
+    bad_rule.rule = 9
+    assert _step(s, bad_rule)[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, good, v_new=None)[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, good, k=FAKE + 2)[0] == B.KV_ERR_UNSUPPORTED
+    rc, out = _step(s, good)
+    assert rc == B.KV_ERR_WORKSPACE and out == -7                      # nothing written on failure

@@ -1,0 +1,92 @@
+"""Multi-step GPU parity of kv_evict_step against the oracle in lockstep, on the five workloads at sizes the
+oracle finishes in seconds (same GQA shapes, dtypes, schedules and input laws; fewer tokens and layers).
+
+Per step: per-layer scores and the compacted utilities within 1e-3 relative; retention sets equal outside
+the 1e-4 band around the B-th utility; positions and compacted K/V rows bit-exact.  When the GPU takes an
+equally valid in-band decision, the oracle adopts it (its own float64 utilities kept) so the runs stay
+comparable; such flips are counted and reported."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import evict_step
+from parity import assert_close, check_keep, oracle_cache, oracle_params, to_device
+from workload import LLAMA8B, LLAMA8B_LAZY, QWEN, SCOREFREE128K, TINY, Workload, raw_numpy
+
+pytestmark = pytest.mark.gpu
+
+B = pytest.importorskip("paper_2609_03515_amd.binding")
+
+
+def run_lockstep(cfg, steps, seed=None, rule="ema"):
+    w = Workload(cfg, seed=seed)
+    cap = max(cfg.prefill_len, cfg.budget) + 1          # room for the cache to grow up to B + 1
+    st = w.prefill(capacity=cap)
+    oc = oracle_cache(st, cfg.dtype)
+    dev = to_device(st)
+    shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
+    params = B.make_params(cfg.alpha, cfg.budget, cfg.refresh_period, cfg.score_free, cfg.nonrefresh_init,
+                           cfg.recency_bias, cfg.recency_window, rule)
+    op = oracle_params(cfg, rule=rule)
+    ws = B.workspace(shape, cap)
+    n = st["n"]
+    flips = 0
+    for t in range(1, steps + 1):
+        si = w.step_inputs(t)
+        sig = to_device(si)
+        keep = torch.zeros(cfg.batch, cap, dtype=torch.uint8, device="cuda")
+        s_out = torch.full((cfg.layers, cfg.batch, n + 1), -1.0, device="cuda")
+        n_out = B.kv_evict_step(shape, params, t, n, si["new_pos"], sig["q"], sig["k_new"], sig["v_new"],
+                                dev["k"], dev["v"], dev["u"], dev["pos"], ws, keep_out=keep, s_out=s_out)
+        torch.cuda.synchronize()
+        q_raw, kn_raw, vn_raw = raw_numpy(si["q"]), raw_numpy(si["k_new"]), raw_numpy(si["v_new"])
+        before = oc.copy()
+        ref = evict_step(oc, q_raw, kn_raw, vn_raw, t, si["new_pos"], op)
+        assert n_out == ref.n_out == min(cfg.budget, n + 1)
+        keep_g = keep.cpu().numpy()[:, : n + 1].astype(bool)
+        step_flips = 0
+        for b in range(cfg.batch):
+            step_flips += check_keep(keep_g[b], ref.keep[b], ref.u_pre[b], cfg.budget, f"{cfg.name} t={t} b={b}")
+        if step_flips:
+            oc = before
+            ref = evict_step(oc, q_raw, kn_raw, vn_raw, t, si["new_pos"], op, keep_override=keep_g)
+            flips += step_flips
+        if ref.refreshed:
+            assert_close(s_out.cpu().numpy(), ref.s_layers, f"{cfg.name} t={t} scores")
+        n = n_out
+        assert_close(dev["u"][:, :n].cpu().numpy(), oc.u[:, :n], f"{cfg.name} t={t} utilities")
+        np.testing.assert_array_equal(dev["pos"][:, :n].cpu().numpy(), oc.pos[:, :n])
+        np.testing.assert_array_equal(raw_numpy(dev["k"])[:, :, :, :n], oc.k[:, :, :, :n])
+        np.testing.assert_array_equal(raw_numpy(dev["v"])[:, :, :, :n], oc.v[:, :, :, :n])
+        print(f"{cfg.name} t={t} refresh={ref.refreshed} n={n} in-band flips so far={flips}", flush=True)
+    return flips
+
+
+CASES = {
+    "tiny": (TINY, TINY.steps),
+    "llama8b_reduced": (LLAMA8B.scaled(batch=2, layers=4, prefill_len=1200, budget=120), 6),
+    "llama8b_split_step1": (LLAMA8B.scaled(batch=1, layers=2, prefill_len=6000, budget=600), 3),
+    "lazy_r4_min": (LLAMA8B_LAZY.scaled(batch=2, layers=3, prefill_len=800, budget=80), 10),
+    "lazy_r4_mean": (LLAMA8B_LAZY.scaled(batch=2, layers=3, prefill_len=800, budget=80, nonrefresh_init="mean"), 10),
+    "lazy_r8_min": (LLAMA8B_LAZY.scaled(batch=2, layers=3, prefill_len=800, budget=80, refresh_period=8), 12),
+    "scorefree_min": (SCOREFREE128K.scaled(batch=2, layers=3, prefill_len=3000, budget=300), 12),
+    "scorefree_mean": (SCOREFREE128K.scaled(batch=2, layers=3, prefill_len=3000, budget=300,
+                                            nonrefresh_init="mean"), 12),
+    "qwen_reduced": (QWEN.scaled(batch=3, layers=3, prefill_len=1000, budget=250), 5),
+    "qwen_split_step1": (QWEN.scaled(batch=1, layers=2, prefill_len=3000, budget=750), 3),
+    "under_budget": (TINY.scaled(prefill_len=40, budget=45), 8),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_evict_step_lockstep(name):
+    cfg, steps = CASES[name]
+    print(f"lockstep case {name}: {cfg}", flush=True)
+    flips = run_lockstep(cfg, steps)
+    print(f"{name}: in-band flips {flips}", flush=True)
+
+
+@pytest.mark.parametrize("rule", ["single", "cumulative"])
+def test_aggregation_rules(rule):
+    cfg = LLAMA8B.scaled(batch=1, layers=3, prefill_len=500, budget=50)
+    run_lockstep(cfg, 4, rule=rule)
