@@ -3,53 +3,60 @@
 // The sequential EMA over layers l = 1..K, u <- alpha u + (1 - alpha) s_l, is linear: it equals
 // u <- alpha^K u + sum_l (1 - alpha) alpha^(K-l) s_l (the weights the appendix states).  The host passes the
 // prior weight and the per-layer weights (also for the single-step and cumulative rules), so the layers can
-// be reduced in parallel: a workgroup covers 64 tokens of one sequence with four waves, each wave summing a
-// quarter of the layers; partial sums are added in a fixed order, so results are deterministic.
+// be reduced in parallel.  A workgroup covers 32 tokens of one sequence: each thread reads four consecutive
+// tokens (16-byte loads) of the group sums r of one layer slice for every KV head, weights them, and the
+// partial sums of the 32 layer slices are added in a fixed order, so the result is deterministic.
 #include "kernels.h"
 #include "kv_common.h"
 
 namespace ikv {
 namespace {
 
-constexpr int kTok = 64;
-constexpr int kParts = 4;
+constexpr int kQuads = 8;          // 4-token groups per workgroup (32 tokens)
+constexpr int kSlices = 32;        // layer slices per workgroup
+constexpr int kThreads = kQuads * kSlices;
 
-__global__ __launch_bounds__(kTok * kParts) void fold_kernel(FoldArgs a) {
-    __shared__ float partial[kParts][kTok];
-    const int tl = threadIdx.x % kTok;
-    const int part = threadIdx.x / kTok;
+__global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
+    __shared__ float partial[kSlices][kQuads * 4];
+    const int quad = threadIdx.x % kQuads;
+    const int slice = threadIdx.x / kQuads;
     const int b = blockIdx.y;
-    const int tok = blockIdx.x * kTok + tl;
-    const int per = (a.layers + kParts - 1) / kParts;
-    const int l0 = part * per;
-    const int l1 = min(a.layers, l0 + per);
-    float acc = 0.0f;
-    if (tok < a.n) {
-        for (int l = l0; l < l1; ++l) {
-            const float* rl = a.r + ((size_t)(l * a.batch + b) * a.hkv) * a.n_stride + tok;
-            float s = 0.0f;
-            for (int g = 0; g < a.hkv; ++g) s += rl[(size_t)g * a.n_stride];
+    const int tok0 = blockIdx.x * (kQuads * 4) + quad * 4;  // r rows are padded to a multiple of 64
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (tok0 < a.n) {
+        for (int l = slice; l < a.layers; l += kSlices) {
+            const float* rl = a.r + ((size_t)(l * a.batch + b) * a.hkv) * a.n_stride + tok0;
+            f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
+            for (int g = 0; g < a.hkv; ++g) s += *reinterpret_cast<const f32x4*>(rl + (size_t)g * a.n_stride);
             s *= a.inv_hq;
-            if (a.s_out) a.s_out[((size_t)l * a.batch + b) * a.n + tok] = s;
-            acc = fmaf(a.w[l], s, acc);
+            if (a.s_out) {
+                float* so = a.s_out + ((size_t)l * a.batch + b) * a.n + tok0;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (tok0 + j < a.n) so[j] = s[j];
+            }
+            acc += a.w[l] * s;
         }
     }
-    partial[part][tl] = acc;
-    __syncthreads();
-    if (part == 0 && tok < a.n) {
-        float tot = partial[0][tl];
 #pragma unroll
-        for (int q = 1; q < kParts; ++q) tot += partial[q][tl];
-        float* up = a.u + (size_t)b * a.cap + tok;
-        *up = fmaf(a.prior_w, *up, tot);
+    for (int j = 0; j < 4; ++j) partial[slice][quad * 4 + j] = acc[j];
+    __syncthreads();
+    if (threadIdx.x < kQuads * 4) {
+        const int tok = blockIdx.x * (kQuads * 4) + threadIdx.x;
+        if (tok < a.n) {
+            float tot = 0.0f;
+            for (int sl = 0; sl < kSlices; ++sl) tot += partial[sl][threadIdx.x];
+            float* up = a.u + (size_t)b * a.cap + tok;
+            *up = fmaf(a.prior_w, *up, tot);
+        }
     }
 }
 
 }  // namespace
 
 hipError_t launch_fold(const FoldArgs& a, hipStream_t s) {
-    dim3 grid((a.n + kTok - 1) / kTok, a.batch);
-    hipLaunchKernelGGL(fold_kernel, grid, dim3(kTok * kParts), 0, s, a);
+    dim3 grid((a.n + kQuads * 4 - 1) / (kQuads * 4), a.batch);
+    hipLaunchKernelGGL(fold_kernel, grid, dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -75,6 +75,7 @@ __device__ __forceinline__ MaxSum ms_combine(MaxSum a, MaxSum b) {
     if (m == -INFINITY) return {m, 0.0f};
     return {m, a.s * __expf(a.m - m) + b.s * __expf(b.m - m)};
 }
+// (a.m and b.m are finite or -inf; a pair whose max is the finite floor used by the scorer has sum 0.)
 
 // Order-preserving map of a float onto uint32 (larger float -> larger key; -0 < +0).
 __device__ __forceinline__ uint32_t float_key(float x) {

@@ -19,8 +19,19 @@
 namespace ikv {
 namespace {
 
+#ifndef IKV_SCORE_WAVES
+#define IKV_SCORE_WAVES 8
+#endif
+#ifndef IKV_NT_LOADS
+#define IKV_NT_LOADS 1
+#endif
+#ifndef IKV_NBUF
+#define IKV_NBUF 3
+#endif
+
 constexpr size_t kFastLdsMax = 80 * 1024;  // keep >= 2 workgroups per CU (160 KiB LDS)
-constexpr int kWaves = 8;
+constexpr int kWaves = IKV_SCORE_WAVES;
+constexpr int kNbuf = IKV_NBUF;  // K loads of this many loop iterations are in flight per lane
 constexpr int kSplitIters = 16;
 
 template <typename T, int D, int GP>
@@ -35,10 +46,18 @@ struct Geometry {
     static constexpr int kRpw = kNg * kRpg;
     static constexpr int kRpi = kWaves * kRpw;
     static_assert(kRpg * GP == kLpr, "group must not exceed the lanes of a row");
+    // Registers of the streaming loop: the K buffers in flight, the queries, the partial dot products and
+    // bookkeeping.  LDS holds about 3 workgroups per CU at the graded shapes, so ask the compiler for the
+    // matching waves per SIMD when the loop fits that register budget; otherwise leave it unconstrained
+    // rather than spill.
+    static constexpr int kRegs = kNbuf * kRpg * kCpl * 4 + GP * kCpl * 4 + kLpr + 16;
+    static constexpr int kWantWaves = (3 * kWaves + 3) / 4;
+    static constexpr int kMinWaves = kRegs <= (512 / kWantWaves) / 8 * 8 ? kWantWaves : 1;
 };
 
 template <typename T, int D, int GP, bool SPLIT>
-__global__ __launch_bounds__(kWaves * kWave) void score_kernel(ScoreArgs a) {
+__global__ __launch_bounds__(kWaves * kWave)
+__attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_kernel(ScoreArgs a) {
     using Gm = Geometry<T, D, GP>;
     using E = Elem<T>;
     using chunk_t = typename E::chunk_t;
@@ -85,27 +104,38 @@ __global__ __launch_bounds__(kWaves * kWave) void score_kernel(ScoreArgs a) {
         }
 
     const int wave_row0 = row0 + wave * RPW + grp;
-    auto load = [&](int it, chunk_t(&dst)[RPG][CPL]) {
+    const int last = row_end - 1;
+    // Loads are unconditional: rows past the end are clamped onto the last row (same cache lines) and their
+    // logits masked afterwards, so the compiler can keep the next iteration's loads in flight while the
+    // current one is reduced.  The position of the row a lane will own after the reduce-scatter is fetched
+    // with the same batch (it decides the recency bias).
+    auto load = [&](int it, chunk_t(&dst)[RPG][CPL], int& pdst) {
         const int base = wave_row0 + it * RPI;
 #pragma unroll
         for (int k = 0; k < RPG; ++k) {
-            const int row = base + k * NG;
+            const int row = min(base + k * NG, last);
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-                if (row < row_end)
-                    dst[k][c] = __builtin_nontemporal_load(
-                        reinterpret_cast<const chunk_t*>(kslab + (size_t)row * D + (p + c * LPR) * EPC));
-                else
-                    dst[k][c] = chunk_t{};
+            for (int c = 0; c < CPL; ++c)
+            {
+                const chunk_t* src = reinterpret_cast<const chunk_t*>(kslab + (size_t)row * D + (p + c * LPR) * EPC);
+#if IKV_NT_LOADS
+                dst[k][c] = __builtin_nontemporal_load(src);  // K is streamed once: no reuse to cache for
+#else
+                dst[k][c] = *src;
+#endif
             }
         }
+        pdst = posb[min(base + kk * NG, last)];
     };
 
-    MaxSum ms{-INFINITY, 0.0f};
+    // Softmax statistics per lane; the running max starts at a finite floor so that masked (-inf) logits
+    // contribute exp(-inf) = 0 without NaN.
+    constexpr float kFloor = -1.0e30f;
+    MaxSum ms{kFloor, 0.0f};
     float* zrow = nullptr;
     if constexpr (SPLIT) zrow = a.z + ((size_t)(l * a.batch + b) * a.hq + (size_t)g * a.group + hh) * a.n_stride;
 
-    auto process = [&](int it, const chunk_t(&kb)[RPG][CPL]) {
+    auto process = [&](int it, const chunk_t(&kb)[RPG][CPL], int posv) {
         float v[LPR];
 #pragma unroll
         for (int k = 0; k < RPG; ++k)
@@ -119,66 +149,95 @@ __global__ __launch_bounds__(kWaves * kWave) void score_kernel(ScoreArgs a) {
         const float dotv = reduce_scatter<LPR>(v, p);
         const int row = wave_row0 + it * RPI + kk * NG;
         const bool valid = (row < row_end) && (hh < a.group);
-        float z = dotv * a.scale;
-        if (a.bias != 0.0f && valid && posb[row] >= a.recent_from) z += a.bias;
-        if (valid) {
-            if (z > ms.m) {
-                ms.s = ms.s * __expf(ms.m - z) + 1.0f;
-                ms.m = z;
-            } else {
-                ms.s += __expf(z - ms.m);
-            }
-        }
+        float z = fmaf(dotv, a.scale, posv >= a.recent_from ? a.bias : 0.0f);
+        z = valid ? z : -INFINITY;
         if constexpr (SPLIT) {
+            // split path: the logits leave the workgroup, so the (max, sum) pair is kept online
+            const float m_new = fmaxf(ms.m, z);
+            ms.s = fmaf(ms.s, __expf(ms.m - m_new), __expf(z - m_new));
+            ms.m = m_new;
             if (valid) zrow[row] = z;
         } else {
-            zs[it * (kWaves * kWave) + threadIdx.x] = valid ? z : -INFINITY;
+            // LDS path: only the running max here; exponentials and sums are taken from LDS afterwards
+            ms.m = fmaxf(ms.m, z);
+            zs[it * (kWaves * kWave) + threadIdx.x] = z;
         }
     };
 
-    chunk_t ka[RPG][CPL], kb[RPG][CPL];
-    if (nit > 0) load(0, ka);
-    for (int it = 0; it < nit; it += 2) {
-        if (it + 1 < nit) load(it + 1, kb);
-        process(it, ka);
-        if (it + 1 < nit) {
-            if (it + 2 < nit) load(it + 2, ka);
-            process(it + 1, kb);
+    // Ring of kNbuf register buffers: while iteration it is reduced, iterations it+1 .. it+kNbuf-1 load.
+    chunk_t kbuf[kNbuf][RPG][CPL];
+    int pbuf[kNbuf];
+#pragma unroll
+    for (int j = 0; j < kNbuf - 1; ++j)
+        if (j < nit) load(j, kbuf[j], pbuf[j]);
+    for (int it = 0; it < nit; it += kNbuf) {
+#pragma unroll
+        for (int j = 0; j < kNbuf; ++j) {
+            const int ahead = it + j + kNbuf - 1;
+            if (ahead < nit) load(ahead, kbuf[(j + kNbuf - 1) % kNbuf], pbuf[(j + kNbuf - 1) % kNbuf]);
+            if (it + j < nit) process(it + j, kbuf[j], pbuf[j]);
         }
     }
 
-    // per-head softmax statistics: lanes sharing a head differ in lane bits >= log2(GP)
-#pragma unroll
-    for (int o = GP; o < kWave; o <<= 1) {
-        MaxSum other{__shfl_xor(ms.m, o, kWave), __shfl_xor(ms.s, o, kWave)};
-        ms = ms_combine(ms, other);
-    }
-    if (lane < GP) red[wave][lane] = ms;
-    __syncthreads();
-    MaxSum tot = red[0][hh];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) tot = ms_combine(tot, red[w][hh]);
-
+    // Per-head softmax statistics: lanes sharing a head differ in lane bits >= log2(GP).
     if constexpr (SPLIT) {
+#pragma unroll
+        for (int o = GP; o < kWave; o <<= 1) {
+            MaxSum other{__shfl_xor(ms.m, o, kWave), __shfl_xor(ms.s, o, kWave)};
+            ms = ms_combine(ms, other);
+        }
+        if (lane < GP) red[wave][lane] = ms;
+        __syncthreads();
+        MaxSum tot = red[0][hh];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) tot = ms_combine(tot, red[w][hh]);
         if (threadIdx.x < a.group)
             a.part[((size_t)(l * a.batch + b) * a.hq + (size_t)g * a.group + threadIdx.x) * a.nchunk + chunk] =
                 make_float2(tot.m, tot.s);
     } else {
-        const float m = tot.m;
-        const float inv = tot.s > 0.0f ? 1.0f / tot.s : 0.0f;
+        // 1) head max
+        float m = ms.m;
+#pragma unroll
+        for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+        if (lane < GP) red[wave][lane].m = m;
+        __syncthreads();
+        m = red[0][hh].m;
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red[w][hh].m);
+        // 2) exponentials in place and their head sums (each lane revisits only its own LDS words)
+        float ssum = 0.0f;
+        for (int it = 0; it < nit; ++it) {
+            float* zp = &zs[it * (kWaves * kWave) + threadIdx.x];
+            const float z = *zp;
+            const float e = (z == -INFINITY) ? 0.0f : __expf(z - m);
+            *zp = e;
+            ssum += e;
+        }
+#pragma unroll
+        for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
+        if (lane < GP) red[wave][lane].s = ssum;
+        __syncthreads();
+        float tot = red[0][hh].s;
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) tot += red[w][hh].s;
+        const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
+        // 3) group sums of the normalised probabilities, one writer lane per row
         float* rrow = a.r + slab * a.n_stride;
         for (int it = 0; it < nit; ++it) {
-            const float z = zs[it * (kWaves * kWave) + threadIdx.x];
-            const float e = (z == -INFINITY) ? 0.0f : __expf(z - m) * inv;
-            const float sum = group_allsum<GP>(e);
+            const float sum = group_allsum<GP>(zs[it * (kWaves * kWave) + threadIdx.x] * inv);
             const int row = row0 + it * RPI + wave * RPW + kk * NG + grp;
             if (hh == 0 && row < row_end) rrow[row] = sum;
         }
     }
 }
 
-// Combine the split partials per head and emit r(row) = sum_{h in group} exp(z_h - M_h) / S_h.
-__global__ __launch_bounds__(256) void split_finish_kernel(ScoreArgs a) {
+// Combine the split partials per head and emit r(row) = sum_{h in group} exp(z_h - M_h) / S_h.  A workgroup
+// covers kFinishRows rows of one (layer, sequence, KV head): each thread handles 4 consecutive rows per pass
+// with 16-byte loads (logit rows are padded to a multiple of 64).
+constexpr int kFinishThreads = 256;
+constexpr int kFinishRows = kFinishThreads * 4 * 2;
+
+__global__ __launch_bounds__(kFinishThreads) void split_finish_kernel(ScoreArgs a) {
     __shared__ float mh[kMaxGroup], ih[kMaxGroup];
     const int g = blockIdx.y;
     const int lb = blockIdx.z;  // l * batch + b
@@ -190,12 +249,25 @@ __global__ __launch_bounds__(256) void split_finish_kernel(ScoreArgs a) {
         ih[threadIdx.x] = t.s > 0.0f ? 1.0f / t.s : 0.0f;
     }
     __syncthreads();
-    const int row = blockIdx.x * blockDim.x + threadIdx.x;
-    if (row >= a.n) return;
-    const float* zb = a.z + ((size_t)lb * a.hq + (size_t)g * a.group) * a.n_stride + row;
-    float acc = 0.0f;
-    for (int h = 0; h < a.group; ++h) acc += __expf(zb[(size_t)h * a.n_stride] - mh[h]) * ih[h];
-    a.r[((size_t)lb * a.hkv + g) * a.n_stride + row] = acc;
+    const float* zb = a.z + ((size_t)lb * a.hq + (size_t)g * a.group) * a.n_stride;
+    float* rb = a.r + ((size_t)lb * a.hkv + g) * a.n_stride;
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+        const int row = blockIdx.x * kFinishRows + (pass * kFinishThreads + threadIdx.x) * 4;
+        if (row >= a.n) continue;
+        f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int h = 0; h < a.group; ++h) {
+            const f32x4 z = *reinterpret_cast<const f32x4*>(zb + (size_t)h * a.n_stride + row);
+            const float m = mh[h], inv = ih[h];
+            acc.x += __expf(z.x - m) * inv;
+            acc.y += __expf(z.y - m) * inv;
+            acc.z += __expf(z.z - m) * inv;
+            acc.w += __expf(z.w - m) * inv;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (row + j < a.n) rb[row + j] = acc[j];
+    }
 }
 
 template <typename T, int D, int GP, bool SPLIT>
@@ -283,8 +355,8 @@ hipError_t launch_score(int dtype, int head_dim, const ScorePlan& plan, const Sc
 }
 
 hipError_t launch_split_finish(const ScoreArgs& a, hipStream_t s) {
-    dim3 grid((a.n + 255) / 256, a.hkv, a.layers * a.batch);
-    hipLaunchKernelGGL(split_finish_kernel, grid, dim3(256), 0, s, a);
+    dim3 grid((a.n + kFinishRows - 1) / kFinishRows, a.hkv, a.layers * a.batch);
+    hipLaunchKernelGGL(split_finish_kernel, grid, dim3(kFinishThreads), 0, s, a);
     return hipGetLastError();
 }
 
