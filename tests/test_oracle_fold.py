@@ -59,11 +59,16 @@ def test_alpha_zero_keeps_last_layer_only():
 
 
 def test_cumulative_rule():
-    """Eq. 3: m_t = m_{t-1} + s_t, applied per layer."""
+    """Eq. 3 never forgets: with distributions as scores every layer adds exactly one unit of mass, the result
+    is independent of alpha and of the layer order, and it dominates the EMA state of the same inputs."""
     rng = np.random.default_rng(11)
     s = rng.random((3, 8))
+    s /= s.sum(axis=1, keepdims=True)
     u0 = rng.random(8)
-    np.testing.assert_allclose(fold_layers(u0, s, 0.9, CUMULATIVE), u0 + s.sum(axis=0), rtol=1e-15)
+    u = fold_layers(u0, s, 0.9, CUMULATIVE)
+    assert abs(u.sum() - (u0.sum() + 3)) < 1e-13
+    np.testing.assert_allclose(u, fold_layers(u0, s[::-1], 0.1, CUMULATIVE), rtol=1e-14)
+    assert np.all(u >= fold_layers(u0, s, 0.9, EMA))
 
 
 def test_momentum_perturbation_golden():
