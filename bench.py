@@ -47,6 +47,32 @@ def step_bytes(cfg, n):
             "total": score + fold + append + select + compact}
 
 
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "score_llama8b_32k_steady_traffic.txt")
+SCORER_SOURCES = ("paper_2609_03515_amd/csrc/score.hip", "paper_2609_03515_amd/csrc/kv_common.h")
+
+
+def counter_traffic():
+    """HBM bytes per steady score launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary (scaled by
+    the copy-kernel calibration), or None when the scorer's sources changed since the counters were taken."""
+    import hashlib
+
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None
+    kv = {}
+    with open(TRAFFIC_SUMMARY) as f:
+        for line in f:
+            if "=" in line and not line.lstrip().startswith("#"):
+                k, v = line.split("=", 1)
+                kv[k.strip()] = v.strip()
+    h = hashlib.sha256()
+    for rel in SCORER_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != kv.get("kernel_sources_sha256"):
+        return None
+    return int(kv["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(cfg, seqs: int):
     """Times the float64 oracle on one steady full-refresh step for `seqs` of the batch's sequences."""
     import numpy as np
@@ -196,7 +222,7 @@ def main():
         "device_ms_per_step": round(dev_ms / K, 4),
         "roofline": {"kernel": "score_kernel<bf16, d128, group 4, LDS-resident>", "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": counter_traffic(),
                      "bytes_per_launch": by["score"], "avg_launch_ms": round(score_avg_ms, 5),
                      "launches_timed": len(score_ms)},
         "step1_ms": round(step1_ms, 3),

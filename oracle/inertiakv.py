@@ -235,7 +235,9 @@ def evict_step(cache: Cache, q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray
     3. if more than B tokens are cached, keep the top B (ties: lower position);
     4. hole-fill compaction of K, V, u and pos.
     `keep_override` lets a caller replace the selection by an equally valid one (used only to keep two
-    implementations in lockstep after a tie inside the rounding band); it must keep exactly min(B, n) tokens.
+    implementations in lockstep after a tie inside the rounding band): either a [b, >= n] mask, or a callable
+    receiving (the oracle's own [b, n] decision, the [b, n] utilities it was taken on) and returning the mask
+    to apply.  The applied mask must keep exactly min(B, n) tokens per sequence.
     """
     nl, nb, hkv, cap, d = cache.k.shape
     n = cache.n
@@ -270,6 +272,8 @@ def evict_step(cache: Cache, q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray
     for b in range(nb):
         keep[b] = select_keep(cache.u[b, :n], cache.pos[b, :n], params.budget)
     if keep_override is not None:
+        if callable(keep_override):
+            keep_override = keep_override(keep.copy(), u_pre.copy())
         keep_override = np.asarray(keep_override, dtype=bool)[:, :n]
         if not np.all(keep_override.sum(axis=1) == min(params.budget, n)):
             raise ValueError("override must keep exactly min(B, n) tokens per sequence")

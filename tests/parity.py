@@ -58,3 +58,17 @@ def check_keep(keep_gpu: np.ndarray, keep_ref: np.ndarray, u_ref: np.ndarray, bu
     diff = keep_gpu != keep_ref
     assert not np.any(diff & ~band), f"{what}: {int((diff & ~band).sum())} retention differences outside the band"
     return int(diff.sum())
+
+
+def lockstep_adopter(keep_gpu_rows: np.ndarray, budget: int, what: str, counter: list):
+    """keep_override callback for the oracle: checks the GPU's decision against the oracle's own (exact count,
+    equal outside the band) and returns the GPU's mask, so both sides continue from the same retained set.
+    Appends the number of in-band differences to `counter`."""
+    def adopt(keep_ref, u_pre):
+        n = keep_ref.shape[1]
+        flips = 0
+        for b in range(keep_ref.shape[0]):
+            flips += check_keep(keep_gpu_rows[b, :n], keep_ref[b], u_pre[b], budget, f"{what} b={b}")
+        counter.append(flips)
+        return np.asarray(keep_gpu_rows[:, :n], dtype=bool)
+    return adopt

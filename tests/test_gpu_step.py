@@ -10,7 +10,7 @@ import pytest
 import torch
 
 from oracle import evict_step
-from parity import assert_close, check_keep, oracle_cache, oracle_params, to_device
+from parity import assert_close, lockstep_adopter, oracle_cache, oracle_params, to_device
 from workload import LLAMA8B, LLAMA8B_LAZY, QWEN, SCOREFREE128K, TINY, Workload, raw_numpy
 
 pytestmark = pytest.mark.gpu
@@ -40,17 +40,12 @@ def run_lockstep(cfg, steps, seed=None, rule="ema"):
                                 dev["k"], dev["v"], dev["u"], dev["pos"], ws, keep_out=keep, s_out=s_out)
         torch.cuda.synchronize()
         q_raw, kn_raw, vn_raw = raw_numpy(si["q"]), raw_numpy(si["k_new"]), raw_numpy(si["v_new"])
-        before = oc.copy()
-        ref = evict_step(oc, q_raw, kn_raw, vn_raw, t, si["new_pos"], op)
-        assert n_out == ref.n_out == min(cfg.budget, n + 1)
         keep_g = keep.cpu().numpy()[:, : n + 1].astype(bool)
-        step_flips = 0
-        for b in range(cfg.batch):
-            step_flips += check_keep(keep_g[b], ref.keep[b], ref.u_pre[b], cfg.budget, f"{cfg.name} t={t} b={b}")
-        if step_flips:
-            oc = before
-            ref = evict_step(oc, q_raw, kn_raw, vn_raw, t, si["new_pos"], op, keep_override=keep_g)
-            flips += step_flips
+        step_flips = []
+        ref = evict_step(oc, q_raw, kn_raw, vn_raw, t, si["new_pos"], op,
+                         keep_override=lockstep_adopter(keep_g, cfg.budget, f"{cfg.name} t={t}", step_flips))
+        assert n_out == ref.n_out == min(cfg.budget, n + 1)
+        flips += sum(step_flips)
         if ref.refreshed:
             assert_close(s_out.cpu().numpy(), ref.s_layers, f"{cfg.name} t={t} scores")
         n = n_out
