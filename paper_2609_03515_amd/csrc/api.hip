@@ -294,6 +294,7 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
     ap.n_in = n_in;
     ap.new_pos = new_pos;
     ap.init_mode = refresh ? 0 : (p.nonrefresh_init == KV_INIT_MEAN ? 1 : 2);
+
     record(trace, 0, true, st);
     rc = hip_status(launch_append(ap, st));
     record(trace, 0, false, st);

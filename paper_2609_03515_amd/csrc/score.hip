@@ -8,11 +8,12 @@
 // d = 128 bf16 / d = 64 f32, 8 for d = 64 bf16); a wave load instruction therefore covers 64/LPR consecutive
 // rows, 1 KiB contiguous.  Each lane handles RPG = LPR / GP rows per iteration (GP = group size rounded up to
 // a power of two), producing RPG * GP = LPR partial dot products; a DPP reduce-scatter over the group leaves
-// each lane with one complete (row, head) logit.  Per-lane online max/sum gives the softmax statistics.
+// each lane with one complete (row, head) logit.
 //
-// Fast path (whole slab fits in LDS): logits stay in LDS; after the per-head (max, sum) reduction the kernel
-// writes r(row) = sum over the group's heads of exp(z - max) / sum.  Split path: several workgroups per slab
-// write their logits and per-head partial (max, sum); a finish kernel combines them.
+// LDS path (a whole slab's logits fit in LDS): one workgroup per slab keeps its logits in LDS; after the
+// per-head (max, sum) reduction it writes r(row) = sum over the group's heads of exp(z - max) / sum.  Split
+// path (long first steps): several workgroups per slab write their logits and per-head partial (max, sum);
+// a finish kernel combines them.
 #include "kernels.h"
 #include "kv_common.h"
 
@@ -26,13 +27,14 @@ namespace {
 #define IKV_NT_LOADS 1
 #endif
 #ifndef IKV_NBUF
-#define IKV_NBUF 3
+#define IKV_NBUF 0
 #endif
 
 constexpr size_t kFastLdsMax = 80 * 1024;  // keep >= 2 workgroups per CU (160 KiB LDS)
 constexpr int kWaves = IKV_SCORE_WAVES;
-constexpr int kNbuf = IKV_NBUF;  // K loads of this many loop iterations are in flight per lane
+constexpr int kThreads = kWaves * kWave;
 constexpr int kSplitIters = 16;
+constexpr float kFloor = -1.0e30f;  // finite start of running maxima: exp(-inf - floor) = 0, no NaN
 
 template <typename T, int D, int GP>
 struct Geometry {
@@ -46,78 +48,72 @@ struct Geometry {
     static constexpr int kRpw = kNg * kRpg;
     static constexpr int kRpi = kWaves * kRpw;
     static_assert(kRpg * GP == kLpr, "group must not exceed the lanes of a row");
+    // K loads of this many loop iterations are in flight per lane: measured best 4 when a lane loads four
+    // 16-byte chunks per iteration, 3 for wider groups (more arithmetic per byte); 2 when a lane loads more
+    // than four chunks per iteration, which would otherwise cost too many registers.
+    static constexpr int kNbuf = IKV_NBUF > 0 ? IKV_NBUF : (kRpg * kCpl > 4 ? 2 : (GP <= 4 ? 4 : 3));
     // Registers of the streaming loop: the K buffers in flight, the queries, the partial dot products and
     // bookkeeping.  LDS holds about 3 workgroups per CU at the graded shapes, so ask the compiler for the
     // matching waves per SIMD when the loop fits that register budget; otherwise leave it unconstrained
     // rather than spill.
     static constexpr int kRegs = kNbuf * kRpg * kCpl * 4 + GP * kCpl * 4 + kLpr + 16;
     static constexpr int kWantWaves = (3 * kWaves + 3) / 4;
+#ifdef IKV_MIN_WAVES
+    static constexpr int kMinWaves = IKV_MIN_WAVES;
+#else
     static constexpr int kMinWaves = kRegs <= (512 / kWantWaves) / 8 * 8 ? kWantWaves : 1;
+#endif
 };
 
-template <typename T, int D, int GP, bool SPLIT>
-__global__ __launch_bounds__(kWaves * kWave)
-__attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_kernel(ScoreArgs a) {
+// Per-lane streaming machinery shared by both paths.
+template <typename T, int D, int GP>
+struct Lane {
     using Gm = Geometry<T, D, GP>;
     using E = Elem<T>;
     using chunk_t = typename E::chunk_t;
-    constexpr int LPR = Gm::kLpr, CPL = Gm::kCpl, NG = Gm::kNg, RPG = Gm::kRpg, RPW = Gm::kRpw;
-    constexpr int RPI = Gm::kRpi, EPC = Gm::kEpc;
+    static constexpr int LPR = Gm::kLpr, CPL = Gm::kCpl, NG = Gm::kNg, RPG = Gm::kRpg, RPW = Gm::kRpw;
+    static constexpr int RPI = Gm::kRpi, EPC = Gm::kEpc;
 
-    extern __shared__ float zs[];
-    __shared__ MaxSum red[kWaves][GP];
+    int lane, wave, grp, p, hh, kk;
 
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
-    const int grp = lane / LPR, p = lane % LPR;
-    const int hh = p % GP, kk = p / GP;  // (head, row slot) this lane owns after the reduce-scatter
-
-    int bid = blockIdx.x;
-    int chunk = 0;
-    if constexpr (SPLIT) {
-        chunk = bid % a.nchunk;
-        bid /= a.nchunk;
+    __device__ Lane() {
+        lane = threadIdx.x & (kWave - 1);
+        wave = threadIdx.x / kWave;
+        grp = lane / LPR;
+        p = lane % LPR;
+        hh = p % GP;  // head owned after the reduce-scatter
+        kk = p / GP;  // row slot owned after the reduce-scatter
     }
-    const int g = bid % a.hkv;
-    bid /= a.hkv;
-    const int b = bid % a.batch;
-    const int l = bid / a.batch;
 
-    const int row0 = chunk * a.chunk_rows;
-    const int row_end = min(a.n, row0 + a.chunk_rows);
-    const int nit = row_end > row0 ? (row_end - row0 + RPI - 1) / RPI : 0;
+    // Row of iteration `it` owned by this lane after the reduce-scatter.
+    __device__ int owned_row(int row0, int it) const { return row0 + it * RPI + wave * RPW + kk * NG + grp; }
 
-    const size_t slab = (size_t)(l * a.batch + b) * a.hkv + g;
-    const T* kslab = static_cast<const T*>(a.k) + slab * a.cap * D;
-    const T* qg = static_cast<const T*>(a.q) + ((size_t)(l * a.batch + b) * a.hq + (size_t)g * a.group) * D;
-    const int* posb = a.pos + (size_t)b * a.cap;
-
-    chunk_t qv[GP][CPL];
+    __device__ void load_q(const ScoreArgs& a, size_t lb, int g, chunk_t (&qv)[GP][CPL]) const {
+        const T* qg = static_cast<const T*>(a.q) + (lb * a.hq + (size_t)g * a.group) * D;
 #pragma unroll
-    for (int h = 0; h < GP; ++h)
+        for (int h = 0; h < GP; ++h)
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            if (h < a.group)
-                qv[h][c] = *reinterpret_cast<const chunk_t*>(qg + h * D + (p + c * LPR) * EPC);
-            else
-                qv[h][c] = chunk_t{};
-        }
+            for (int c = 0; c < CPL; ++c) {
+                if (h < a.group)
+                    qv[h][c] = *reinterpret_cast<const chunk_t*>(qg + h * D + (p + c * LPR) * EPC);
+                else
+                    qv[h][c] = chunk_t{};
+            }
+    }
 
-    const int wave_row0 = row0 + wave * RPW + grp;
-    const int last = row_end - 1;
     // Loads are unconditional: rows past the end are clamped onto the last row (same cache lines) and their
-    // logits masked afterwards, so the compiler can keep the next iteration's loads in flight while the
-    // current one is reduced.  The position of the row a lane will own after the reduce-scatter is fetched
-    // with the same batch (it decides the recency bias).
-    auto load = [&](int it, chunk_t(&dst)[RPG][CPL], int& pdst) {
-        const int base = wave_row0 + it * RPI;
+    // logits masked afterwards, so the compiler keeps the next iterations' loads in flight while the current
+    // one is reduced.  The position of the row this lane will own is fetched with the same batch (it decides
+    // the recency bias).
+    __device__ void load(const T* kslab, const int* posb, int row0, int last, int it, chunk_t (&dst)[RPG][CPL],
+                         int& pdst) const {
+        const int base = row0 + it * RPI + wave * RPW + grp;
 #pragma unroll
         for (int k = 0; k < RPG; ++k) {
-            const int row = min(base + k * NG, last);
+            const T* rp = kslab + (size_t)min(base + k * NG, last) * D;
 #pragma unroll
-            for (int c = 0; c < CPL; ++c)
-            {
-                const chunk_t* src = reinterpret_cast<const chunk_t*>(kslab + (size_t)row * D + (p + c * LPR) * EPC);
+            for (int c = 0; c < CPL; ++c) {
+                const chunk_t* src = reinterpret_cast<const chunk_t*>(rp + (p + c * LPR) * EPC);
 #if IKV_NT_LOADS
                 dst[k][c] = __builtin_nontemporal_load(src);  // K is streamed once: no reuse to cache for
 #else
@@ -126,16 +122,12 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_k
             }
         }
         pdst = posb[min(base + kk * NG, last)];
-    };
+    }
 
-    // Softmax statistics per lane; the running max starts at a finite floor so that masked (-inf) logits
-    // contribute exp(-inf) = 0 without NaN.
-    constexpr float kFloor = -1.0e30f;
-    MaxSum ms{kFloor, 0.0f};
-    float* zrow = nullptr;
-    if constexpr (SPLIT) zrow = a.z + ((size_t)(l * a.batch + b) * a.hq + (size_t)g * a.group + hh) * a.n_stride;
-
-    auto process = [&](int it, const chunk_t(&kb)[RPG][CPL], int posv) {
+    // Logit of the (row, head) this lane owns for one iteration; -inf when masked (a padded head, or a row
+    // past the end of the range).
+    __device__ float logit(const ScoreArgs& a, const chunk_t (&kb)[RPG][CPL], const chunk_t (&qv)[GP][CPL],
+                           int posv, int row, int row_end) const {
         float v[LPR];
 #pragma unroll
         for (int k = 0; k < RPG; ++k)
@@ -147,88 +139,184 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_k
                 v[k * GP + h] = acc;
             }
         const float dotv = reduce_scatter<LPR>(v, p);
-        const int row = wave_row0 + it * RPI + kk * NG;
-        const bool valid = (row < row_end) && (hh < a.group);
-        float z = fmaf(dotv, a.scale, posv >= a.recent_from ? a.bias : 0.0f);
-        z = valid ? z : -INFINITY;
-        if constexpr (SPLIT) {
-            // split path: the logits leave the workgroup, so the (max, sum) pair is kept online
-            const float m_new = fmaxf(ms.m, z);
-            ms.s = fmaf(ms.s, __expf(ms.m - m_new), __expf(z - m_new));
-            ms.m = m_new;
-            if (valid) zrow[row] = z;
-        } else {
-            // LDS path: only the running max here; exponentials and sums are taken from LDS afterwards
-            ms.m = fmaxf(ms.m, z);
-            zs[it * (kWaves * kWave) + threadIdx.x] = z;
-        }
-    };
+        const float z = fmaf(dotv, a.scale, posv >= a.recent_from ? a.bias : 0.0f);
+        return (row < row_end && hh < a.group) ? z : -INFINITY;
+    }
+};
 
-    // Ring of kNbuf register buffers: while iteration it is reduced, iterations it+1 .. it+kNbuf-1 load.
+#ifndef IKV_EPI_UNROLL
+#define IKV_EPI_UNROLL 8
+#endif
+constexpr int kEpi = IKV_EPI_UNROLL;  // epilogue LDS reads kept in flight per lane
+
+template <typename T, int D, int GP>
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_lds_kernel(ScoreArgs a) {
+    using L = Lane<T, D, GP>;
+    using chunk_t = typename L::chunk_t;
+    constexpr int RPG = L::RPG, CPL = L::CPL, RPI = L::RPI;
+    constexpr int kNbuf = Geometry<T, D, GP>::kNbuf;
+
+    extern __shared__ float zs[];
+    __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
+
+    const L ln;
+    const int s = blockIdx.x;
+    const int g = s % a.hkv;
+    const int b = (s / a.hkv) % a.batch;
+    const int l = s / (a.hkv * a.batch);
+    const size_t slab = (size_t)s;
+    const int n = a.n, last = n - 1;
+    const int nit = (n + RPI - 1) / RPI;
+    const T* kslab = static_cast<const T*>(a.k) + slab * a.cap * D;
+    const int* posb = a.pos + (size_t)b * a.cap;
+
+    chunk_t qv[GP][CPL];
     chunk_t kbuf[kNbuf][RPG][CPL];
     int pbuf[kNbuf];
+    ln.load_q(a, (size_t)l * a.batch + b, g, qv);
 #pragma unroll
     for (int j = 0; j < kNbuf - 1; ++j)
-        if (j < nit) load(j, kbuf[j], pbuf[j]);
+        ln.load(kslab, posb, 0, last, j, kbuf[j], pbuf[j]);
+
+    // stream the slab: logits to LDS (each lane only ever touches its own words), running max per lane
+    float m = kFloor;
     for (int it = 0; it < nit; it += kNbuf) {
 #pragma unroll
         for (int j = 0; j < kNbuf; ++j) {
-            const int ahead = it + j + kNbuf - 1;
-            if (ahead < nit) load(ahead, kbuf[(j + kNbuf - 1) % kNbuf], pbuf[(j + kNbuf - 1) % kNbuf]);
-            if (it + j < nit) process(it + j, kbuf[j], pbuf[j]);
+            // unconditional (clamped) so every path issues the same loads and the wait before the reduction
+            // below covers only this iteration's buffer
+            ln.load(kslab, posb, 0, last, it + j + kNbuf - 1, kbuf[(j + kNbuf - 1) % kNbuf],
+                    pbuf[(j + kNbuf - 1) % kNbuf]);
+            if (it + j < nit) {
+                const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.owned_row(0, it + j), n);
+                m = fmaxf(m, z);
+                zs[(it + j) * kThreads + threadIdx.x] = z;
+            }
         }
     }
 
-    // Per-head softmax statistics: lanes sharing a head differ in lane bits >= log2(GP).
-    if constexpr (SPLIT) {
+    // epilogue: head max, exponentials and head sums, normalised group sums.  The LDS passes work on kEpi
+    // iterations at a time so their reads overlap instead of forming one long latency chain.
 #pragma unroll
-        for (int o = GP; o < kWave; o <<= 1) {
-            MaxSum other{__shfl_xor(ms.m, o, kWave), __shfl_xor(ms.s, o, kWave)};
-            ms = ms_combine(ms, other);
-        }
-        if (lane < GP) red[wave][lane] = ms;
-        __syncthreads();
-        MaxSum tot = red[0][hh];
+    for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+    if (ln.lane < GP) red_m[ln.wave][ln.lane] = m;
+    __syncthreads();
+    m = red_m[0][ln.hh];
 #pragma unroll
-        for (int w = 1; w < kWaves; ++w) tot = ms_combine(tot, red[w][hh]);
-        if (threadIdx.x < a.group)
-            a.part[((size_t)(l * a.batch + b) * a.hq + (size_t)g * a.group + threadIdx.x) * a.nchunk + chunk] =
-                make_float2(tot.m, tot.s);
-    } else {
-        // 1) head max
-        float m = ms.m;
+    for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][ln.hh]);
+    float* zl = zs + threadIdx.x;
+    auto expo = [&](float z) { return z == -INFINITY ? 0.0f : __expf(z - m); };
+    float ssum = 0.0f;
+    int it = 0;
+    for (; it + kEpi <= nit; it += kEpi) {
+        float e[kEpi];
 #pragma unroll
-        for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
-        if (lane < GP) red[wave][lane].m = m;
-        __syncthreads();
-        m = red[0][hh].m;
+        for (int u = 0; u < kEpi; ++u) e[u] = zl[(it + u) * kThreads];
 #pragma unroll
-        for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red[w][hh].m);
-        // 2) exponentials in place and their head sums (each lane revisits only its own LDS words)
-        float ssum = 0.0f;
-        for (int it = 0; it < nit; ++it) {
-            float* zp = &zs[it * (kWaves * kWave) + threadIdx.x];
-            const float z = *zp;
-            const float e = (z == -INFINITY) ? 0.0f : __expf(z - m);
-            *zp = e;
-            ssum += e;
-        }
-#pragma unroll
-        for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
-        if (lane < GP) red[wave][lane].s = ssum;
-        __syncthreads();
-        float tot = red[0][hh].s;
-#pragma unroll
-        for (int w = 1; w < kWaves; ++w) tot += red[w][hh].s;
-        const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
-        // 3) group sums of the normalised probabilities, one writer lane per row
-        float* rrow = a.r + slab * a.n_stride;
-        for (int it = 0; it < nit; ++it) {
-            const float sum = group_allsum<GP>(zs[it * (kWaves * kWave) + threadIdx.x] * inv);
-            const int row = row0 + it * RPI + wave * RPW + kk * NG + grp;
-            if (hh == 0 && row < row_end) rrow[row] = sum;
+        for (int u = 0; u < kEpi; ++u) {
+            e[u] = expo(e[u]);
+            ssum += e[u];
+            zl[(it + u) * kThreads] = e[u];
         }
     }
+    for (; it < nit; ++it) {
+        const float e = expo(zl[it * kThreads]);
+        ssum += e;
+        zl[it * kThreads] = e;
+    }
+#pragma unroll
+    for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
+    if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;
+    __syncthreads();
+    float tot = red_s[0][ln.hh];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) tot += red_s[w][ln.hh];
+    const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
+    float* rrow = a.r + slab * a.n_stride;
+    it = 0;
+    for (; it + kEpi <= nit; it += kEpi) {
+        float e[kEpi];
+#pragma unroll
+        for (int u = 0; u < kEpi; ++u) e[u] = zl[(it + u) * kThreads];
+#pragma unroll
+        for (int u = 0; u < kEpi; ++u) {
+            const float sum = group_allsum<GP>(e[u] * inv);
+            const int row = ln.owned_row(0, it + u);
+            if (ln.hh == 0 && row < n) rrow[row] = sum;
+        }
+    }
+    for (; it < nit; ++it) {
+        const float sum = group_allsum<GP>(zl[it * kThreads] * inv);
+        const int row = ln.owned_row(0, it);
+        if (ln.hh == 0 && row < n) rrow[row] = sum;
+    }
+}
+
+template <typename T, int D, int GP>
+__global__ __launch_bounds__(kThreads)
+__attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_split_kernel(ScoreArgs a) {
+    using L = Lane<T, D, GP>;
+    using chunk_t = typename L::chunk_t;
+    constexpr int RPG = L::RPG, CPL = L::CPL, RPI = L::RPI;
+    constexpr int kNbuf = Geometry<T, D, GP>::kNbuf;
+    __shared__ MaxSum red[kWaves][GP];
+
+    const L ln;
+    int bid = blockIdx.x;
+    const int chunk = bid % a.nchunk;
+    bid /= a.nchunk;
+    const int g = bid % a.hkv;
+    bid /= a.hkv;
+    const int b = bid % a.batch;
+    const int l = bid / a.batch;
+    const size_t slab = ((size_t)l * a.batch + b) * a.hkv + g;
+    const int row0 = chunk * a.chunk_rows;
+    const int row_end = min(a.n, row0 + a.chunk_rows);
+    const int last = row_end - 1;
+    const int nit = row_end > row0 ? (row_end - row0 + RPI - 1) / RPI : 0;
+    const T* kslab = static_cast<const T*>(a.k) + slab * a.cap * D;
+    const int* posb = a.pos + (size_t)b * a.cap;
+
+    chunk_t qv[GP][CPL];
+    chunk_t kbuf[kNbuf][RPG][CPL];
+    int pbuf[kNbuf];
+    ln.load_q(a, (size_t)l * a.batch + b, g, qv);
+#pragma unroll
+    for (int j = 0; j < kNbuf - 1; ++j)
+        ln.load(kslab, posb, row0, last, j, kbuf[j], pbuf[j]);
+
+    // the logits leave the workgroup, so the (max, sum) pair is kept online
+    MaxSum ms{kFloor, 0.0f};
+    float* zrow = a.z + (((size_t)l * a.batch + b) * a.hq + (size_t)g * a.group + ln.hh) * a.n_stride;
+    for (int it = 0; it < nit; it += kNbuf) {
+#pragma unroll
+        for (int j = 0; j < kNbuf; ++j) {
+            ln.load(kslab, posb, row0, last, it + j + kNbuf - 1, kbuf[(j + kNbuf - 1) % kNbuf],
+                    pbuf[(j + kNbuf - 1) % kNbuf]);
+            if (it + j < nit) {
+                const int row = ln.owned_row(row0, it + j);
+                const float z = ln.logit(a, kbuf[j], qv, pbuf[j], row, row_end);
+                const float m_new = fmaxf(ms.m, z);
+                ms.s = fmaf(ms.s, __expf(ms.m - m_new), __expf(z - m_new));
+                ms.m = m_new;
+                if (z != -INFINITY) zrow[row] = z;
+            }
+        }
+    }
+#pragma unroll
+    for (int o = GP; o < kWave; o <<= 1) {
+        MaxSum other{__shfl_xor(ms.m, o, kWave), __shfl_xor(ms.s, o, kWave)};
+        ms = ms_combine(ms, other);
+    }
+    if (ln.lane < GP) red[ln.wave][ln.lane] = ms;
+    __syncthreads();
+    MaxSum tot = red[0][ln.hh];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) tot = ms_combine(tot, red[w][ln.hh]);
+    if (threadIdx.x < a.group)
+        a.part[(((size_t)l * a.batch + b) * a.hq + (size_t)g * a.group + threadIdx.x) * a.nchunk + chunk] =
+            make_float2(tot.m, tot.s);
 }
 
 // Combine the split partials per head and emit r(row) = sum_{h in group} exp(z_h - M_h) / S_h.  A workgroup
@@ -270,10 +358,10 @@ __global__ __launch_bounds__(kFinishThreads) void split_finish_kernel(ScoreArgs 
     }
 }
 
-template <typename T, int D, int GP, bool SPLIT>
-hipError_t launch_one(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
-    auto kern = score_kernel<T, D, GP, SPLIT>;
-    if (!SPLIT && plan.lds_bytes > 64 * 1024) {
+template <typename T, int D, int GP>
+hipError_t launch_lds(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
+    auto kern = score_lds_kernel<T, D, GP>;
+    if (plan.lds_bytes > 64 * 1024) {
         static bool raised = false;  // idempotent attribute; a benign race between threads
         if (!raised) {
             hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -282,7 +370,7 @@ hipError_t launch_one(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) 
             raised = true;
         }
     }
-    hipLaunchKernelGGL(kern, dim3(plan.grid), dim3(kWaves * kWave), SPLIT ? 0 : plan.lds_bytes, s, a);
+    hipLaunchKernelGGL(kern, dim3(a.layers * a.batch * a.hkv), dim3(kThreads), plan.lds_bytes, s, a);
     return hipGetLastError();
 }
 
@@ -291,7 +379,9 @@ hipError_t launch_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
     if constexpr (Geometry<T, D, 1>::kLpr < GP) {
         return hipErrorInvalidValue;
     } else {
-        return plan.split ? launch_one<T, D, GP, true>(plan, a, s) : launch_one<T, D, GP, false>(plan, a, s);
+        if (!plan.split) return launch_lds<T, D, GP>(plan, a, s);
+        hipLaunchKernelGGL((score_split_kernel<T, D, GP>), dim3(plan.grid), dim3(kThreads), 0, s, a);
+        return hipGetLastError();
     }
 }
 
@@ -323,7 +413,7 @@ bool score_plan(int dtype, int head_dim, int group, int n, ScorePlan* plan) {
     plan->group_pad = gp;
     plan->waves = kWaves;
     plan->rows_per_iter = rpi;
-    const size_t lds = (size_t)nit * kWaves * kWave * sizeof(float);
+    const size_t lds = (size_t)nit * kThreads * sizeof(float);
     if (lds <= kFastLdsMax) {
         plan->split = false;
         plan->chunk_rows = nit * rpi;
