@@ -29,40 +29,55 @@ namespace {
 #ifndef IKV_NBUF
 #define IKV_NBUF 0
 #endif
+#ifndef IKV_LPR
+#define IKV_LPR 16
+#endif
 
 constexpr size_t kFastLdsMax = 80 * 1024;  // keep >= 2 workgroups per CU (160 KiB LDS)
 constexpr int kWaves = IKV_SCORE_WAVES;
 constexpr int kThreads = kWaves * kWave;
 constexpr int kSplitIters = 16;
 constexpr float kFloor = -1.0e30f;  // finite start of running maxima: exp(-inf - floor) = 0, no NaN
+constexpr int kNonTemporal = 2;     // buffer-load cache policy: K is streamed once, no reuse to cache for
+constexpr int kRsrcConfig = 0x00020000;  // raw (unformatted, stride 0) buffer resource, gfx9 family
+
+// Raw buffer resource over `bytes` bytes at `base` (reads at offsets >= bytes return zero).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kRsrcConfig);
+}
 
 template <typename T, int D, int GP>
 struct Geometry {
     using E = Elem<T>;
     static constexpr int kEpc = E::kPerChunk;
     static constexpr int kChunks = D / kEpc;
-    static constexpr int kLpr = kChunks >= 16 ? 16 : kChunks;
+    static constexpr int kLpr = kChunks >= IKV_LPR ? IKV_LPR : kChunks;
     static constexpr int kCpl = kChunks / kLpr;
     static constexpr int kNg = kWave / kLpr;
     static constexpr int kRpg = kLpr / GP;
     static constexpr int kRpw = kNg * kRpg;
     static constexpr int kRpi = kWaves * kRpw;
     static_assert(kRpg * GP == kLpr, "group must not exceed the lanes of a row");
-    // K loads of this many loop iterations are in flight per lane: measured best 4 when a lane loads four
-    // 16-byte chunks per iteration, 3 for wider groups (more arithmetic per byte); 2 when a lane loads more
-    // than four chunks per iteration, which would otherwise cost too many registers.
-    static constexpr int kNbuf = IKV_NBUF > 0 ? IKV_NBUF : (kRpg * kCpl > 4 ? 2 : (GP <= 4 ? 4 : 3));
+    // K loads of this many loop iterations are in flight per lane.  The LDS path claims its rows dynamically
+    // and measured best with 2 (more buffers cost occupancy without raising the stream rate).  The split path
+    // streams static chunks and measured best with 4 when a lane loads four 16-byte chunks per iteration, 3 for
+    // wider groups (more arithmetic per byte), 2 when a lane loads more than four chunks per iteration.
+    static constexpr int kNbufLds = IKV_NBUF > 0 ? IKV_NBUF : 2;
+    static constexpr int kNbufSplit = IKV_NBUF > 0 ? IKV_NBUF : (kRpg * kCpl > 4 ? 2 : (GP <= 4 ? 4 : 3));
     // Registers of the streaming loop: the K buffers in flight, the queries, the partial dot products and
     // bookkeeping.  LDS holds about 3 workgroups per CU at the graded shapes, so ask the compiler for the
     // matching waves per SIMD when the loop fits that register budget; otherwise leave it unconstrained
     // rather than spill.
-    static constexpr int kRegs = kNbuf * kRpg * kCpl * 4 + GP * kCpl * 4 + kLpr + 16;
     static constexpr int kWantWaves = (3 * kWaves + 3) / 4;
+    static constexpr int min_waves(int nbuf) {
 #ifdef IKV_MIN_WAVES
-    static constexpr int kMinWaves = IKV_MIN_WAVES;
+        return IKV_MIN_WAVES;
 #else
-    static constexpr int kMinWaves = kRegs <= (512 / kWantWaves) / 8 * 8 ? kWantWaves : 1;
+        return nbuf * kRpg * kCpl * 4 + GP * kCpl * 4 + kLpr + 16 <= (512 / kWantWaves) / 8 * 8 ? kWantWaves : 1;
 #endif
+    }
+    static constexpr int kMinWavesLds = min_waves(kNbufLds);
+    static constexpr int kMinWavesSplit = min_waves(kNbufSplit);
 };
 
 // Per-lane streaming machinery shared by both paths.
@@ -101,27 +116,39 @@ struct Lane {
             }
     }
 
-    // Loads are unconditional: rows past the end are clamped onto the last row (same cache lines) and their
-    // logits masked afterwards, so the compiler keeps the next iterations' loads in flight while the current
-    // one is reduced.  The position of the row this lane will own is fetched with the same batch (it decides
-    // the recency bias).
-    __device__ void load(const T* kslab, const int* posb, int row0, int last, int it, chunk_t (&dst)[RPG][CPL],
-                         int& pdst) const {
+    // K rows and positions are read with raw buffer loads over the range's rows: 32-bit lane offsets with
+    // immediate row/chunk offsets, and reads past the range return zero instead of needing a clamp (those
+    // logits are masked).  Loads are unconditional, so the compiler keeps the next iterations' loads in flight
+    // while the current one is reduced.  The position of the row this lane will own comes with the same batch
+    // (it decides the recency bias).
+    static constexpr int kRowBytes = D * (int)sizeof(T);
+    __device__ void load(__amdgpu_buffer_rsrc_t krs, __amdgpu_buffer_rsrc_t prs, int row0, int it,
+                         chunk_t (&dst)[RPG][CPL], int& pdst) const {
         const int base = row0 + it * RPI + wave * RPW + grp;
+        const int off = base * kRowBytes + p * 16;
 #pragma unroll
-        for (int k = 0; k < RPG; ++k) {
-            const T* rp = kslab + (size_t)min(base + k * NG, last) * D;
+        for (int k = 0; k < RPG; ++k)
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) {
-                const chunk_t* src = reinterpret_cast<const chunk_t*>(rp + (p + c * LPR) * EPC);
-#if IKV_NT_LOADS
-                dst[k][c] = __builtin_nontemporal_load(src);  // K is streamed once: no reuse to cache for
-#else
-                dst[k][c] = *src;
-#endif
-            }
-        }
-        pdst = posb[min(base + kk * NG, last)];
+            for (int c = 0; c < CPL; ++c)
+                dst[k][c] = __builtin_bit_cast(
+                    chunk_t, __builtin_amdgcn_raw_buffer_load_b128(krs, off + k * NG * kRowBytes + c * LPR * 16, 0,
+                                                                   IKV_NT_LOADS ? kNonTemporal : 0));
+        pdst = (int)__builtin_amdgcn_raw_buffer_load_b32(prs, (base + kk * NG) * 4, 0, 0);
+    }
+
+    // Unit u = the RPW consecutive rows [u * RPW, (u + 1) * RPW) one wave covers in one step.
+    __device__ int unit_row(int u) const { return u * RPW + kk * NG + grp; }
+    __device__ void load_unit(__amdgpu_buffer_rsrc_t krs, __amdgpu_buffer_rsrc_t prs, int u, chunk_t (&dst)[RPG][CPL],
+                              int& pdst) const {
+        const int off = (u * RPW + grp) * kRowBytes + p * 16;
+#pragma unroll
+        for (int k = 0; k < RPG; ++k)
+#pragma unroll
+            for (int c = 0; c < CPL; ++c)
+                dst[k][c] = __builtin_bit_cast(
+                    chunk_t, __builtin_amdgcn_raw_buffer_load_b128(krs, off + k * NG * kRowBytes + c * LPR * 16, 0,
+                                                                   IKV_NT_LOADS ? kNonTemporal : 0));
+        pdst = (int)__builtin_amdgcn_raw_buffer_load_b32(prs, unit_row(u) * 4, 0, 0);
     }
 
     // Logit of the (row, head) this lane owns for one iteration; -inf when masked (a padded head, or a row
@@ -149,16 +176,21 @@ struct Lane {
 #endif
 constexpr int kEpi = IKV_EPI_UNROLL;  // epilogue LDS reads kept in flight per lane
 
+// One workgroup per slab.  The slab is cut into units of RPW rows; waves claim units from an LDS counter when
+// they issue the units' loads, so a wave whose loads come back late simply processes fewer units instead of
+// holding the whole workgroup at the barrier (with a static split the last wave finished ~40% after the first).
+// Logits are stored per unit; after a barrier the epilogue walks the units in a fixed pattern.
 template <typename T, int D, int GP>
 __global__ __launch_bounds__(kThreads)
-__attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_lds_kernel(ScoreArgs a) {
+__attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWavesLds))) void score_lds_kernel(ScoreArgs a) {
     using L = Lane<T, D, GP>;
     using chunk_t = typename L::chunk_t;
-    constexpr int RPG = L::RPG, CPL = L::CPL, RPI = L::RPI;
-    constexpr int kNbuf = Geometry<T, D, GP>::kNbuf;
+    constexpr int RPG = L::RPG, CPL = L::CPL, RPW = L::RPW;
+    constexpr int kNbuf = Geometry<T, D, GP>::kNbufLds;
 
     extern __shared__ float zs[];
     __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
+    __shared__ int next_unit;
 
     const L ln;
     const int s = blockIdx.x;
@@ -166,38 +198,54 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_l
     const int b = (s / a.hkv) % a.batch;
     const int l = s / (a.hkv * a.batch);
     const size_t slab = (size_t)s;
-    const int n = a.n, last = n - 1;
-    const int nit = (n + RPI - 1) / RPI;
+    const int n = a.n;
+    const int nunits = (n + RPW - 1) / RPW;
     const T* kslab = static_cast<const T*>(a.k) + slab * a.cap * D;
-    const int* posb = a.pos + (size_t)b * a.cap;
+    const __amdgpu_buffer_rsrc_t krs = raw_rsrc(kslab, n * L::kRowBytes);
+    const __amdgpu_buffer_rsrc_t prs = raw_rsrc(a.pos + (size_t)b * a.cap, n * 4);
 
+    if (threadIdx.x == 0) next_unit = 0;
     chunk_t qv[GP][CPL];
-    chunk_t kbuf[kNbuf][RPG][CPL];
-    int pbuf[kNbuf];
     ln.load_q(a, (size_t)l * a.batch + b, g, qv);
-#pragma unroll
-    for (int j = 0; j < kNbuf - 1; ++j)
-        ln.load(kslab, posb, 0, last, j, kbuf[j], pbuf[j]);
+    __syncthreads();
+    auto claim = [&]() -> int {
+        int u = 0;
+        if (ln.lane == 0) u = atomicAdd(&next_unit, 1);
+        return __builtin_amdgcn_readfirstlane(u);
+    };
 
-    // stream the slab: logits to LDS (each lane only ever touches its own words), running max per lane
+    // stream: claim a unit, issue its loads kNbuf-1 units ahead of the one being reduced.  Loads are issued on
+    // every path (claims past the end read zeros), so the wait before a reduction covers only its own buffer.
+    chunk_t kbuf[kNbuf][RPG][CPL];
+    int pbuf[kNbuf], ubuf[kNbuf];
+#pragma unroll
+    for (int j = 0; j < kNbuf - 1; ++j) {
+        ubuf[j] = claim();
+        ln.load_unit(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
+    }
     float m = kFloor;
-    for (int it = 0; it < nit; it += kNbuf) {
+    bool more = true;
+    while (more) {
 #pragma unroll
         for (int j = 0; j < kNbuf; ++j) {
-            // unconditional (clamped) so every path issues the same loads and the wait before the reduction
-            // below covers only this iteration's buffer
-            ln.load(kslab, posb, 0, last, it + j + kNbuf - 1, kbuf[(j + kNbuf - 1) % kNbuf],
-                    pbuf[(j + kNbuf - 1) % kNbuf]);
-            if (it + j < nit) {
-                const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.owned_row(0, it + j), n);
+            const int slot = (j + kNbuf - 1) % kNbuf;
+            ubuf[slot] = claim();
+            ln.load_unit(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
+            if (more && ubuf[j] < nunits) {
+                const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.unit_row(ubuf[j]), n);
                 m = fmaxf(m, z);
-                zs[(it + j) * kThreads + threadIdx.x] = z;
+                zs[ubuf[j] * kWave + ln.lane] = z;
+            } else {
+                more = false;  // claims only grow: every later unit of this wave is past the end too
             }
         }
     }
 
-    // epilogue: head max, exponentials and head sums, normalised group sums.  The LDS passes work on kEpi
-    // iterations at a time so their reads overlap instead of forming one long latency chain.
+    // epilogue: per-head softmax statistics, then normalised group sums.  Thread (wave w, lane) visits units
+    // w, w + kWaves, ...; a lane's head is the same in every unit.
+    float* zl = zs + ln.wave * kWave + ln.lane;
+    constexpr int kStep = kWaves * kWave;  // LDS words between a thread's consecutive units
+    const int mine = nunits > ln.wave ? (nunits - ln.wave + kWaves - 1) / kWaves : 0;
 #pragma unroll
     for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
     if (ln.lane < GP) red_m[ln.wave][ln.lane] = m;
@@ -205,25 +253,24 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_l
     m = red_m[0][ln.hh];
 #pragma unroll
     for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][ln.hh]);
-    float* zl = zs + threadIdx.x;
     auto expo = [&](float z) { return z == -INFINITY ? 0.0f : __expf(z - m); };
     float ssum = 0.0f;
-    int it = 0;
-    for (; it + kEpi <= nit; it += kEpi) {
+    int i = 0;
+    for (; i + kEpi <= mine; i += kEpi) {
         float e[kEpi];
 #pragma unroll
-        for (int u = 0; u < kEpi; ++u) e[u] = zl[(it + u) * kThreads];
+        for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
 #pragma unroll
-        for (int u = 0; u < kEpi; ++u) {
-            e[u] = expo(e[u]);
-            ssum += e[u];
-            zl[(it + u) * kThreads] = e[u];
+        for (int v = 0; v < kEpi; ++v) {
+            e[v] = expo(e[v]);
+            ssum += e[v];
+            zl[(i + v) * kStep] = e[v];
         }
     }
-    for (; it < nit; ++it) {
-        const float e = expo(zl[it * kThreads]);
+    for (; i < mine; ++i) {
+        const float e = expo(zl[i * kStep]);
         ssum += e;
-        zl[it * kThreads] = e;
+        zl[i * kStep] = e;
     }
 #pragma unroll
     for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
@@ -233,33 +280,40 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_l
 #pragma unroll
     for (int w = 1; w < kWaves; ++w) tot += red_s[w][ln.hh];
     const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
+    auto prob = [&](float e) { return e * inv; };
     float* rrow = a.r + slab * a.n_stride;
-    it = 0;
-    for (; it + kEpi <= nit; it += kEpi) {
+    // group sum of the normalised probabilities of each row, staged by one lane per row in the first RPW words
+    // of the row's unit block (only this wave reads that block, and it has already read the words) for the
+    // coalesced store below
+    static_assert(RPW % 4 == 0, "the coalesced store moves 4 rows at a time");
+    auto emit = [&](int unit, float sum) {
+        if (ln.hh == 0) zs[unit * kWave + ln.kk * L::NG + ln.grp] = sum;
+    };
+    i = 0;
+    for (; i + kEpi <= mine; i += kEpi) {
         float e[kEpi];
 #pragma unroll
-        for (int u = 0; u < kEpi; ++u) e[u] = zl[(it + u) * kThreads];
+        for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
 #pragma unroll
-        for (int u = 0; u < kEpi; ++u) {
-            const float sum = group_allsum<GP>(e[u] * inv);
-            const int row = ln.owned_row(0, it + u);
-            if (ln.hh == 0 && row < n) rrow[row] = sum;
-        }
+        for (int v = 0; v < kEpi; ++v) emit(ln.wave + (i + v) * kWaves, group_allsum<GP>(prob(e[v])));
     }
-    for (; it < nit; ++it) {
-        const float sum = group_allsum<GP>(zl[it * kThreads] * inv);
-        const int row = ln.owned_row(0, it);
-        if (ln.hh == 0 && row < n) rrow[row] = sum;
+    for (; i < mine; ++i) emit(ln.wave + i * kWaves, group_allsum<GP>(prob(zl[i * kStep])));
+    __syncthreads();
+    // rows [4j, 4j + 4) lie in one unit (RPW is a multiple of 4); rows up to the padded stride are scratch
+    for (int j = threadIdx.x; j * 4 < n; j += kThreads) {
+        const int row = j * 4;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]);
+        *reinterpret_cast<f32x4*>(rrow + row) = v;
     }
 }
 
 template <typename T, int D, int GP>
 __global__ __launch_bounds__(kThreads)
-__attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_split_kernel(ScoreArgs a) {
+__attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWavesSplit))) void score_split_kernel(ScoreArgs a) {
     using L = Lane<T, D, GP>;
     using chunk_t = typename L::chunk_t;
     constexpr int RPG = L::RPG, CPL = L::CPL, RPI = L::RPI;
-    constexpr int kNbuf = Geometry<T, D, GP>::kNbuf;
+    constexpr int kNbuf = Geometry<T, D, GP>::kNbufSplit;
     __shared__ MaxSum red[kWaves][GP];
 
     const L ln;
@@ -273,18 +327,17 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_s
     const size_t slab = ((size_t)l * a.batch + b) * a.hkv + g;
     const int row0 = chunk * a.chunk_rows;
     const int row_end = min(a.n, row0 + a.chunk_rows);
-    const int last = row_end - 1;
     const int nit = row_end > row0 ? (row_end - row0 + RPI - 1) / RPI : 0;
     const T* kslab = static_cast<const T*>(a.k) + slab * a.cap * D;
-    const int* posb = a.pos + (size_t)b * a.cap;
+    const __amdgpu_buffer_rsrc_t krs = raw_rsrc(kslab, row_end * L::kRowBytes);
+    const __amdgpu_buffer_rsrc_t prs = raw_rsrc(a.pos + (size_t)b * a.cap, row_end * 4);
 
     chunk_t qv[GP][CPL];
     chunk_t kbuf[kNbuf][RPG][CPL];
     int pbuf[kNbuf];
     ln.load_q(a, (size_t)l * a.batch + b, g, qv);
 #pragma unroll
-    for (int j = 0; j < kNbuf - 1; ++j)
-        ln.load(kslab, posb, row0, last, j, kbuf[j], pbuf[j]);
+    for (int j = 0; j < kNbuf - 1; ++j) ln.load(krs, prs, row0, j, kbuf[j], pbuf[j]);
 
     // the logits leave the workgroup, so the (max, sum) pair is kept online
     MaxSum ms{kFloor, 0.0f};
@@ -292,7 +345,7 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWaves))) void score_s
     for (int it = 0; it < nit; it += kNbuf) {
 #pragma unroll
         for (int j = 0; j < kNbuf; ++j) {
-            ln.load(kslab, posb, row0, last, it + j + kNbuf - 1, kbuf[(j + kNbuf - 1) % kNbuf],
+            ln.load(krs, prs, row0, it + j + kNbuf - 1, kbuf[(j + kNbuf - 1) % kNbuf],
                     pbuf[(j + kNbuf - 1) % kNbuf]);
             if (it + j < nit) {
                 const int row = ln.owned_row(row0, it + j);
