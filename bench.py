@@ -73,8 +73,9 @@ def counter_traffic():
     return int(kv["traffic_bytes_per_launch"])
 
 
-def cpu_baseline(cfg, seqs: int):
-    """Times the float64 oracle on one steady full-refresh step for `seqs` of the batch's sequences."""
+def cpu_baseline(cfg, seqs: int, steps: int):
+    """Times the float64 oracle on `steps` consecutive steady full-refresh steps for `seqs` of the batch's
+    sequences (each step appends one token, scores B + 1 tokens over all layers and evicts one)."""
     import numpy as np
     import threadpoolctl
 
@@ -84,21 +85,24 @@ def cpu_baseline(cfg, seqs: int):
     sub = cfg.scaled(batch=seqs)
     w = Workload(sub, device="cpu")
     st = w.steady_state()                       # B tokens cached, drawn like the prefill
-    si = w.step_inputs(2)
     cache = Cache(raw_numpy(st["k"]), raw_numpy(st["v"]), st["u"].numpy().astype(np.float64),
                   st["pos"].numpy().astype(np.int64), st["n"], cfg.dtype)
     p = Params(alpha=cfg.alpha, budget=cfg.budget, recency_bias=cfg.recency_bias,
                recency_window=cfg.recency_window)
-    q, kn, vn = raw_numpy(si["q"]), raw_numpy(si["k_new"]), raw_numpy(si["v_new"])
+    inputs = []
+    for t in range(2, 2 + steps):
+        si = w.step_inputs(t)
+        inputs.append((t, raw_numpy(si["q"]), raw_numpy(si["k_new"]), raw_numpy(si["v_new"]), si["new_pos"]))
     threads = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
     t0 = time.perf_counter()
-    evict_step(cache, q, kn, vn, 2, si["new_pos"], p)
+    for t, q, kn, vn, new_pos in inputs:
+        evict_step(cache, q, kn, vn, t, new_pos, p)
     dt = time.perf_counter() - t0
-    per_step = dt * cfg.batch / seqs
+    per_step = dt / steps * cfg.batch / seqs
     return {"value": 1.0 / per_step, "unit": "evict-steps/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"one steady full-refresh step (n = B + 1 = {cfg.budget + 1}) for {seqs} of {cfg.batch} "
-                      f"sequences, all {cfg.layers} layers; {dt:.2f} s measured, scaled by {cfg.batch // seqs} "
-                      f"to the whole batch",
+            "sample": f"{steps} consecutive steady full-refresh steps (n = B + 1 = {cfg.budget + 1} scored) for "
+                      f"{seqs} of {cfg.batch} sequences, all {cfg.layers} layers; {dt:.2f} s measured, scaled by "
+                      f"{cfg.batch / seqs:g} to the whole batch",
             "seconds_measured": dt}
 
 
@@ -108,6 +112,7 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--cpu-seqs", type=int, default=8, help="sequences of the batch the CPU oracle times")
+    ap.add_argument("--cpu-steps", type=int, default=12, help="consecutive steps the CPU oracle times")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
                     help="run a plain device copy of this size first (counter calibration)")
@@ -236,7 +241,7 @@ def main():
         "setup_s": round(setup_s, 1),
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seqs)
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seqs, args.cpu_steps)
     print(json.dumps(out), flush=True)
 
 
