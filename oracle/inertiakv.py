@@ -12,6 +12,7 @@ Each function names the passage it follows:
   query heads.  Appendix "Implementation Details / Per-step scoring": under GQA each KV head's attention is
   shared by its query-head group before pooling.
 * Eq. 2 / 3 / 4: single-step, cumulative and EMA aggregation rules.
+* The step's decode attention (the softmax Eq. 1 pools, applied to V), for the fused attention + score path.
 * Appendix "Implementation Details / Layer scoring": the EMA state is updated after every eligible layer,
   m_{t,l} = alpha m_{t,l-1} + (1 - alpha) s_{t,l}, l = 1..K, m_{t,0} = m_{t-1,K}.
 * Appendix "Implementation Details / Momentum initialization": m_0 = 0 for every prefill position.
@@ -116,6 +117,31 @@ def layer_scores(q_l: np.ndarray, keys_l: np.ndarray, pos: np.ndarray | None = N
 
 
 # ----------------------------------------------------------------------------------------------------------
+# The step's own decode attention: the same softmax of the last query that Eq. 1 pools, applied to V
+# (scaled dot-product attention, Sec. 3 cites it for a_t)
+# ----------------------------------------------------------------------------------------------------------
+def attention_output(q_l: np.ndarray, keys_l: np.ndarray, values_l: np.ndarray, pos: np.ndarray | None = None,
+                     cur_pos: int = 0, recency_bias: float = 0.0, recency_window: int = 0):
+    """Last-query attention of one layer and one sequence.
+
+    q_l: [H_q, d]; keys_l, values_l: [H_kv, n, d] float64.  Returns (o, scale), both [H_q, d]:
+    o_h = sum_i a^(h)(i) v_{h // G}(i) with a^(h) the softmax of `head_attention`, and
+    scale_h = sum_i a^(h)(i) |v_{h // G}(i)|, the magnitude that bounds rounding in the weighted sum.
+    """
+    hq, hkv = q_l.shape[0], keys_l.shape[0]
+    if hq % hkv:
+        raise ValueError("query heads must be a multiple of KV heads")
+    group = hq // hkv
+    o = np.zeros((hq, values_l.shape[-1]), dtype=np.float64)
+    scale = np.zeros_like(o)
+    for h in range(hq):
+        a = head_attention(q_l[h], keys_l[h // group], pos, cur_pos, recency_bias, recency_window)
+        o[h] = a @ values_l[h // group]
+        scale[h] = a @ np.abs(values_l[h // group])
+    return o, scale
+
+
+# ----------------------------------------------------------------------------------------------------------
 # Eq. 2-4 + Appendix "Layer scoring": per-layer sequential aggregation
 # ----------------------------------------------------------------------------------------------------------
 EMA, SINGLE_STEP, CUMULATIVE = "ema", "single", "cumulative"
@@ -207,6 +233,8 @@ class StepResult:
     s_layers: np.ndarray | None = None         # [K, b, n_scored] per-layer scores (refresh steps)
     moves: list = field(default_factory=list)  # per sequence (dst, src)
     n_out: int = 0
+    o: np.ndarray | None = None                # [K, b, H_q, d] decode attention output (when asked for)
+    o_scale: np.ndarray | None = None          # [K, b, H_q, d] sum_i a |v|, the output's rounding scale
 
 
 def new_token_prior(u_existing: np.ndarray, refresh: bool, policy: str) -> float:
@@ -226,7 +254,7 @@ def new_token_prior(u_existing: np.ndarray, refresh: bool, policy: str) -> float
 
 
 def evict_step(cache: Cache, q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray, t: int, new_pos: int,
-               params: Params, keep_override: np.ndarray | None = None) -> StepResult:
+               params: Params, keep_override: np.ndarray | None = None, attention: bool = False) -> StepResult:
     """One decode step, mutating `cache` in place.
 
     q: [K, b, H_q, d] raw; k_new, v_new: [K, b, H_kv, d] raw.
@@ -234,6 +262,8 @@ def evict_step(cache: Cache, q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray
     2. on refresh steps, score every cached token layer by layer (Eq. 1) and fold (Eq. 4, layer-sequential);
     3. if more than B tokens are cached, keep the top B (ties: lower position);
     4. hole-fill compaction of K, V, u and pos.
+    `attention`: also return the step's decode attention output of every layer over the n + 1 cached tokens
+    (after the append, before eviction; computed on every step, refresh or not).
     `keep_override` lets a caller replace the selection by an equally valid one (used only to keep two
     implementations in lockstep after a tie inside the rounding band): either a [b, >= n] mask, or a callable
     receiving (the oracle's own [b, n] decision, the [b, n] utilities it was taken on) and returning the mask
@@ -253,6 +283,18 @@ def evict_step(cache: Cache, q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray
     cache.v[:, :, :, n, :] = v_new
     n += 1
     cache.n = n
+
+    # decode attention of the step (the decoder runs it whether or not the step refreshes the scores)
+    o_all = o_scale = None
+    if attention:
+        o_all = np.zeros((nl, nb, q.shape[2], d), dtype=np.float64)
+        o_scale = np.zeros_like(o_all)
+        for b in range(nb):
+            for l in range(nl):
+                o_all[l, b], o_scale[l, b] = attention_output(
+                    to_f64(q[l, b], cache.dtype), to_f64(cache.k[l, b, :, :n, :], cache.dtype),
+                    to_f64(cache.v[l, b, :, :n, :], cache.dtype), cache.pos[b, :n], new_pos,
+                    params.recency_bias, params.recency_window)
 
     # 2. score + fold
     s_all = None
@@ -289,7 +331,7 @@ def evict_step(cache: Cache, q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray
         cache.pos[b, dst] = cache.pos[b, src]
         moves.append((dst, src))
     cache.n = min(params.budget, n)
-    return StepResult(refresh, n, keep, u_pre, s_all, moves, cache.n)
+    return StepResult(refresh, n, keep, u_pre, s_all, moves, cache.n, o_all, o_scale)
 
 
 def compact_rows(rows: np.ndarray, keep: np.ndarray, budget: int) -> np.ndarray:
