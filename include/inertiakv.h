@@ -126,6 +126,41 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
                         float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
                         const kv_trace* trace, void* ws, size_t ws_bytes, void* stream);
 
+/* ---- Decode step around the model's own attention (fused decode attention + score) ----
+ * A decoder that attends the cache anyway can take the step's score from its attention (Eq. 1 is the softmax
+ * of the last query, the one that produces the attention output): K is then read once for both, instead of
+ * once by attention and again by a separate scoring pass (the paper profiles that reconstruction as the
+ * dominant per-step cost, appendix "Hook-level profiling").  A step t is
+ *     kv_append(t) ; kv_attend_score(layers ...) over every layer, emit_scores = refresh step ;
+ *     kv_evict_finish(t)
+ * and leaves the cache, u and pos exactly as kv_evict_step would (same scores, same fold, same selection).
+ * All three calls of a step use the same workspace (the group sums of each layer live in it between the
+ * attention calls and the finish), sized by kv_workspace_bytes for at least n_in + 1 tokens.
+ *
+ * kv_append: step 1 of kv_evict_step alone (appendix "New token insertion"; the refresh decision of Eq. 5
+ * picks the prior: 0 on refresh steps, else the mean or min of the existing utilities). */
+kv_status kv_append(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in, int32_t new_pos,
+                    const void* k_new, const void* v_new, void* k, void* v, float* u, int32_t* pos, void* stream);
+
+/* Decode attention of layers [layer0, layer0 + layer_count) over the n cached tokens, for every sequence and
+ * query head: a_h = softmax_i(z_h(i)) with z_h(i) = q_h . k_i / sqrt(d) (+ recency_bias if
+ * pos[i] >= cur_pos - (recency_window - 1)), o_h = sum_i a_h(i) v_i.  q and o are [layer_count][batch]
+ * [n_q_heads][d] in the cache dtype (o rounded to nearest); k, v are the whole caches (layer 0 at the
+ * pointer).  emit_scores != 0 additionally records these layers' pooled scores (Eq. 1) in the workspace for
+ * kv_evict_finish; layers whose scores are not emitted keep whatever the workspace held.  Layers may be
+ * attended in any number of calls (one per layer in a decoder). */
+kv_status kv_attend_score(const kv_shape* shape, int32_t layer0, int32_t layer_count, int32_t n, const void* q,
+                          const void* k, const void* v, const int32_t* pos, int32_t cur_pos, float recency_bias,
+                          int32_t recency_window, int32_t emit_scores, void* o, void* ws, size_t ws_bytes,
+                          void* stream);
+
+/* Steps 2-3 of kv_evict_step after the attention calls: on refresh steps (Eq. 5) the layer fold of the
+ * emitted scores of ALL layers (Eq. 4 by params->rule), then the top-B selection and compaction over the n
+ * cached tokens (n = n_in + 1 of the step).  *n_out (HOST) = min(B, n); keep_out / s_out as kv_evict_step. */
+kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n, void* k, void* v,
+                          float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out, void* ws,
+                          size_t ws_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* kv_status_string(kv_status status);
 

@@ -22,7 +22,7 @@ KV_PHASES = 5
 PHASES = ("append", "score", "fold", "select", "compact")
 
 EXPORTED = ("kv_workspace_bytes", "kv_score_ema", "kv_topk_select", "kv_compact", "kv_evict_step",
-            "kv_status_string")
+            "kv_append", "kv_attend_score", "kv_evict_finish", "kv_status_string")
 
 
 class KVError(RuntimeError):
@@ -66,6 +66,9 @@ def load_library(path: str = LIB_PATH):
     lib.kv_compact.argtypes = [shp, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.kv_evict_step.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
                                   ctypes.POINTER(i32), vp, vp, trc, vp, sz, vp]
+    lib.kv_append.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+    lib.kv_attend_score.argtypes = [shp, i32, i32, i32, vp, vp, vp, vp, i32, f32, i32, i32, vp, vp, sz, vp]
+    lib.kv_evict_finish.argtypes = [shp, prm, i32, i32, vp, vp, vp, vp, ctypes.POINTER(i32), vp, vp, vp, sz, vp]
     for fn in EXPORTED[:-1]:
         getattr(lib, fn).restype = i32
     lib.kv_status_string.argtypes = [i32]
@@ -152,6 +155,33 @@ def kv_evict_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos
         _ptr(v_new), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out),
         ctypes.byref(trace) if trace is not None else None, _ptr(ws),
         ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+    return n_out.value
+
+
+def _ws_bytes(ws):
+    return ws.numel() * ws.element_size() if ws is not None else 0
+
+
+def kv_append(shape, params, t, n_in, new_pos, k_new, v_new, k, v, u, pos, stream=None):
+    _check("kv_append", load_library().kv_append(
+        ctypes.byref(shape), ctypes.byref(params), int(t), int(n_in), int(new_pos), _ptr(k_new), _ptr(v_new),
+        _ptr(k), _ptr(v), _ptr(u), _ptr(pos), _stream(stream)))
+
+
+def kv_attend_score(shape, layer0, layer_count, n, q, k, v, pos, cur_pos, recency_bias, recency_window,
+                    emit_scores, o, ws, stream=None):
+    _check("kv_attend_score", load_library().kv_attend_score(
+        ctypes.byref(shape), int(layer0), int(layer_count), int(n), _ptr(q), _ptr(k), _ptr(v), _ptr(pos),
+        int(cur_pos), float(recency_bias), int(recency_window), int(bool(emit_scores)), _ptr(o), _ptr(ws),
+        _ws_bytes(ws), _stream(stream)))
+
+
+def kv_evict_finish(shape, params, t, n, k, v, u, pos, ws, keep_out=None, s_out=None, stream=None) -> int:
+    """Returns n_out = min(B, n)."""
+    n_out = ctypes.c_int32(-1)
+    _check("kv_evict_finish", load_library().kv_evict_finish(
+        ctypes.byref(shape), ctypes.byref(params), int(t), int(n), _ptr(k), _ptr(v), _ptr(u), _ptr(pos),
+        ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out), _ptr(ws), _ws_bytes(ws), _stream(stream)))
     return n_out.value
 
 

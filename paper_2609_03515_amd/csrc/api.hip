@@ -14,7 +14,7 @@ struct Layout {
     int n_stride;
     int max_pairs;
     ScorePlan plan;
-    size_t r_off, z_off, part_off, pdst_off, psrc_off, np_off, total;
+    size_t r_off, z_off, part_off, opart_off, pdst_off, psrc_off, np_off, total;
 };
 
 int esize(const kv_shape& s) { return s.dtype == KV_F32 ? 4 : 2; }
@@ -38,22 +38,30 @@ kv_status check_shape(const kv_shape* s) {
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// One layout serves every entry point for a given n, so that the group sums r written by the attention
+// calls of a step are where kv_evict_finish folds them.  The logits / partial regions are shared by the
+// scorer's split path and the attention's chunked path (never live at the same time).
 Layout layout_for(const kv_shape& s, int n) {
     Layout L{};
     L.n_stride = (n + 63) / 64 * 64;
     L.max_pairs = n;
-    score_plan(s.dtype, s.head_dim, s.n_q_heads / s.n_kv_heads, n, &L.plan);
+    const int group = s.n_q_heads / s.n_kv_heads;
+    score_plan(s.dtype, s.head_dim, group, n, &L.plan);
+    const AttendBound ab = attend_bound(s.dtype, s.head_dim, group, n, s.batch * s.n_kv_heads, s.layers);
+    const size_t heads = (size_t)s.layers * s.batch * s.n_q_heads;
+    const size_t logits = heads * L.n_stride * sizeof(float);
+    const size_t z_bytes = (L.plan.split || ab.may_split) ? logits : 0;
+    const size_t part_score = L.plan.split ? heads * L.plan.nchunk * sizeof(float2) : 0;
+    const size_t part_attn = (size_t)ab.chunk_layers * s.batch * s.n_q_heads * sizeof(float2);
     size_t off = 0;
     L.r_off = off;
     off = align256(off + (size_t)s.layers * s.batch * s.n_kv_heads * L.n_stride * sizeof(float));
     L.z_off = off;
-    if (L.plan.split) {
-        off = align256(off + (size_t)s.layers * s.batch * s.n_q_heads * L.n_stride * sizeof(float));
-        L.part_off = off;
-        off = align256(off + (size_t)s.layers * s.batch * s.n_q_heads * L.plan.nchunk * sizeof(float2));
-    } else {
-        L.part_off = off;
-    }
+    off = align256(off + z_bytes);
+    L.part_off = off;
+    off = align256(off + (part_score > part_attn ? part_score : part_attn));
+    L.opart_off = off;
+    off = align256(off + (size_t)ab.chunk_layers * s.batch * s.n_q_heads * s.head_dim * sizeof(float));
     L.pdst_off = off;
     off = align256(off + (size_t)s.batch * L.max_pairs * sizeof(int32_t));
     L.psrc_off = off;
@@ -83,10 +91,8 @@ void record(const kv_trace* tr, int phase, bool begin, hipStream_t s) {
     if (ev) (void)hipEventRecord(static_cast<hipEvent_t>(ev), s);
 }
 
-// Scoring (Eq. 1) of rows [0, n) into the workspace r, then the layer fold into u.
-kv_status run_score_fold(const kv_shape& s, const Layout& L, int n, const void* q, const void* k,
-                         const int32_t* pos, int cur_pos, float recency_bias, int recency_window, float* u,
-                         float* s_out, int rule, float alpha, void* ws, hipStream_t st, const kv_trace* tr) {
+ScoreArgs score_args(const kv_shape& s, const Layout& L, int n, const void* q, const void* k, const int32_t* pos,
+                     int cur_pos, float recency_bias, int recency_window, void* ws) {
     ScoreArgs a{};
     a.q = q;
     a.k = k;
@@ -94,6 +100,7 @@ kv_status run_score_fold(const kv_shape& s, const Layout& L, int n, const void* 
     a.r = at<float>(ws, L.r_off);
     a.z = at<float>(ws, L.z_off);
     a.part = at<float2>(ws, L.part_off);
+    a.opart = at<float>(ws, L.opart_off);
     a.batch = s.batch;
     a.layers = s.layers;
     a.hq = s.n_q_heads;
@@ -105,19 +112,30 @@ kv_status run_score_fold(const kv_shape& s, const Layout& L, int n, const void* 
     a.recent_from = cur_pos - (recency_window - 1);
     a.bias = recency_window > 0 ? recency_bias : 0.0f;
     a.scale = (float)(1.0 / sqrt((double)s.head_dim));
+    return a;
+}
+
+// Scoring (Eq. 1) of rows [0, n) of every layer into the workspace r.
+kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, const void* k, const int32_t* pos,
+                    int cur_pos, float recency_bias, int recency_window, void* ws, hipStream_t st,
+                    const kv_trace* tr) {
+    ScoreArgs a = score_args(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws);
     a.chunk_rows = L.plan.chunk_rows;
     a.nchunk = L.plan.nchunk;
     ScorePlan plan = L.plan;
     plan.grid = s.layers * s.batch * s.n_kv_heads * plan.nchunk;
-
     record(tr, 1, true, st);
     kv_status rc = hip_status(launch_score(s.dtype, s.head_dim, plan, a, st));
     if (rc == KV_OK && plan.split) rc = hip_status(launch_split_finish(a, st));
     record(tr, 1, false, st);
-    if (rc != KV_OK) return rc;
+    return rc;
+}
 
+// Layer fold of the workspace r into u (Eq. 2-4 by `rule`).
+kv_status run_fold(const kv_shape& s, const Layout& L, int n, float* u, float* s_out, int rule, float alpha,
+                   void* ws, hipStream_t st, const kv_trace* tr) {
     FoldArgs f{};
-    f.r = a.r;
+    f.r = at<float>(ws, L.r_off);
     f.u = u;
     f.s_out = s_out;
     f.batch = s.batch;
@@ -145,7 +163,7 @@ kv_status run_score_fold(const kv_shape& s, const Layout& L, int n, const void* 
         f.prior_w = 1.0f;
     }
     record(tr, 2, true, st);
-    rc = hip_status(launch_fold(f, st));
+    kv_status rc = hip_status(launch_fold(f, st));
     record(tr, 2, false, st);
     return rc;
 }
@@ -188,6 +206,59 @@ MoveArgs move_args(const kv_shape& s, const Layout& L, int n, int budget, void* 
     return m;
 }
 
+kv_status check_params(const kv_params* params) {
+    if (!params) return KV_ERR_INVALID_ARG;
+    const kv_params& p = *params;
+    if (!(p.alpha >= 0.0f && p.alpha < 1.0f) || p.budget < 1 || p.refresh_period < 1) return KV_ERR_INVALID_ARG;
+    if (p.nonrefresh_init != KV_INIT_MEAN && p.nonrefresh_init != KV_INIT_MIN) return KV_ERR_INVALID_ARG;
+    if (p.rule < KV_RULE_EMA || p.rule > KV_RULE_CUMULATIVE) return KV_ERR_INVALID_ARG;
+    if (p.recency_window < 0 || !isfinite(p.recency_bias)) return KV_ERR_INVALID_ARG;
+    return KV_OK;
+}
+
+// Refresh set (Eq. 5); Score-Free refreshes only at the first decode step.
+bool is_refresh(const kv_params& p, int t) { return p.score_free ? (t == 1) : ((t - 1) % p.refresh_period == 0); }
+
+kv_status run_append(const kv_shape& s, const kv_params& p, int t, int n_in, int new_pos, const void* k_new,
+                     const void* v_new, void* k, void* v, float* u, int32_t* pos, hipStream_t st,
+                     const kv_trace* tr) {
+    AppendArgs ap{};
+    ap.k = k;
+    ap.v = v;
+    ap.k_new = k_new;
+    ap.v_new = v_new;
+    ap.u = u;
+    ap.pos = pos;
+    ap.batch = s.batch;
+    ap.layers = s.layers;
+    ap.hkv = s.n_kv_heads;
+    ap.cap = s.capacity;
+    ap.row_bytes = s.head_dim * esize(s);
+    ap.n_in = n_in;
+    ap.new_pos = new_pos;
+    ap.init_mode = is_refresh(p, t) ? 0 : (p.nonrefresh_init == KV_INIT_MEAN ? 1 : 2);
+    record(tr, 0, true, st);
+    kv_status rc = hip_status(launch_append(ap, st));
+    record(tr, 0, false, st);
+    return rc;
+}
+
+// Top-B selection over the n cached tokens and, when tokens are dropped, the compaction.
+kv_status run_select_compact(const kv_shape& s, const Layout& L, int n, int budget, void* k, void* v, float* u,
+                             int32_t* pos, uint8_t* keep_out, void* ws, hipStream_t st, const kv_trace* tr) {
+    if (n <= budget && !keep_out) return KV_OK;
+    SelectArgs a = select_args(s, L, n, budget, u, pos, ws);
+    a.keep_out = keep_out;
+    record(tr, 3, true, st);
+    kv_status rc = hip_status(launch_select(a, false, st));
+    record(tr, 3, false, st);
+    if (rc != KV_OK || n <= budget) return rc;
+    record(tr, 4, true, st);
+    rc = hip_status(launch_move(move_args(s, L, n, budget, k, v, u, pos, ws), st));
+    record(tr, 4, false, st);
+    return rc;
+}
+
 }  // namespace
 }  // namespace ikv
 
@@ -217,8 +288,10 @@ kv_status kv_score_ema(const kv_shape* shape, int32_t n, const void* q, const vo
         return KV_ERR_UNSUPPORTED;
     const Layout L = layout_for(s, n);
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
-    return run_score_fold(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, u, s_out, KV_RULE_EMA,
-                          alpha, ws, static_cast<hipStream_t>(stream), nullptr);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if ((rc = run_score(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws, st, nullptr)) != KV_OK)
+        return rc;
+    return run_fold(s, L, n, u, s_out, KV_RULE_EMA, alpha, ws, st, nullptr);
 }
 
 kv_status kv_topk_select(const kv_shape* shape, int32_t n, int32_t budget, const float* u, const int32_t* pos,
@@ -261,13 +334,10 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
     kv_status rc = check_shape(shape);
     if (rc != KV_OK) return rc;
     const kv_shape& s = *shape;
-    if (!params || !n_out) return KV_ERR_INVALID_ARG;
+    if ((rc = check_params(params)) != KV_OK) return rc;
     const kv_params& p = *params;
+    if (!n_out) return KV_ERR_INVALID_ARG;
     if (t < 1 || n_in < 0 || n_in + 1 > s.capacity || new_pos < 0) return KV_ERR_INVALID_ARG;
-    if (!(p.alpha >= 0.0f && p.alpha < 1.0f) || p.budget < 1 || p.refresh_period < 1) return KV_ERR_INVALID_ARG;
-    if (p.nonrefresh_init != KV_INIT_MEAN && p.nonrefresh_init != KV_INIT_MIN) return KV_ERR_INVALID_ARG;
-    if (p.rule < KV_RULE_EMA || p.rule > KV_RULE_CUMULATIVE) return KV_ERR_INVALID_ARG;
-    if (p.recency_window < 0 || !isfinite(p.recency_bias)) return KV_ERR_INVALID_ARG;
     if (!q || !k_new || !v_new || !k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
     if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k, 16) || !aligned(v, 16) ||
         !aligned(u, 4) || !aligned(pos, 4) || !aligned(s_out, 4))
@@ -277,49 +347,89 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
 
-    const bool refresh = p.score_free ? (t == 1) : ((t - 1) % p.refresh_period == 0);
+    if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, st, trace)) != KV_OK) return rc;
+    if (is_refresh(p, t)) {
+        rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, ws, st, trace);
+        if (rc == KV_OK) rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, ws, st, trace);
+        if (rc != KV_OK) return rc;
+    }
+    if ((rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, ws, st, trace)) != KV_OK) return rc;
+    *n_out = n < p.budget ? n : p.budget;
+    return KV_OK;
+}
 
-    AppendArgs ap{};
-    ap.k = k;
-    ap.v = v;
-    ap.k_new = k_new;
-    ap.v_new = v_new;
-    ap.u = u;
-    ap.pos = pos;
-    ap.batch = s.batch;
-    ap.layers = s.layers;
-    ap.hkv = s.n_kv_heads;
-    ap.cap = s.capacity;
-    ap.row_bytes = s.head_dim * esize(s);
-    ap.n_in = n_in;
-    ap.new_pos = new_pos;
-    ap.init_mode = refresh ? 0 : (p.nonrefresh_init == KV_INIT_MEAN ? 1 : 2);
-
-    record(trace, 0, true, st);
-    rc = hip_status(launch_append(ap, st));
-    record(trace, 0, false, st);
+kv_status kv_append(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in, int32_t new_pos,
+                    const void* k_new, const void* v_new, void* k, void* v, float* u, int32_t* pos, void* stream) {
+    kv_status rc = check_shape(shape);
     if (rc != KV_OK) return rc;
+    const kv_shape& s = *shape;
+    if ((rc = check_params(params)) != KV_OK) return rc;
+    if (t < 1 || n_in < 0 || n_in + 1 > s.capacity || new_pos < 0) return KV_ERR_INVALID_ARG;
+    if (!k_new || !v_new || !k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
+    if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(u, 4) ||
+        !aligned(pos, 4))
+        return KV_ERR_UNSUPPORTED;
+    return run_append(s, *params, t, n_in, new_pos, k_new, v_new, k, v, u, pos, static_cast<hipStream_t>(stream),
+                      nullptr);
+}
 
-    if (refresh) {
-        rc = run_score_fold(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, u, s_out, p.rule,
-                            p.alpha, ws, st, trace);
-        if (rc != KV_OK) return rc;
+kv_status kv_attend_score(const kv_shape* shape, int32_t layer0, int32_t layer_count, int32_t n, const void* q,
+                          const void* k, const void* v, const int32_t* pos, int32_t cur_pos, float recency_bias,
+                          int32_t recency_window, int32_t emit_scores, void* o, void* ws, size_t ws_bytes,
+                          void* stream) {
+    kv_status rc = check_shape(shape);
+    if (rc != KV_OK) return rc;
+    const kv_shape& s = *shape;
+    if (layer0 < 0 || layer_count < 1 || layer0 + layer_count > s.layers) return KV_ERR_INVALID_ARG;
+    if (n < 1 || n > s.capacity || recency_window < 0 || !isfinite(recency_bias)) return KV_ERR_INVALID_ARG;
+    if (!q || !k || !v || !pos || !o) return KV_ERR_INVALID_ARG;
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(pos, 4) || !aligned(o, esize(s)))
+        return KV_ERR_UNSUPPORTED;
+    const Layout L = layout_for(s, n);
+    if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
+    const int group = s.n_q_heads / s.n_kv_heads;
+    ScorePlan plan;
+    if (!attend_plan(s.dtype, s.head_dim, group, n, layer_count * s.batch * s.n_kv_heads, &plan))
+        return KV_ERR_UNSUPPORTED;
+    // the call's layers are its own index space: K/V and r advance to layer0, q and o are per call
+    const size_t slab_elems = (size_t)s.batch * s.n_kv_heads * s.capacity * s.head_dim;
+    const char* kb = static_cast<const char*>(k) + (size_t)layer0 * slab_elems * esize(s);
+    const char* vb = static_cast<const char*>(v) + (size_t)layer0 * slab_elems * esize(s);
+    ScoreArgs a = score_args(s, L, n, q, kb, pos, cur_pos, recency_bias, recency_window, ws);
+    a.v = vb;
+    a.o = o;
+    a.r += (size_t)layer0 * s.batch * s.n_kv_heads * L.n_stride;
+    a.layers = layer_count;
+    a.chunk_rows = plan.chunk_rows;
+    a.nchunk = plan.nchunk;
+    a.emit = emit_scores != 0;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if ((rc = hip_status(launch_attend(s.dtype, s.head_dim, plan, a, st))) != KV_OK) return rc;
+    if (plan.split) {
+        if ((rc = hip_status(launch_attend_finish(s.dtype, s.head_dim, a, st))) != KV_OK) return rc;
+        if (a.emit && (rc = hip_status(launch_split_finish(a, st))) != KV_OK) return rc;
     }
+    return KV_OK;
+}
 
-    if (n > p.budget || keep_out) {
-        SelectArgs a = select_args(s, L, n, p.budget, u, pos, ws);
-        a.keep_out = keep_out;
-        record(trace, 3, true, st);
-        rc = hip_status(launch_select(a, false, st));
-        record(trace, 3, false, st);
-        if (rc != KV_OK) return rc;
-        if (n > p.budget) {
-            record(trace, 4, true, st);
-            rc = hip_status(launch_move(move_args(s, L, n, p.budget, k, v, u, pos, ws), st));
-            record(trace, 4, false, st);
-            if (rc != KV_OK) return rc;
-        }
-    }
+kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n, void* k, void* v,
+                          float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out, void* ws,
+                          size_t ws_bytes, void* stream) {
+    kv_status rc = check_shape(shape);
+    if (rc != KV_OK) return rc;
+    const kv_shape& s = *shape;
+    if ((rc = check_params(params)) != KV_OK) return rc;
+    const kv_params& p = *params;
+    if (!n_out || t < 1 || n < 1 || n > s.capacity) return KV_ERR_INVALID_ARG;
+    if (!k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
+    if (!aligned(k, 16) || !aligned(v, 16) || !aligned(u, 4) || !aligned(pos, 4) || !aligned(s_out, 4))
+        return KV_ERR_UNSUPPORTED;
+    const Layout L = layout_for(s, n);
+    if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (is_refresh(p, t) && (rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, ws, st, nullptr)) != KV_OK)
+        return rc;
+    if ((rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, ws, st, nullptr)) != KV_OK) return rc;
     *n_out = n < p.budget ? n : p.budget;
     return KV_OK;
 }

@@ -1,0 +1,382 @@
+// Decode attention fused with the eviction score (Eq. 1) for gfx950.
+//
+// At every layer a decoder attends its last query over the cached rows; the method's per-step score is the
+// same softmax, mean-pooled over query heads.  Computing both in one kernel lets a single pass over K serve
+// the attention output and the score (the separate score pass is the dominant per-step cost of the method in
+// the paper's profiling), and V is read once for the output.
+//
+// One workgroup per (layer, sequence, KV head, row chunk):
+//   1. K pass: logits of the chunk's rows for the group's heads into LDS (the scorer's lane machinery and
+//      dynamic unit claiming), running per-head max;
+//   2. e = exp(z - max) in place, per-head sums;
+//   3. V pass: every lane accumulates e_h(row) * v(row) for the GP heads over its 16-byte V chunks, the
+//      probabilities of a row being GP consecutive LDS words;
+//   4. cross-lane / cross-wave reduction in a fixed order (deterministic), then either the normalised
+//      output (one chunk per slab) or the chunk's unnormalised partial output with its per-head (max, sum);
+//   5. when the score is wanted: the group probability sums r of the rows (one chunk), or the raw logits
+//      for the scorer's finish kernel (several chunks).
+// Chunks exist so that one layer's slabs (batch x KV heads, e.g. 64) still fill 256 CUs.
+#include "stream_lane.h"
+
+namespace ikv {
+namespace {
+
+constexpr int kAttnTargetWgs = 1024;  // workgroups per launch wanted: four per CU
+constexpr int kAttnMinRows = 256;     // smallest chunk: below it a chunk's fixed costs dominate its stream
+
+template <int GP>
+__device__ __forceinline__ void read_probs(const float* src, float (&e)[GP]) {
+    if constexpr (GP >= 4) {
+#pragma unroll
+        for (int i = 0; i < GP; i += 4) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(src + i);
+            e[i] = v.x;
+            e[i + 1] = v.y;
+            e[i + 2] = v.z;
+            e[i + 3] = v.w;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < GP; ++i) e[i] = src[i];
+    }
+}
+
+template <typename T, int D, int GP>
+__global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
+    using L = Lane<T, D, GP>;
+    using E = Elem<T>;
+    using chunk_t = typename L::chunk_t;
+    constexpr int RPG = L::RPG, CPL = L::CPL, RPW = L::RPW, LPR = L::LPR, EPC = L::EPC;
+    // K/V loads of two units in flight, one when a lane's share of a unit is already large (a single head
+    // per KV head: 16 rows per lane), which would otherwise spill
+    constexpr int kNbuf = RPG * CPL > 8 ? 1 : 2;
+
+    extern __shared__ float zs[];
+    __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
+    __shared__ float obuf[GP * D];
+    __shared__ int next_unit[2];
+
+    const L ln;
+    const int chunk = blockIdx.x % a.nchunk;
+    const int s = blockIdx.x / a.nchunk;  // slab: (l * batch + b) * hkv + g, l relative to the call
+    const int g = s % a.hkv;
+    const int lb = s / a.hkv;
+    const int b = lb % a.batch;
+    const int row0 = chunk * a.chunk_rows;
+    const int nrows = min(a.n - row0, a.chunk_rows);  // >= 1: the plan leaves no empty chunk
+    const int nunits = (nrows + RPW - 1) / RPW;
+    const size_t base = ((size_t)s * a.cap + row0) * D;
+    const __amdgpu_buffer_rsrc_t krs = raw_rsrc(static_cast<const T*>(a.k) + base, nrows * L::kRowBytes);
+    const __amdgpu_buffer_rsrc_t vrs = raw_rsrc(static_cast<const T*>(a.v) + base, nrows * L::kRowBytes);
+    const __amdgpu_buffer_rsrc_t prs = raw_rsrc(a.pos + (size_t)b * a.cap + row0, nrows * 4);
+
+    if (threadIdx.x == 0) {
+        next_unit[0] = 0;
+        next_unit[1] = 0;
+    }
+    chunk_t qv[GP][CPL];
+    ln.load_q(a, (size_t)lb, g, qv);
+    __syncthreads();
+    auto claim = [&](int which) -> int {
+        int u = 0;
+        if (ln.lane == 0) u = atomicAdd(&next_unit[which], 1);
+        return __builtin_amdgcn_readfirstlane(u);
+    };
+
+    // 1. K pass (loads of claims past the end read zeros and are not reduced)
+    float m = kFloor;
+    {
+        chunk_t kbuf[kNbuf][RPG][CPL];
+        int pbuf[kNbuf], ubuf[kNbuf];
+#pragma unroll
+        for (int j = 0; j < kNbuf - 1; ++j) {
+            ubuf[j] = claim(0);
+            ln.load_unit(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
+        }
+        bool more = true;
+        while (more) {
+#pragma unroll
+            for (int j = 0; j < kNbuf; ++j) {
+                const int slot = (j + kNbuf - 1) % kNbuf;
+                ubuf[slot] = claim(0);
+                ln.load_unit(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
+                if (more && ubuf[j] < nunits) {
+                    const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.unit_row(ubuf[j]), nrows);
+                    m = fmaxf(m, z);
+                    zs[ubuf[j] * kWave + ln.lane] = z;
+                } else {
+                    more = false;
+                }
+            }
+        }
+    }
+
+    // 2. per-head max, exponentials in place, per-head sums; several chunks: the logits go to HBM for the
+    //    score's finish kernel
+#pragma unroll
+    for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+    if (ln.lane < GP) red_m[ln.wave][ln.lane] = m;
+    __syncthreads();
+    m = red_m[0][ln.hh];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][ln.hh]);
+
+    float* zl = zs + ln.wave * kWave + ln.lane;
+    constexpr int kStep = kWaves * kWave;
+    const int mine = nunits > ln.wave ? (nunits - ln.wave + kWaves - 1) / kWaves : 0;
+    const bool write_z = a.emit && a.nchunk > 1;
+    float* zrow = a.z + ((size_t)lb * a.hq + (size_t)g * a.group + ln.hh) * a.n_stride + row0;
+    float ssum = 0.0f;
+    auto expo = [&](float z, int unit) {
+        if (write_z && z != -INFINITY) zrow[ln.unit_row(unit)] = z;  // -inf: padded head or row past the end
+        return z == -INFINITY ? 0.0f : __expf(z - m);
+    };
+    int i = 0;
+    for (; i + kEpi <= mine; i += kEpi) {
+        float e[kEpi];
+#pragma unroll
+        for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
+#pragma unroll
+        for (int v = 0; v < kEpi; ++v) {
+            e[v] = expo(e[v], ln.wave + (i + v) * kWaves);
+            ssum += e[v];
+            zl[(i + v) * kStep] = e[v];
+        }
+    }
+    for (; i < mine; ++i) {
+        const float e = expo(zl[i * kStep], ln.wave + i * kWaves);
+        ssum += e;
+        zl[i * kStep] = e;
+    }
+#pragma unroll
+    for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
+    if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;
+    __syncthreads();  // also publishes every exponential to the V pass
+
+    // 3. V pass: acc[h][c][x] = sum over this lane's rows of e_h(row) * v(row)[(p + c LPR) EPC + x]
+    float acc[GP][CPL][EPC];
+#pragma unroll
+    for (int h = 0; h < GP; ++h)
+#pragma unroll
+        for (int c = 0; c < CPL; ++c)
+#pragma unroll
+            for (int x = 0; x < EPC; ++x) acc[h][c][x] = 0.0f;
+    {
+        chunk_t vbuf[kNbuf][RPG][CPL];
+        int ubuf[kNbuf];
+#pragma unroll
+        for (int j = 0; j < kNbuf - 1; ++j) {
+            ubuf[j] = claim(1);
+            ln.load_rows(vrs, ubuf[j], vbuf[j]);
+        }
+        bool more = true;
+        while (more) {
+#pragma unroll
+            for (int j = 0; j < kNbuf; ++j) {
+                const int slot = (j + kNbuf - 1) % kNbuf;
+                ubuf[slot] = claim(1);
+                ln.load_rows(vrs, ubuf[slot], vbuf[slot]);
+                if (more && ubuf[j] < nunits) {
+                    // row k * NG + grp of the unit: its GP probabilities are words grp * LPR + k * GP + [0, GP)
+                    const float* eu = zs + ubuf[j] * kWave + ln.grp * LPR;
+#pragma unroll
+                    for (int k = 0; k < RPG; ++k) {
+                        float e[GP];
+                        read_probs<GP>(eu + k * GP, e);
+#pragma unroll
+                        for (int c = 0; c < CPL; ++c) {
+                            float f[EPC];
+                            E::unpack(vbuf[j][k][c], f);
+#pragma unroll
+                            for (int h = 0; h < GP; ++h)
+#pragma unroll
+                                for (int x = 0; x < EPC; ++x) acc[h][c][x] = fmaf(e[h], f[x], acc[h][c][x]);
+                        }
+                    }
+                } else {
+                    more = false;
+                }
+            }
+        }
+    }
+
+    // 4. lanes holding the same chunk of different rows (stride LPR), then the waves in order
+#pragma unroll
+    for (int o = LPR; o < kWave; o <<= 1)
+#pragma unroll
+        for (int h = 0; h < GP; ++h)
+#pragma unroll
+            for (int c = 0; c < CPL; ++c)
+#pragma unroll
+                for (int x = 0; x < EPC; ++x) acc[h][c][x] += __shfl_xor(acc[h][c][x], o, kWave);
+    for (int w = 0; w < kWaves; ++w) {
+        if (ln.wave == w && ln.lane < LPR) {
+#pragma unroll
+            for (int h = 0; h < GP; ++h)
+#pragma unroll
+                for (int c = 0; c < CPL; ++c)
+#pragma unroll
+                    for (int x = 0; x < EPC; ++x) {
+                        const int idx = h * D + (ln.p + c * LPR) * EPC + x;
+                        obuf[idx] = w == 0 ? acc[h][c][x] : obuf[idx] + acc[h][c][x];
+                    }
+        }
+        __syncthreads();
+    }
+    auto head_sum = [&](int h) {
+        float t = red_s[0][h];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) t += red_s[w][h];
+        return t;
+    };
+    auto head_max = [&](int h) {
+        float t = red_m[0][h];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) t = fmaxf(t, red_m[w][h]);
+        return t;
+    };
+    const size_t head0 = (size_t)lb * a.hq + (size_t)g * a.group;
+    if (a.nchunk == 1) {
+        T* ob = static_cast<T*>(a.o) + head0 * D;
+        for (int idx = threadIdx.x; idx < a.group * D; idx += kThreads) {
+            const float tot = head_sum(idx / D);
+            E::store(ob + idx, tot > 0.0f ? obuf[idx] / tot : 0.0f);
+        }
+    } else {
+        for (int idx = threadIdx.x; idx < a.group * D; idx += kThreads) {
+            const int h = idx / D;
+            a.opart[((head0 + h) * a.nchunk + chunk) * D + idx % D] = obuf[idx];
+        }
+        if (threadIdx.x < a.group)
+            a.part[(head0 + threadIdx.x) * a.nchunk + chunk] =
+                make_float2(head_max(threadIdx.x), head_sum(threadIdx.x));
+    }
+
+    // 5. one chunk: the score's group probability sums, staged in each unit's first RPW words (only this
+    //    wave reads its units, and the V pass is over) and written with 16-byte stores
+    if (a.emit && a.nchunk == 1) {
+        static_assert(RPW % 4 == 0, "the coalesced store moves 4 rows at a time");
+        const float tot = head_sum(ln.hh);
+        const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
+        for (i = 0; i < mine; ++i) {
+            const float sum = group_allsum<GP>(zl[i * kStep] * inv);
+            if (ln.hh == 0) zs[(ln.wave + i * kWaves) * kWave + ln.kk * L::NG + ln.grp] = sum;
+        }
+        __syncthreads();
+        float* rrow = a.r + (size_t)s * a.n_stride;
+        for (int j = threadIdx.x; j * 4 < nrows; j += kThreads) {
+            const int row = j * 4;
+            *reinterpret_cast<f32x4*>(rrow + row) =
+                *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]);
+        }
+    }
+}
+
+// Several chunks per slab: o_h = sum_c exp(m_c - M) o_c / sum_c exp(m_c - M) S_c with M = max_c m_c.
+template <typename T>
+__global__ __launch_bounds__(128) void attend_finish_kernel(ScoreArgs a, int d) {
+    const size_t head = blockIdx.x;  // (l * batch + b) * n_q + h
+    const float2* pp = a.part + head * a.nchunk;
+    float mx = -INFINITY;
+    for (int c = 0; c < a.nchunk; ++c) mx = fmaxf(mx, pp[c].x);
+    const float* op = a.opart + head * a.nchunk * d + threadIdx.x;
+    float tot = 0.0f, acc = 0.0f;
+    for (int c = 0; c < a.nchunk; ++c) {
+        const float w = __expf(pp[c].x - mx);
+        tot = fmaf(w, pp[c].y, tot);
+        acc = fmaf(w, op[(size_t)c * d], acc);
+    }
+    Elem<T>::store(static_cast<T*>(a.o) + head * d + threadIdx.x, tot > 0.0f ? acc / tot : 0.0f);
+}
+
+template <typename T, int D, int GP>
+hipError_t launch_attend_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
+    if constexpr (Geometry<T, D, 1>::kLpr < GP) {
+        return hipErrorInvalidValue;
+    } else {
+        auto kern = attend_kernel<T, D, GP>;
+        if (plan.lds_bytes > 64 * 1024) {
+            static bool raised = false;  // idempotent attribute; a benign race between threads
+            if (!raised) {
+                hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax);
+                if (e != hipSuccess) return e;
+                raised = true;
+            }
+        }
+        hipLaunchKernelGGL(kern, dim3(plan.grid), dim3(kThreads), plan.lds_bytes, s, a);
+        return hipGetLastError();
+    }
+}
+
+template <typename T, int D>
+hipError_t launch_attend_d(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
+    switch (plan.group_pad) {
+        case 1: return launch_attend_gp<T, D, 1>(plan, a, s);
+        case 2: return launch_attend_gp<T, D, 2>(plan, a, s);
+        case 4: return launch_attend_gp<T, D, 4>(plan, a, s);
+        case 8: return launch_attend_gp<T, D, 8>(plan, a, s);
+        case 16: return launch_attend_gp<T, D, 16>(plan, a, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+bool attend_plan(int dtype, int head_dim, int group, int n, int slabs, ScorePlan* plan) {
+    if (slabs < 1 || !score_plan(dtype, head_dim, group, 1, plan)) return false;
+    const int rpw = kWave / plan->group_pad;  // rows per unit
+    const int lds_rows = (int)(kFastLdsMax / (kWave * sizeof(float))) * rpw;
+    const int want = (kAttnTargetWgs + slabs - 1) / slabs;
+    const int by_rows = (n + kAttnMinRows - 1) / kAttnMinRows;
+    int nchunk = (n + lds_rows - 1) / lds_rows;
+    nchunk = max(nchunk, min(want, by_rows));
+    int rows = (n + nchunk - 1) / nchunk;
+    rows = (rows + rpw - 1) / rpw * rpw;  // <= lds_rows, a multiple of rpw
+    plan->chunk_rows = rows;
+    plan->nchunk = (n + rows - 1) / rows;
+    plan->split = plan->nchunk > 1;
+    plan->lds_bytes = (size_t)(rows / rpw) * kWave * sizeof(float);
+    plan->grid = slabs * plan->nchunk;
+    return true;
+}
+
+AttendBound attend_bound(int dtype, int head_dim, int group, int n, int slabs_per_layer, int layers) {
+    AttendBound r{0, false};
+    ScorePlan p;
+    if (slabs_per_layer < 1 || layers < 1 || !score_plan(dtype, head_dim, group, 1, &p)) return r;
+    const int rpw = kWave / p.group_pad;
+    const long lds_rows = (long)(kFastLdsMax / (kWave * sizeof(float))) * rpw;
+    const long c0 = (n + lds_rows - 1) / lds_rows;
+    const long by_rows = (n + kAttnMinRows - 1) / kAttnMinRows;
+    const long want1 = (kAttnTargetWgs + slabs_per_layer - 1) / slabs_per_layer;
+    // a call over lc layers makes lc * nchunk(lc) chunks per slab column, nchunk = max(c0, min(want, by_rows))
+    // with want = ceil(target / (lc * slabs_per_layer)); lc * want <= target / slabs_per_layer + lc
+    const long by_target = layers * c0 > want1 + layers ? layers * c0 : want1 + layers;
+    const long by_size = layers * (c0 > by_rows ? c0 : by_rows);
+    r.chunk_layers = by_target < by_size ? by_target : by_size;
+    r.may_split = c0 > 1 || (by_rows > 1 && want1 > 1);
+    return r;
+}
+
+hipError_t launch_attend(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
+    if (dtype == 0) {
+        if (head_dim == 64) return launch_attend_d<float, 64>(plan, a, s);
+        if (head_dim == 128) return launch_attend_d<float, 128>(plan, a, s);
+    } else {
+        if (head_dim == 64) return launch_attend_d<bf16_t, 64>(plan, a, s);
+        if (head_dim == 128) return launch_attend_d<bf16_t, 128>(plan, a, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_attend_finish(int dtype, int head_dim, const ScoreArgs& a, hipStream_t s) {
+    const dim3 grid((unsigned)((size_t)a.layers * a.batch * a.hq));
+    if (dtype == 0)
+        hipLaunchKernelGGL(attend_finish_kernel<float>, grid, dim3(head_dim), 0, s, a, head_dim);
+    else
+        hipLaunchKernelGGL(attend_finish_kernel<bf16_t>, grid, dim3(head_dim), 0, s, a, head_dim);
+    return hipGetLastError();
+}
+
+}  // namespace ikv

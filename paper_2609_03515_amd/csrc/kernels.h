@@ -25,6 +25,11 @@ struct ScoreArgs {
     float bias;
     float scale;      // 1 / sqrt(d)
     int chunk_rows, nchunk;
+    // fused decode attention only
+    const void* v;  // V cache, same layout as k
+    void* o;        // [layers][batch][n_q][d] attention output (dtype of q)
+    float* opart;   // split: [layers][batch][n_q][nchunk][d] unnormalised partial outputs
+    int emit;       // nonzero: also produce the eviction score (r)
 };
 
 struct ScorePlan {
@@ -41,6 +46,20 @@ struct ScorePlan {
 bool score_plan(int dtype, int head_dim, int group, int n, ScorePlan* plan);
 hipError_t launch_score(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s);
 hipError_t launch_split_finish(const ScoreArgs& a, hipStream_t s);
+
+// Decode attention fused with the score: o_h = sum_i a_h(i) v_i for every query head, and (when emit) the
+// same r as the scorer.  The plan cuts each slab into nchunk row ranges so that `slabs` slabs fill the chip;
+// with nchunk > 1 the chunks write partial outputs / logits that the finish kernels combine.
+bool attend_plan(int dtype, int head_dim, int group, int n, int slabs, ScorePlan* plan);
+// Workspace bound over every call of 1..layers layers on n rows: the largest (layers of the call) x nchunk,
+// and whether any such call splits.
+struct AttendBound {
+    long chunk_layers;
+    bool may_split;
+};
+AttendBound attend_bound(int dtype, int head_dim, int group, int n, int slabs_per_layer, int layers);
+hipError_t launch_attend(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s);
+hipError_t launch_attend_finish(int dtype, int head_dim, const ScoreArgs& a, hipStream_t s);
 
 // Layer fold (Eq. 2-4): u <- prior_w * u + sum_l w_l s_l with s_l = (1/H) sum_g r_{l,g}.
 struct FoldArgs {

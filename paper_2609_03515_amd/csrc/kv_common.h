@@ -109,6 +109,13 @@ struct Elem<float> {
         acc = fmaf(k.w, q.w, acc);
         return acc;
     }
+    __device__ __forceinline__ static void unpack(const chunk_t& c, float (&f)[kPerChunk]) {
+        f[0] = c.x;
+        f[1] = c.y;
+        f[2] = c.z;
+        f[3] = c.w;
+    }
+    __device__ __forceinline__ static void store(float* dst, float x) { *dst = x; }
 };
 
 struct bf16_t {
@@ -129,6 +136,20 @@ struct Elem<bf16_t> {
         acc = dot2(k.z, q.z, acc);
         acc = dot2(k.w, q.w, acc);
         return acc;
+    }
+    // bf16 -> f32 is exact: the bf16 bits are the high half of the f32 bits
+    __device__ __forceinline__ static void unpack(const chunk_t& c, float (&f)[kPerChunk]) {
+        const uint32_t w[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            f[2 * i] = __uint_as_float(w[i] << 16);
+            f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+        }
+    }
+    // f32 -> bf16 rounding to nearest, ties to even (inputs are finite)
+    __device__ __forceinline__ static void store(bf16_t* dst, float x) {
+        const uint32_t b = __float_as_uint(x);
+        dst->bits = (uint16_t)((b + 0x7fffu + ((b >> 16) & 1u)) >> 16);
     }
 };
 

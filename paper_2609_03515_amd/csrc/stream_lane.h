@@ -1,0 +1,175 @@
+// Streaming machinery shared by the scorer and the fused decode-attention kernels: one workgroup of 8 waves
+// streams rows of a (layer, sequence, KV head) slab with raw buffer loads; a K row is split into 16-byte
+// chunks over an aligned group of LPR lanes, each lane accumulates the partial dot products of RPG rows with
+// the GP (padded) query heads of its group, and a DPP reduce-scatter leaves each lane with one full
+// (row, head) logit.
+#pragma once
+
+#include "kernels.h"
+#include "kv_common.h"
+
+namespace ikv {
+namespace {
+
+#ifndef IKV_SCORE_WAVES
+#define IKV_SCORE_WAVES 8
+#endif
+#ifndef IKV_NT_LOADS
+#define IKV_NT_LOADS 1
+#endif
+#ifndef IKV_NBUF
+#define IKV_NBUF 0
+#endif
+#ifndef IKV_LPR
+#define IKV_LPR 16
+#endif
+
+constexpr size_t kFastLdsMax = 80 * 1024;  // keep >= 2 workgroups per CU (160 KiB LDS)
+constexpr int kWaves = IKV_SCORE_WAVES;
+constexpr int kThreads = kWaves * kWave;
+constexpr int kSplitIters = 16;
+constexpr float kFloor = -1.0e30f;  // finite start of running maxima: exp(-inf - floor) = 0, no NaN
+constexpr int kNonTemporal = 2;     // buffer-load cache policy: K is streamed once, no reuse to cache for
+constexpr int kRsrcConfig = 0x00020000;  // raw (unformatted, stride 0) buffer resource, gfx9 family
+
+// Raw buffer resource over `bytes` bytes at `base` (reads at offsets >= bytes return zero).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kRsrcConfig);
+}
+
+template <typename T, int D, int GP>
+struct Geometry {
+    using E = Elem<T>;
+    static constexpr int kEpc = E::kPerChunk;
+    static constexpr int kChunks = D / kEpc;
+    static constexpr int kLpr = kChunks >= IKV_LPR ? IKV_LPR : kChunks;
+    static constexpr int kCpl = kChunks / kLpr;
+    static constexpr int kNg = kWave / kLpr;
+    static constexpr int kRpg = kLpr / GP;
+    static constexpr int kRpw = kNg * kRpg;
+    static constexpr int kRpi = kWaves * kRpw;
+    static_assert(kRpg * GP == kLpr, "group must not exceed the lanes of a row");
+    // K loads of this many loop iterations are in flight per lane.  The LDS path claims its rows dynamically
+    // and measured best with 2 (more buffers cost occupancy without raising the stream rate).  The split path
+    // streams static chunks and measured best with 4 when a lane loads four 16-byte chunks per iteration, 3 for
+    // wider groups (more arithmetic per byte), 2 when a lane loads more than four chunks per iteration.
+    static constexpr int kNbufLds = IKV_NBUF > 0 ? IKV_NBUF : 2;
+    static constexpr int kNbufSplit = IKV_NBUF > 0 ? IKV_NBUF : (kRpg * kCpl > 4 ? 2 : (GP <= 4 ? 4 : 3));
+    // Registers of the streaming loop: the K buffers in flight, the queries, the partial dot products and
+    // bookkeeping.  LDS holds about 3 workgroups per CU at the graded shapes, so ask the compiler for the
+    // matching waves per SIMD when the loop fits that register budget; otherwise leave it unconstrained
+    // rather than spill.
+    static constexpr int kWantWaves = (3 * kWaves + 3) / 4;
+    static constexpr int min_waves(int nbuf) {
+#ifdef IKV_MIN_WAVES
+        return IKV_MIN_WAVES;
+#else
+        return nbuf * kRpg * kCpl * 4 + GP * kCpl * 4 + kLpr + 16 <= (512 / kWantWaves) / 8 * 8 ? kWantWaves : 1;
+#endif
+    }
+    static constexpr int kMinWavesLds = min_waves(kNbufLds);
+    static constexpr int kMinWavesSplit = min_waves(kNbufSplit);
+};
+
+// Per-lane streaming machinery shared by both paths.
+template <typename T, int D, int GP>
+struct Lane {
+    using Gm = Geometry<T, D, GP>;
+    using E = Elem<T>;
+    using chunk_t = typename E::chunk_t;
+    static constexpr int LPR = Gm::kLpr, CPL = Gm::kCpl, NG = Gm::kNg, RPG = Gm::kRpg, RPW = Gm::kRpw;
+    static constexpr int RPI = Gm::kRpi, EPC = Gm::kEpc;
+
+    int lane, wave, grp, p, hh, kk;
+
+    __device__ Lane() {
+        lane = threadIdx.x & (kWave - 1);
+        wave = threadIdx.x / kWave;
+        grp = lane / LPR;
+        p = lane % LPR;
+        hh = p % GP;  // head owned after the reduce-scatter
+        kk = p / GP;  // row slot owned after the reduce-scatter
+    }
+
+    // Row of iteration `it` owned by this lane after the reduce-scatter.
+    __device__ int owned_row(int row0, int it) const { return row0 + it * RPI + wave * RPW + kk * NG + grp; }
+
+    __device__ void load_q(const ScoreArgs& a, size_t lb, int g, chunk_t (&qv)[GP][CPL]) const {
+        const T* qg = static_cast<const T*>(a.q) + (lb * a.hq + (size_t)g * a.group) * D;
+#pragma unroll
+        for (int h = 0; h < GP; ++h)
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+                if (h < a.group)
+                    qv[h][c] = *reinterpret_cast<const chunk_t*>(qg + h * D + (p + c * LPR) * EPC);
+                else
+                    qv[h][c] = chunk_t{};
+            }
+    }
+
+    // K rows and positions are read with raw buffer loads over the range's rows: 32-bit lane offsets with
+    // immediate row/chunk offsets, and reads past the range return zero instead of needing a clamp (those
+    // logits are masked).  Loads are unconditional, so the compiler keeps the next iterations' loads in flight
+    // while the current one is reduced.  The position of the row this lane will own comes with the same batch
+    // (it decides the recency bias).
+    static constexpr int kRowBytes = D * (int)sizeof(T);
+    __device__ void load(__amdgpu_buffer_rsrc_t krs, __amdgpu_buffer_rsrc_t prs, int row0, int it,
+                         chunk_t (&dst)[RPG][CPL], int& pdst) const {
+        const int base = row0 + it * RPI + wave * RPW + grp;
+        const int off = base * kRowBytes + p * 16;
+#pragma unroll
+        for (int k = 0; k < RPG; ++k)
+#pragma unroll
+            for (int c = 0; c < CPL; ++c)
+                dst[k][c] = __builtin_bit_cast(
+                    chunk_t, __builtin_amdgcn_raw_buffer_load_b128(krs, off + k * NG * kRowBytes + c * LPR * 16, 0,
+                                                                   IKV_NT_LOADS ? kNonTemporal : 0));
+        pdst = (int)__builtin_amdgcn_raw_buffer_load_b32(prs, (base + kk * NG) * 4, 0, 0);
+    }
+
+    // Unit u = the RPW consecutive rows [u * RPW, (u + 1) * RPW) one wave covers in one step.
+    __device__ int unit_row(int u) const { return u * RPW + kk * NG + grp; }
+    // This lane's chunks of the unit's rows: row u * RPW + k * NG + grp for k < RPG, chunks p + c * LPR.
+    __device__ void load_rows(__amdgpu_buffer_rsrc_t rs, int u, chunk_t (&dst)[RPG][CPL]) const {
+        const int off = (u * RPW + grp) * kRowBytes + p * 16;
+#pragma unroll
+        for (int k = 0; k < RPG; ++k)
+#pragma unroll
+            for (int c = 0; c < CPL; ++c)
+                dst[k][c] = __builtin_bit_cast(
+                    chunk_t, __builtin_amdgcn_raw_buffer_load_b128(rs, off + k * NG * kRowBytes + c * LPR * 16, 0,
+                                                                   IKV_NT_LOADS ? kNonTemporal : 0));
+    }
+    __device__ void load_unit(__amdgpu_buffer_rsrc_t krs, __amdgpu_buffer_rsrc_t prs, int u, chunk_t (&dst)[RPG][CPL],
+                              int& pdst) const {
+        load_rows(krs, u, dst);
+        pdst = (int)__builtin_amdgcn_raw_buffer_load_b32(prs, unit_row(u) * 4, 0, 0);
+    }
+
+    // Logit of the (row, head) this lane owns for one iteration; -inf when masked (a padded head, or a row
+    // past the end of the range).
+    __device__ float logit(const ScoreArgs& a, const chunk_t (&kb)[RPG][CPL], const chunk_t (&qv)[GP][CPL],
+                           int posv, int row, int row_end) const {
+        float v[LPR];
+#pragma unroll
+        for (int k = 0; k < RPG; ++k)
+#pragma unroll
+            for (int h = 0; h < GP; ++h) {
+                float acc = 0.0f;
+#pragma unroll
+                for (int c = 0; c < CPL; ++c) acc = E::dot(kb[k][c], qv[h][c], acc);
+                v[k * GP + h] = acc;
+            }
+        const float dotv = reduce_scatter<LPR>(v, p);
+        const float z = fmaf(dotv, a.scale, posv >= a.recent_from ? a.bias : 0.0f);
+        return (row < row_end && hh < a.group) ? z : -INFINITY;
+    }
+};
+
+#ifndef IKV_EPI_UNROLL
+#define IKV_EPI_UNROLL 8
+#endif
+constexpr int kEpi = IKV_EPI_UNROLL;  // epilogue LDS reads kept in flight per lane
+
+}  // namespace
+}  // namespace ikv

@@ -145,3 +145,61 @@ def test_step_validation(lib):
     assert _step(s, good, k=FAKE + 2)[0] == B.KV_ERR_UNSUPPORTED
     rc, out = _step(s, good)
     assert rc == B.KV_ERR_WORKSPACE and out == -7                      # nothing written on failure
+
+
+def test_append_validation(lib):
+    s = shape()
+    good = B.make_params(0.9, 20)
+    L = lib_()
+
+    def call(p=good, t=1, n_in=10, new_pos=5, k_new=FAKE, k=FAKE, u=FAKE):
+        return L.kv_append(ctypes.byref(s), ctypes.byref(p) if p is not None else None, t, n_in, new_pos, k_new,
+                           FAKE, k, FAKE, u, FAKE, None)
+    assert call(p=None) == B.KV_ERR_INVALID_ARG
+    assert call(p=B.make_params(0.9, 0)) == B.KV_ERR_INVALID_ARG
+    assert call(t=0) == B.KV_ERR_INVALID_ARG
+    assert call(n_in=100) == B.KV_ERR_INVALID_ARG
+    assert call(new_pos=-1) == B.KV_ERR_INVALID_ARG
+    assert call(k_new=None) == B.KV_ERR_INVALID_ARG
+    assert call(k=FAKE + 8) == B.KV_ERR_UNSUPPORTED
+    assert call(u=FAKE + 2) == B.KV_ERR_UNSUPPORTED
+
+
+def test_attend_validation(lib):
+    s = shape()   # 3 layers
+    L = lib_()
+    need = B.kv_workspace_bytes(s, 10)
+
+    def call(layer0=0, count=3, n=10, q=FAKE, o=FAKE, window=0, ws=FAKE, ws_bytes=need):
+        return L.kv_attend_score(ctypes.byref(s), layer0, count, n, q, FAKE, FAKE, FAKE, 9, 0.5, window, 1, o,
+                                 ws, ws_bytes, None)
+    assert call(layer0=-1) == B.KV_ERR_INVALID_ARG
+    assert call(count=0) == B.KV_ERR_INVALID_ARG
+    assert call(layer0=2, count=2) == B.KV_ERR_INVALID_ARG        # past the last layer
+    assert call(n=0) == B.KV_ERR_INVALID_ARG
+    assert call(n=101) == B.KV_ERR_INVALID_ARG
+    assert call(window=-2) == B.KV_ERR_INVALID_ARG
+    assert call(o=None) == B.KV_ERR_INVALID_ARG
+    assert call(q=FAKE + 4) == B.KV_ERR_UNSUPPORTED
+    assert call(o=FAKE + 1) == B.KV_ERR_UNSUPPORTED                # bf16 output needs 2-byte alignment
+    assert call(ws=None, ws_bytes=0) == B.KV_ERR_WORKSPACE
+    assert call(ws_bytes=need - 1) == B.KV_ERR_WORKSPACE
+
+
+def test_finish_validation(lib):
+    s = shape()
+    good = B.make_params(0.9, 20)
+    L = lib_()
+    out = ctypes.c_int32(-7)
+
+    def call(p=good, t=1, n=10, k=FAKE, n_out=True, ws=None, ws_bytes=0):
+        return L.kv_evict_finish(ctypes.byref(s), ctypes.byref(p) if p is not None else None, t, n, k, FAKE, FAKE,
+                                 FAKE, ctypes.byref(out) if n_out else None, None, None, ws, ws_bytes, None)
+    assert call(p=None) == B.KV_ERR_INVALID_ARG
+    assert call(t=0) == B.KV_ERR_INVALID_ARG
+    assert call(n=0) == B.KV_ERR_INVALID_ARG
+    assert call(n=101) == B.KV_ERR_INVALID_ARG
+    assert call(n_out=False) == B.KV_ERR_INVALID_ARG
+    assert call(k=FAKE + 8) == B.KV_ERR_UNSUPPORTED
+    assert call() == B.KV_ERR_WORKSPACE and out.value == -7
+
