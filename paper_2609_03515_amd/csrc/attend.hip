@@ -21,8 +21,14 @@
 namespace ikv {
 namespace {
 
-constexpr int kAttnTargetWgs = 1024;  // workgroups per launch wanted: four per CU
-constexpr int kAttnMinRows = 256;     // smallest chunk: below it a chunk's fixed costs dominate its stream
+#ifndef IKV_ATTN_TARGET
+#define IKV_ATTN_TARGET 512
+#endif
+#ifndef IKV_ATTN_MIN_ROWS
+#define IKV_ATTN_MIN_ROWS 256
+#endif
+constexpr int kAttnTargetWgs = IKV_ATTN_TARGET;   // workgroups per launch wanted: two per CU
+constexpr int kAttnMinRows = IKV_ATTN_MIN_ROWS;   // smallest chunk: below it a chunk's fixed costs dominate
 
 template <int GP>
 __device__ __forceinline__ void read_probs(const float* src, float (&e)[GP]) {
