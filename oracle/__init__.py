@@ -5,7 +5,7 @@ the HIP library and its binding never do, and the two share no code.
 """
 from .inertiakv import (  # noqa: F401
     BF16, CUMULATIVE, EMA, F32, SINGLE_STEP, Cache, Params, StepResult, attention_output, budget_from_ratio,
-    compact_rows,
+    compact_rows, layer_scores_variant, normalized_entropy, value_norm_weights,
     evict_step, fold_layers, head_attention, holefill_moves, layer_scores, new_token_prior, refresh_due,
     select_keep, to_f64,
 )

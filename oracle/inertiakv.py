@@ -13,6 +13,8 @@ Each function names the passage it follows:
   shared by its query-head group before pooling.
 * Eq. 2 / 3 / 4: single-step, cumulative and EMA aggregation rules.
 * The step's decode attention (the softmax Eq. 1 pools, applied to V), for the fused attention + score path.
+* Sec. 5.1 / appendix "Per-step scoring": VNorm (attention times the mean-normalised l2 norm of the value
+  row) and entropy weighting (the layer's score times the normalised entropy of its attention).
 * Appendix "Implementation Details / Layer scoring": the EMA state is updated after every eligible layer,
   m_{t,l} = alpha m_{t,l-1} + (1 - alpha) s_{t,l}, l = 1..K, m_{t,0} = m_{t-1,K}.
 * Appendix "Implementation Details / Momentum initialization": m_0 = 0 for every prefill position.
@@ -36,6 +38,9 @@ Readings where the paper is silent (the same list is kept in the design notes):
   evicted slots < k, in ascending order.  Attention is invariant to row order, so any layout is faithful;
   this one moves the fewest rows.
 * Non-refresh initialisation policy "min" (lowest existing utility) is offered beside the paper's "mean".
+* VNorm's mean runs over the cached tokens of the same layer and KV head at scoring time; entropy weighting
+  uses the entropy of the layer's pooled attention (before VNorm) divided by ln(n), per sequence; with both
+  enabled the entropy factor multiplies the VNorm-weighted score.
 """
 from __future__ import annotations
 
@@ -114,6 +119,52 @@ def layer_scores(q_l: np.ndarray, keys_l: np.ndarray, pos: np.ndarray | None = N
     for h in range(hq):
         s += head_attention(q_l[h], keys_l[h // group], pos, cur_pos, recency_bias, recency_window)
     return s / hq
+
+
+# ----------------------------------------------------------------------------------------------------------
+# Sec. 5.1 and appendix "Per-step scoring": the two order-preserving scorer perturbations
+# ----------------------------------------------------------------------------------------------------------
+def value_norm_weights(values_g: np.ndarray) -> np.ndarray:
+    """VNorm factor of every cached token of one KV head: the l2 norm of its value row divided by the mean
+    of those norms over the cached tokens (so the factors average to 1).  All-zero values: factor 1."""
+    norms = np.sqrt(np.sum(values_g * values_g, axis=-1))
+    mean = norms.mean()
+    return norms / mean if mean > 0 else np.ones_like(norms)
+
+
+def normalized_entropy(s: np.ndarray) -> float:
+    """Entropy of the distribution s (normalised to sum 1) divided by its maximum ln(n); 1 when n = 1."""
+    n = len(s)
+    if n <= 1:
+        return 1.0
+    p = s / s.sum()
+    nz = p > 0
+    return float(-np.sum(p[nz] * np.log(p[nz])) / math.log(n))
+
+
+def layer_scores_variant(q_l: np.ndarray, keys_l: np.ndarray, values_l: np.ndarray, pos: np.ndarray | None,
+                         cur_pos: int, recency_bias: float, recency_window: int, vnorm: bool,
+                         entropy: bool) -> np.ndarray:
+    """Eq. 1 with the optional perturbations, both applied to the step's score before the fold:
+    VNorm multiplies each head's attention a^(h)(i) by the VNorm factor of token i under that head's KV
+    head before pooling; entropy weighting multiplies the layer's pooled score by the normalised entropy
+    of the layer's pooled attention distribution (a per-layer, per-sequence scalar)."""
+    hq, hkv = q_l.shape[0], keys_l.shape[0]
+    if hq % hkv:
+        raise ValueError("query heads must be a multiple of KV heads")
+    group = hq // hkv
+    nu = [value_norm_weights(values_l[g]) for g in range(hkv)] if vnorm else None
+    s = np.zeros(keys_l.shape[1], dtype=np.float64)
+    s_attn = np.zeros_like(s)
+    for h in range(hq):
+        a = head_attention(q_l[h], keys_l[h // group], pos, cur_pos, recency_bias, recency_window)
+        s_attn += a
+        s += a * nu[h // group] if vnorm else a
+    s /= hq
+    s_attn /= hq
+    if entropy:
+        s = s * normalized_entropy(s_attn)
+    return s
 
 
 # ----------------------------------------------------------------------------------------------------------
@@ -207,6 +258,8 @@ class Params:
     recency_bias: float = 0.0
     recency_window: int = 0
     rule: str = EMA
+    vnorm: bool = False                # Sec. 5.1 scorer perturbations
+    entropy: bool = False
 
 
 @dataclass
@@ -304,8 +357,13 @@ def evict_step(cache: Cache, q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray
             for l in range(nl):
                 keys = to_f64(cache.k[l, b, :, :n, :], cache.dtype)
                 ql = to_f64(q[l, b], cache.dtype)
-                s_all[l, b] = layer_scores(ql, keys, cache.pos[b, :n], new_pos,
-                                           params.recency_bias, params.recency_window)
+                if params.vnorm or params.entropy:
+                    s_all[l, b] = layer_scores_variant(ql, keys, to_f64(cache.v[l, b, :, :n, :], cache.dtype),
+                                                       cache.pos[b, :n], new_pos, params.recency_bias,
+                                                       params.recency_window, params.vnorm, params.entropy)
+                else:
+                    s_all[l, b] = layer_scores(ql, keys, cache.pos[b, :n], new_pos,
+                                               params.recency_bias, params.recency_window)
             cache.u[b, :n] = fold_layers(cache.u[b, :n], s_all[:, b], params.alpha, params.rule)
     u_pre = cache.u[:, :n].copy()
 
