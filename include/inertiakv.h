@@ -59,6 +59,16 @@ typedef enum { KV_INIT_MEAN = 0, KV_INIT_MIN = 1 } kv_init;
  * cumulative u <- u + s_l. */
 typedef enum { KV_RULE_EMA = 0, KV_RULE_SINGLE_STEP = 1, KV_RULE_CUMULATIVE = 2 } kv_rule;
 
+/* Scorer perturbations of Sec. 5.1 (implementation appendix "Per-step scoring"), a bit mask applied to the
+ * score of every refresh step before the fold (kv_evict_step, kv_evict_finish; kv_score_ema is plain Eq. 1):
+ *  KV_SCORE_VNORM:   head h's attention to token i is multiplied by |v_i| / mean_j |v_j|, the l2 norm of
+ *                    token i's value row under h's KV head over the mean of those norms over the n cached
+ *                    tokens of that layer and KV head (factor 1 if all those norms are zero);
+ *  KV_SCORE_ENTROPY: the layer's pooled score is multiplied by the entropy of the layer's pooled attention
+ *                    distribution (before VNorm) divided by ln n, one factor per layer and sequence (1 if
+ *                    n = 1).  s_out then holds the perturbed scores that were folded. */
+typedef enum { KV_SCORE_ATTENTION = 0, KV_SCORE_VNORM = 1, KV_SCORE_ENTROPY = 2 } kv_score_variant;
+
 typedef struct {
     int32_t batch;      /* sequences                                   >= 1              */
     int32_t layers;     /* eligible layers K, folded in ascending order 1..256           */
@@ -78,6 +88,7 @@ typedef struct {
     float recency_bias;     /* added to logits of the `recency_window` newest positions; 0 = off    */
     int32_t recency_window; /* positions p >= new_pos - (window - 1) get the bias                   */
     int32_t rule;           /* kv_rule                                                             */
+    int32_t score_variant;  /* kv_score_variant bits (0 = the attention score of Eq. 1)             */
 } kv_params;
 
 /* Optional timing hooks: when an entry is non-NULL, kv_evict_step records that hipEvent_t on its stream

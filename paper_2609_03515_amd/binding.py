@@ -18,6 +18,7 @@ KV_OK, KV_ERR_INVALID_ARG, KV_ERR_UNSUPPORTED, KV_ERR_WORKSPACE, KV_ERR_HIP = 0,
 KV_F32, KV_BF16 = 0, 1
 KV_INIT_MEAN, KV_INIT_MIN = 0, 1
 KV_RULE_EMA, KV_RULE_SINGLE_STEP, KV_RULE_CUMULATIVE = 0, 1, 2
+KV_SCORE_ATTENTION, KV_SCORE_VNORM, KV_SCORE_ENTROPY = 0, 1, 2
 KV_PHASES = 5
 PHASES = ("append", "score", "fold", "select", "compact")
 
@@ -40,7 +41,8 @@ class KvShape(ctypes.Structure):
 class KvParams(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_float), ("budget", ctypes.c_int32), ("refresh_period", ctypes.c_int32),
                 ("score_free", ctypes.c_int32), ("nonrefresh_init", ctypes.c_int32),
-                ("recency_bias", ctypes.c_float), ("recency_window", ctypes.c_int32), ("rule", ctypes.c_int32)]
+                ("recency_bias", ctypes.c_float), ("recency_window", ctypes.c_int32), ("rule", ctypes.c_int32),
+                ("score_variant", ctypes.c_int32)]
 
 
 class KvTrace(ctypes.Structure):
@@ -111,13 +113,14 @@ def make_shape(batch, layers, n_q_heads, n_kv_heads, head_dim, capacity, dtype) 
 
 
 def make_params(alpha, budget, refresh_period=1, score_free=False, nonrefresh_init="mean", recency_bias=0.0,
-                recency_window=0, rule="ema") -> KvParams:
+                recency_window=0, rule="ema", vnorm=False, entropy=False) -> KvParams:
     init = {"mean": KV_INIT_MEAN, "min": KV_INIT_MIN}[nonrefresh_init] if isinstance(nonrefresh_init, str) \
         else int(nonrefresh_init)
     rl = {"ema": KV_RULE_EMA, "single": KV_RULE_SINGLE_STEP, "cumulative": KV_RULE_CUMULATIVE}[rule] \
         if isinstance(rule, str) else int(rule)
+    variant = (KV_SCORE_VNORM if vnorm else 0) | (KV_SCORE_ENTROPY if entropy else 0)
     return KvParams(float(alpha), int(budget), int(refresh_period), int(bool(score_free)), init,
-                    float(recency_bias), int(recency_window), rl)
+                    float(recency_bias), int(recency_window), rl, variant)
 
 
 def kv_workspace_bytes(shape: KvShape, n_max: int) -> int:

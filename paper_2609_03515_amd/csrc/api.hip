@@ -14,7 +14,7 @@ struct Layout {
     int n_stride;
     int max_pairs;
     ScorePlan plan;
-    size_t r_off, z_off, part_off, opart_off, pdst_off, psrc_off, np_off, total;
+    size_t r_off, z_off, part_off, opart_off, vn_off, vinv_off, eta_off, pdst_off, psrc_off, np_off, total;
 };
 
 int esize(const kv_shape& s) { return s.dtype == KV_F32 ? 4 : 2; }
@@ -62,6 +62,12 @@ Layout layout_for(const kv_shape& s, int n) {
     off = align256(off + (part_score > part_attn ? part_score : part_attn));
     L.opart_off = off;
     off = align256(off + (size_t)ab.chunk_layers * s.batch * s.n_q_heads * s.head_dim * sizeof(float));
+    L.vn_off = off;
+    off = align256(off + (size_t)s.layers * s.batch * s.n_kv_heads * L.n_stride * sizeof(float));
+    L.vinv_off = off;
+    off = align256(off + (size_t)s.layers * s.batch * s.n_kv_heads * sizeof(float));
+    L.eta_off = off;
+    off = align256(off + (size_t)s.layers * s.batch * sizeof(float));
     L.pdst_off = off;
     off = align256(off + (size_t)s.batch * L.max_pairs * sizeof(int32_t));
     L.psrc_off = off;
@@ -124,18 +130,42 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
     a.nchunk = L.plan.nchunk;
     ScorePlan plan = L.plan;
     plan.grid = s.layers * s.batch * s.n_kv_heads * plan.nchunk;
-    record(tr, 1, true, st);
     kv_status rc = hip_status(launch_score(s.dtype, s.head_dim, plan, a, st));
     if (rc == KV_OK && plan.split) rc = hip_status(launch_split_finish(a, st));
-    record(tr, 1, false, st);
+    return rc;
+}
+
+// Scorer perturbations (Sec. 5.1) of a refresh step: value-row norms and entropy factors for the fold.
+kv_status run_variants(const kv_shape& s, const Layout& L, int n, const void* v, int variant, void* ws,
+                       hipStream_t st) {
+    if (!variant) return KV_OK;
+    VariantArgs a{};
+    a.v = v;
+    a.r = at<float>(ws, L.r_off);
+    a.vnorm = at<float>(ws, L.vn_off);
+    a.vnorm_inv_mean = at<float>(ws, L.vinv_off);
+    a.entropy = at<float>(ws, L.eta_off);
+    a.batch = s.batch;
+    a.layers = s.layers;
+    a.hkv = s.n_kv_heads;
+    a.cap = s.capacity;
+    a.n = n;
+    a.n_stride = L.n_stride;
+    a.inv_hq = 1.0f / (float)s.n_q_heads;
+    kv_status rc = KV_OK;
+    if (variant & KV_SCORE_ENTROPY) rc = hip_status(launch_entropy(a, st));
+    if (rc == KV_OK && (variant & KV_SCORE_VNORM)) rc = hip_status(launch_vnorm(s.dtype, s.head_dim, a, st));
     return rc;
 }
 
 // Layer fold of the workspace r into u (Eq. 2-4 by `rule`).
 kv_status run_fold(const kv_shape& s, const Layout& L, int n, float* u, float* s_out, int rule, float alpha,
-                   void* ws, hipStream_t st, const kv_trace* tr) {
+                   int variant, void* ws, hipStream_t st, const kv_trace* tr) {
     FoldArgs f{};
     f.r = at<float>(ws, L.r_off);
+    f.vnorm = (variant & KV_SCORE_VNORM) ? at<float>(ws, L.vn_off) : nullptr;
+    f.vnorm_inv_mean = at<float>(ws, L.vinv_off);
+    f.entropy = (variant & KV_SCORE_ENTROPY) ? at<float>(ws, L.eta_off) : nullptr;
     f.u = u;
     f.s_out = s_out;
     f.batch = s.batch;
@@ -213,6 +243,7 @@ kv_status check_params(const kv_params* params) {
     if (p.nonrefresh_init != KV_INIT_MEAN && p.nonrefresh_init != KV_INIT_MIN) return KV_ERR_INVALID_ARG;
     if (p.rule < KV_RULE_EMA || p.rule > KV_RULE_CUMULATIVE) return KV_ERR_INVALID_ARG;
     if (p.recency_window < 0 || !isfinite(p.recency_bias)) return KV_ERR_INVALID_ARG;
+    if (p.score_variant & ~(KV_SCORE_VNORM | KV_SCORE_ENTROPY)) return KV_ERR_INVALID_ARG;
     return KV_OK;
 }
 
@@ -291,7 +322,7 @@ kv_status kv_score_ema(const kv_shape* shape, int32_t n, const void* q, const vo
     hipStream_t st = static_cast<hipStream_t>(stream);
     if ((rc = run_score(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws, st, nullptr)) != KV_OK)
         return rc;
-    return run_fold(s, L, n, u, s_out, KV_RULE_EMA, alpha, ws, st, nullptr);
+    return run_fold(s, L, n, u, s_out, KV_RULE_EMA, alpha, 0, ws, st, nullptr);
 }
 
 kv_status kv_topk_select(const kv_shape* shape, int32_t n, int32_t budget, const float* u, const int32_t* pos,
@@ -349,8 +380,11 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
 
     if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, st, trace)) != KV_OK) return rc;
     if (is_refresh(p, t)) {
+        record(trace, 1, true, st);
         rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, ws, st, trace);
-        if (rc == KV_OK) rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, ws, st, trace);
+        if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, ws, st);
+        record(trace, 1, false, st);
+        if (rc == KV_OK) rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, ws, st, trace);
         if (rc != KV_OK) return rc;
     }
     if ((rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, ws, st, trace)) != KV_OK) return rc;
@@ -427,8 +461,11 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
     const Layout L = layout_for(s, n);
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (is_refresh(p, t) && (rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, ws, st, nullptr)) != KV_OK)
-        return rc;
+    if (is_refresh(p, t)) {
+        if ((rc = run_variants(s, L, n, v, p.score_variant, ws, st)) != KV_OK) return rc;
+        if ((rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, ws, st, nullptr)) != KV_OK)
+            return rc;
+    }
     if ((rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, ws, st, nullptr)) != KV_OK) return rc;
     *n_out = n < p.budget ? n : p.budget;
     return KV_OK;

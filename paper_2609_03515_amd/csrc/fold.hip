@@ -27,8 +27,23 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
         for (int l = slice; l < a.layers; l += kSlices) {
             const float* rl = a.r + ((size_t)(l * a.batch + b) * a.hkv) * a.n_stride + tok0;
             f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
-            for (int g = 0; g < a.hkv; ++g) s += *reinterpret_cast<const f32x4*>(rl + (size_t)g * a.n_stride);
+            if (a.vnorm) {
+                // VNorm: each KV head's group sum times the token's value-norm factor norm / mean norm
+                // (factor 1 where the slab's norms are all zero)
+                const float* nl = a.vnorm + ((size_t)(l * a.batch + b) * a.hkv) * a.n_stride + tok0;
+                const float* il = a.vnorm_inv_mean + (size_t)(l * a.batch + b) * a.hkv;
+                for (int g = 0; g < a.hkv; ++g) {
+                    const f32x4 rg = *reinterpret_cast<const f32x4*>(rl + (size_t)g * a.n_stride);
+                    const float im = il[g];
+                    const f32x4 f = im > 0.0f ? *reinterpret_cast<const f32x4*>(nl + (size_t)g * a.n_stride) * im
+                                              : f32x4{1.0f, 1.0f, 1.0f, 1.0f};
+                    s += rg * f;
+                }
+            } else {
+                for (int g = 0; g < a.hkv; ++g) s += *reinterpret_cast<const f32x4*>(rl + (size_t)g * a.n_stride);
+            }
             s *= a.inv_hq;
+            if (a.entropy) s *= a.entropy[l * a.batch + b];  // entropy weighting: one factor per layer and sequence
             if (a.s_out) {
                 float* so = a.s_out + ((size_t)l * a.batch + b) * a.n + tok0;
 #pragma unroll

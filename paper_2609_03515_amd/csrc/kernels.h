@@ -64,6 +64,9 @@ hipError_t launch_attend_finish(int dtype, int head_dim, const ScoreArgs& a, hip
 // Layer fold (Eq. 2-4): u <- prior_w * u + sum_l w_l s_l with s_l = (1/H) sum_g r_{l,g}.
 struct FoldArgs {
     const float* r;
+    const float* vnorm;           // nullable: [layers][batch][n_kv][n_stride] value-row l2 norms
+    const float* vnorm_inv_mean;  // [layers][batch][n_kv] 1 / mean norm (0: all norms zero, factor 1)
+    const float* entropy;         // nullable: [layers][batch] normalised entropy of the layer's attention
     float* u;
     float* s_out;  // nullable [layers][batch][n]
     int batch, layers, hkv, n, n_stride, cap;
@@ -72,6 +75,20 @@ struct FoldArgs {
     float w[kMaxLayers];
 };
 hipError_t launch_fold(const FoldArgs& a, hipStream_t s);
+
+// Scorer perturbations (Sec. 5.1): value-row norms with their per-slab mean, and the normalised entropy of
+// each layer's pooled attention, computed from the group sums r.
+struct VariantArgs {
+    const void* v;
+    const float* r;
+    float* vnorm;           // [layers][batch][n_kv][n_stride]
+    float* vnorm_inv_mean;  // [layers][batch][n_kv]
+    float* entropy;         // [layers][batch]
+    int batch, layers, hkv, cap, n, n_stride;
+    float inv_hq;
+};
+hipError_t launch_vnorm(int dtype, int head_dim, const VariantArgs& a, hipStream_t s);
+hipError_t launch_entropy(const VariantArgs& a, hipStream_t s);
 
 // Selection + compaction plan, one workgroup per sequence.
 struct SelectArgs {

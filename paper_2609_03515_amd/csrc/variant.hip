@@ -1,0 +1,118 @@
+// The two order-preserving scorer perturbations of Sec. 5.1 (implementation appendix "Per-step scoring"),
+// applied to the step's score before the fold:
+//   VNorm: each head's attention to token i is multiplied by |v_i| / mean_j |v_j|, the l2 norm of the token's
+//          value row under that head's KV head over the mean norm of the slab's cached tokens;
+//   entropy weighting: the layer's pooled score is multiplied by the entropy of that pooled distribution
+//          over ln(n), one factor per layer and sequence.
+// These kernels produce the norms (with the reciprocal of each slab's mean) and the entropy factors; the
+// fold applies them while it sums the group sums r (which stay the plain attention).
+#include "kernels.h"
+#include "kv_common.h"
+
+namespace ikv {
+namespace {
+
+constexpr int kVThreads = 256;
+
+// One workgroup per (layer, sequence, KV head) slab: a value row is read as 16-byte chunks by an aligned
+// group of LPR lanes, the sum of squares is reduced over the group, and the group's first lane stores the
+// norm; the norms are summed in a fixed order for the mean.
+template <typename T, int D>
+__global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
+    using E = Elem<T>;
+    using chunk_t = typename E::chunk_t;
+    constexpr int EPC = E::kPerChunk, CH = D / EPC, LPR = CH >= 16 ? 16 : CH, CPL = CH / LPR;
+    constexpr int RPI = kVThreads / LPR;
+    __shared__ float part[kVThreads / kWave];
+    const size_t slab = blockIdx.x;
+    const T* vs = static_cast<const T*>(a.v) + slab * a.cap * D;
+    const int p = threadIdx.x % LPR;
+    const int rsub = threadIdx.x / LPR;
+    float* out = a.vnorm + slab * a.n_stride;
+    float sum = 0.0f;
+    for (int base = 0; base < a.n; base += RPI) {  // uniform trip count: every lane joins the shuffles
+        const int row = base + rsub;
+        const bool valid = row < a.n;
+        float ss = 0.0f;
+        if (valid) {
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) {
+                float f[EPC];
+                E::unpack(*reinterpret_cast<const chunk_t*>(vs + (size_t)row * D + (p + c * LPR) * EPC), f);
+#pragma unroll
+                for (int x = 0; x < EPC; ++x) ss = fmaf(f[x], f[x], ss);
+            }
+        }
+#pragma unroll
+        for (int o = 1; o < LPR; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+        if (valid && p == 0) {
+            const float nrm = sqrtf(ss);
+            out[row] = nrm;
+            sum += nrm;
+        }
+    }
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) sum += __shfl_xor(sum, o, kWave);
+    if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = sum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float tot = 0.0f;
+        for (int w = 0; w < kVThreads / kWave; ++w) tot += part[w];
+        a.vnorm_inv_mean[slab] = tot > 0.0f ? (float)a.n / tot : 0.0f;
+    }
+}
+
+// One workgroup per (layer, sequence): s(i) = (1/H) sum_g r_g(i); with S = sum_i s(i) the entropy of
+// p = s / S is ln S - (1/S) sum_i s(i) ln s(i); divided by ln n (factor 1 when n = 1 or S = 0).
+__global__ __launch_bounds__(kVThreads) void entropy_kernel(VariantArgs a) {
+    __shared__ float ps[kVThreads / kWave], pe[kVThreads / kWave];
+    const size_t lb = blockIdx.x;
+    const float* rb = a.r + lb * a.hkv * a.n_stride;
+    float S = 0.0f, E = 0.0f;
+    for (int i = threadIdx.x; i < a.n; i += kVThreads) {
+        float s = 0.0f;
+        for (int g = 0; g < a.hkv; ++g) s += rb[(size_t)g * a.n_stride + i];
+        s *= a.inv_hq;
+        S += s;
+        if (s > 0.0f) E = fmaf(s, logf(s), E);
+    }
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        S += __shfl_xor(S, o, kWave);
+        E += __shfl_xor(E, o, kWave);
+    }
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        ps[threadIdx.x / kWave] = S;
+        pe[threadIdx.x / kWave] = E;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float st = 0.0f, et = 0.0f;
+        for (int w = 0; w < kVThreads / kWave; ++w) {
+            st += ps[w];
+            et += pe[w];
+        }
+        a.entropy[lb] = (a.n > 1 && st > 0.0f) ? (logf(st) - et / st) / logf((float)a.n) : 1.0f;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_vnorm(int dtype, int head_dim, const VariantArgs& a, hipStream_t s) {
+    const dim3 grid((unsigned)((size_t)a.layers * a.batch * a.hkv));
+    if (dtype == 0) {
+        if (head_dim == 64) hipLaunchKernelGGL((vnorm_kernel<float, 64>), grid, dim3(kVThreads), 0, s, a);
+        else hipLaunchKernelGGL((vnorm_kernel<float, 128>), grid, dim3(kVThreads), 0, s, a);
+    } else {
+        if (head_dim == 64) hipLaunchKernelGGL((vnorm_kernel<bf16_t, 64>), grid, dim3(kVThreads), 0, s, a);
+        else hipLaunchKernelGGL((vnorm_kernel<bf16_t, 128>), grid, dim3(kVThreads), 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_entropy(const VariantArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(entropy_kernel, dim3((unsigned)((size_t)a.layers * a.batch)), dim3(kVThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace ikv

@@ -141,6 +141,10 @@ def test_step_validation(lib):
     bad_rule = B.make_params(0.9, 20)
     bad_rule.rule = 9
     assert _step(s, bad_rule)[0] == B.KV_ERR_INVALID_ARG
+    bad_variant = B.make_params(0.9, 20, vnorm=True, entropy=True)
+    assert bad_variant.score_variant == B.KV_SCORE_VNORM | B.KV_SCORE_ENTROPY
+    bad_variant.score_variant = 4
+    assert _step(s, bad_variant)[0] == B.KV_ERR_INVALID_ARG
     assert _step(s, good, v_new=None)[0] == B.KV_ERR_INVALID_ARG
     assert _step(s, good, k=FAKE + 2)[0] == B.KV_ERR_UNSUPPORTED
     rc, out = _step(s, good)

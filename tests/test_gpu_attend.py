@@ -45,7 +45,7 @@ def attend_layers(shape, cfg, n, q, k, v, pos, cur_pos, emit, ws, per_layer):
     return o
 
 
-def run_fused_lockstep(cfg, steps, per_layer):
+def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False):
     w = Workload(cfg)
     cap = max(cfg.prefill_len, cfg.budget) + 1
     st = w.prefill(capacity=cap)
@@ -53,8 +53,8 @@ def run_fused_lockstep(cfg, steps, per_layer):
     dev = to_device(st)
     shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
     params = B.make_params(cfg.alpha, cfg.budget, cfg.refresh_period, cfg.score_free, cfg.nonrefresh_init,
-                           cfg.recency_bias, cfg.recency_window)
-    op = oracle_params(cfg)
+                           cfg.recency_bias, cfg.recency_window, vnorm=vnorm, entropy=entropy)
+    op = oracle_params(cfg, vnorm=vnorm, entropy=entropy)
     ws = B.workspace(shape, cap)
     n = st["n"]
     flips = 0
@@ -105,6 +105,14 @@ def test_fused_step_lockstep(name, per_layer):
     cfg, steps = CASES[name]
     flips = run_fused_lockstep(cfg, steps, per_layer)
     print(f"{name}: in-band flips {flips}")
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b_reduced", "llama8b_split_step1"])
+def test_fused_step_scorer_variants(name):
+    """VNorm + entropy weighting on the fused path: the perturbations are applied by kv_evict_finish to the
+    scores the attention emitted."""
+    cfg, steps = CASES[name]
+    run_fused_lockstep(cfg, steps, per_layer=True, vnorm=True, entropy=True)
 
 
 # ---- one call on random inputs over the supported geometries -------------------------------------------

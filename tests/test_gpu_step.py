@@ -18,7 +18,7 @@ pytestmark = pytest.mark.gpu
 B = pytest.importorskip("paper_2609_03515_amd.binding")
 
 
-def run_lockstep(cfg, steps, seed=None, rule="ema"):
+def run_lockstep(cfg, steps, seed=None, rule="ema", vnorm=False, entropy=False):
     w = Workload(cfg, seed=seed)
     cap = max(cfg.prefill_len, cfg.budget) + 1          # room for the cache to grow up to B + 1
     st = w.prefill(capacity=cap)
@@ -26,8 +26,8 @@ def run_lockstep(cfg, steps, seed=None, rule="ema"):
     dev = to_device(st)
     shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
     params = B.make_params(cfg.alpha, cfg.budget, cfg.refresh_period, cfg.score_free, cfg.nonrefresh_init,
-                           cfg.recency_bias, cfg.recency_window, rule)
-    op = oracle_params(cfg, rule=rule)
+                           cfg.recency_bias, cfg.recency_window, rule, vnorm=vnorm, entropy=entropy)
+    op = oracle_params(cfg, rule=rule, vnorm=vnorm, entropy=entropy)
     ws = B.workspace(shape, cap)
     n = st["n"]
     flips = 0
@@ -85,3 +85,21 @@ def test_evict_step_lockstep(name):
 def test_aggregation_rules(rule):
     cfg = LLAMA8B.scaled(batch=1, layers=3, prefill_len=500, budget=50)
     run_lockstep(cfg, 4, rule=rule)
+
+
+VARIANT_CASES = {
+    "tiny": (TINY, 5),
+    "llama8b_reduced": (LLAMA8B.scaled(batch=2, layers=3, prefill_len=1200, budget=120), 4),
+    "llama8b_split_step1": (LLAMA8B.scaled(batch=1, layers=2, prefill_len=6000, budget=600), 2),
+    "qwen_reduced": (QWEN.scaled(batch=2, layers=2, prefill_len=1000, budget=250), 3),
+    "lazy_r4_mean": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=800, budget=80, nonrefresh_init="mean"), 6),
+}
+
+
+@pytest.mark.parametrize("vnorm,entropy", [(True, False), (False, True), (True, True)],
+                         ids=["vnorm", "entropy", "both"])
+@pytest.mark.parametrize("name", list(VARIANT_CASES))
+def test_scorer_variants_lockstep(name, vnorm, entropy):
+    """Sec. 5.1 scorer perturbations through kv_evict_step, in lockstep with the oracle."""
+    cfg, steps = VARIANT_CASES[name]
+    run_lockstep(cfg, steps, vnorm=vnorm, entropy=entropy)
