@@ -5,7 +5,8 @@ the HIP library and its binding never do, and the two share no code.
 """
 from .inertiakv import (  # noqa: F401
     BF16, CUMULATIVE, EMA, F32, SINGLE_STEP, Cache, Params, StepResult, attention_output, budget_from_ratio,
-    compact_rows, layer_scores_variant, normalized_entropy, value_norm_weights,
+    compact_rows, layer_scores_variant, normalized_entropy, value_norm_weights, RankTraceState, rank_trace_counts,
+    trace_metrics,
     evict_step, fold_layers, head_attention, holefill_moves, layer_scores, new_token_prior, refresh_due,
     select_keep, to_f64,
 )

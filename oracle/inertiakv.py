@@ -13,6 +13,8 @@ Each function names the passage it follows:
   shared by its query-head group before pooling.
 * Eq. 2 / 3 / 4: single-step, cumulative and EMA aggregation rules.
 * The step's decode attention (the softmax Eq. 1 pools, applied to V), for the fused attention + score path.
+* Appendix "Mechanistic Diagnostics": rank-trace set sizes (raw / EMA top-k churn, raw-EMA Jaccard,
+  raw-top evicted rate).
 * Sec. 5.1 / appendix "Per-step scoring": VNorm (attention times the mean-normalised l2 norm of the value
   row) and entropy weighting (the layer's score times the normalised entropy of its attention).
 * Appendix "Implementation Details / Layer scoring": the EMA state is updated after every eligible layer,
@@ -41,6 +43,8 @@ Readings where the paper is silent (the same list is kept in the design notes):
 * VNorm's mean runs over the cached tokens of the same layer and KV head at scoring time; entropy weighting
   uses the entropy of the layer's pooled attention (before VNorm) divided by ln(n), per sequence; with both
   enabled the entropy factor multiplies the VNorm-weighted score.
+* Rank trace: the "raw" score of a step is the mean over layers of the plain per-layer score (Eq. 1); both
+  top-k sets are taken over the n tokens cached before that step's eviction, identified by position.
 """
 from __future__ import annotations
 
@@ -286,6 +290,8 @@ class StepResult:
     s_layers: np.ndarray | None = None         # [K, b, n_scored] per-layer scores (refresh steps)
     moves: list = field(default_factory=list)  # per sequence (dst, src)
     n_out: int = 0
+    raw: np.ndarray | None = None              # [b, n_scored] raw step score: mean over layers of Eq. 1
+    pos_pre: np.ndarray | None = None          # [b, n_scored] positions before compaction
     o: np.ndarray | None = None                # [K, b, H_q, d] decode attention output (when asked for)
     o_scale: np.ndarray | None = None          # [K, b, H_q, d] sum_i a |v|, the output's rounding scale
 
@@ -350,22 +356,26 @@ def evict_step(cache: Cache, q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray
                     params.recency_bias, params.recency_window)
 
     # 2. score + fold
-    s_all = None
+    s_all = raw = None
     if refresh:
         s_all = np.zeros((nl, nb, n), dtype=np.float64)
+        raw = np.zeros((nb, n), dtype=np.float64)
         for b in range(nb):
             for l in range(nl):
                 keys = to_f64(cache.k[l, b, :, :n, :], cache.dtype)
                 ql = to_f64(q[l, b], cache.dtype)
+                plain = layer_scores(ql, keys, cache.pos[b, :n], new_pos, params.recency_bias,
+                                     params.recency_window)
+                raw[b] += plain / nl
                 if params.vnorm or params.entropy:
                     s_all[l, b] = layer_scores_variant(ql, keys, to_f64(cache.v[l, b, :, :n, :], cache.dtype),
                                                        cache.pos[b, :n], new_pos, params.recency_bias,
                                                        params.recency_window, params.vnorm, params.entropy)
                 else:
-                    s_all[l, b] = layer_scores(ql, keys, cache.pos[b, :n], new_pos,
-                                               params.recency_bias, params.recency_window)
+                    s_all[l, b] = plain
             cache.u[b, :n] = fold_layers(cache.u[b, :n], s_all[:, b], params.alpha, params.rule)
     u_pre = cache.u[:, :n].copy()
+    pos_pre = cache.pos[:, :n].copy()
 
     # 3. select
     keep = np.zeros((nb, n), dtype=bool)
@@ -389,7 +399,54 @@ def evict_step(cache: Cache, q: np.ndarray, k_new: np.ndarray, v_new: np.ndarray
         cache.pos[b, dst] = cache.pos[b, src]
         moves.append((dst, src))
     cache.n = min(params.budget, n)
-    return StepResult(refresh, n, keep, u_pre, s_all, moves, cache.n, o_all, o_scale)
+    return StepResult(refresh, n, keep, u_pre, s_all, moves, cache.n, raw, pos_pre, o_all, o_scale)
+
+
+# ----------------------------------------------------------------------------------------------------------
+# Appendix "Mechanistic Diagnostics": rank-trace observables of the stabilisation claim (Sec. 4, Prop. 1)
+# ----------------------------------------------------------------------------------------------------------
+@dataclass
+class RankTraceState:
+    """Previous traced step's top-k position sets of one sequence (None before the first traced step)."""
+    raw: set | None = None
+    ema: set | None = None
+
+
+def rank_trace_counts(state: RankTraceState, raw: np.ndarray, u: np.ndarray, pos: np.ndarray, keep: np.ndarray,
+                      k: int, raw_keep: np.ndarray | None = None, ema_keep: np.ndarray | None = None) -> dict:
+    """Set sizes of one refresh step of one sequence, over the n tokens cached before eviction.
+
+    R_t = top-k of the raw step score (mean over layers of the per-layer attention score, no temporal
+    memory), E_t = top-k of the folded utility u, both under (value descending, position ascending) and
+    identified by absolute position; `keep` is the step's retention decision.  Returns the sizes of R_t,
+    E_t, R_t & R_(t-1), E_t & E_(t-1), R_t & E_t, R_t & evicted_t, R_(t-1), E_(t-1), from which
+    churn = 1 - |A & A'| / |A | A'| (Jaccard) and the raw-top evicted rate = |R & evicted| / |R|.
+    `raw_keep` / `ema_keep` may replace the two top-k decisions by equally valid ones (lockstep use).
+    Updates `state` to this step's sets."""
+    rk = select_keep(raw, pos, k) if raw_keep is None else np.asarray(raw_keep, dtype=bool)
+    ek = select_keep(u, pos, k) if ema_keep is None else np.asarray(ema_keep, dtype=bool)
+    R = set(int(p) for p in pos[rk])
+    E = set(int(p) for p in pos[ek])
+    ev = set(int(p) for p in pos[~np.asarray(keep, dtype=bool)])
+    has_prev = state.raw is not None
+    out = dict(r=len(R), e=len(E), has_prev=int(has_prev),
+               rr=len(R & state.raw) if has_prev else 0, ee=len(E & state.ema) if has_prev else 0,
+               re=len(R & E), rev=len(R & ev),
+               rp=len(state.raw) if has_prev else 0, ep=len(state.ema) if has_prev else 0)
+    state.raw, state.ema = R, E
+    return out
+
+
+def trace_metrics(c: dict) -> dict:
+    """Churn, Jaccard and evicted rate from rank_trace_counts (NaN where undefined)."""
+    def jac(inter, a, b):
+        union = a + b - inter
+        return inter / union if union else float("nan")
+    nan = float("nan")
+    return dict(raw_churn=1 - jac(c["rr"], c["r"], c["rp"]) if c["has_prev"] else nan,
+                ema_churn=1 - jac(c["ee"], c["e"], c["ep"]) if c["has_prev"] else nan,
+                raw_ema_jaccard=jac(c["re"], c["r"], c["e"]),
+                raw_top_evicted=c["rev"] / c["r"] if c["r"] else nan)
 
 
 def compact_rows(rows: np.ndarray, keep: np.ndarray, budget: int) -> np.ndarray:
