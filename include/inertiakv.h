@@ -100,6 +100,31 @@ typedef struct {
     void* end[KV_PHASES];
 } kv_trace;
 
+/* Rank trace (appendix "Mechanistic Diagnostics"): observables of how stable the ranking is, taken on every
+ * refresh step over the n tokens cached before that step's eviction.  R_t = top-k of the raw step score
+ * (the plain per-layer score of Eq. 1 averaged over layers: no memory), E_t = top-k of the folded utility,
+ * both ordered by (value descending, position ascending) and identified by absolute position.  counts[b]
+ * receives, per sequence:
+ *   [0] 1 = traced, 0 = not a refresh step (nothing else written, state unchanged), -2 = a position outside
+ *       [0, max_pos) was in a set (not recorded);
+ *   [1] |R_t|  [2] |E_t|  [3] 1 if a previous traced step exists  [4] |R_t & R_t-1|  [5] |E_t & E_t-1|
+ *   [6] |R_t & E_t|  [7] |R_t & evicted_t|  [8] |R_t-1|  [9] |E_t-1|
+ * so that churn = 1 - |A & A'| / (|A| + |A'| - |A & A'|), raw/EMA Jaccard = [6] / ([1] + [2] - [6]) and the
+ * raw-top evicted rate = [7] / [1].  `state` carries the previous sets (position bitmaps) between steps; it
+ * must be zero-filled before a sequence's first traced step. */
+#define KV_TRACE_COUNTS 10
+typedef struct {
+    int32_t k;          /* size of the traced top-k sets, >= 1 (e.g. the budget B)                  */
+    int32_t max_pos;    /* every traced position must be < max_pos                                   */
+    uint32_t* state;    /* DEVICE, kv_rank_trace_state_bytes() bytes                                 */
+    int32_t* counts;    /* DEVICE [batch][KV_TRACE_COUNTS]                                           */
+    uint8_t* raw_keep;  /* nullable DEVICE [batch][cap]: R_t as a mask over the pre-eviction slots    */
+    uint8_t* ema_keep;  /* nullable DEVICE [batch][cap]: E_t as a mask over the pre-eviction slots    */
+} kv_rank_trace;
+
+/* Bytes of rank-trace state for `batch` sequences and positions < max_pos (host only). */
+kv_status kv_rank_trace_state_bytes(int32_t batch, int32_t max_pos, size_t* bytes);
+
 /* Bytes of workspace needed by every call below for any n <= n_max cached tokens (host only). */
 kv_status kv_workspace_bytes(const kv_shape* shape, int32_t n_max, size_t* bytes);
 
@@ -131,11 +156,12 @@ kv_status kv_compact(const kv_shape* shape, int32_t n, int32_t budget, const uin
  *  3. if n_in + 1 > B: select the top B (stale utilities on non-refresh steps) and compact as kv_compact.
  * *n_out (HOST pointer) receives min(B, n_in + 1).  keep_out (nullable) receives the decision over the
  * n_in + 1 slots before compaction; s_out (nullable) the per-layer scores of a refresh step; trace (nullable)
- * timing events. */
+ * timing events; rank_trace (nullable) the diagnostics above. */
 kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in,
                         int32_t new_pos, const void* q, const void* k_new, const void* v_new, void* k, void* v,
                         float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
-                        const kv_trace* trace, void* ws, size_t ws_bytes, void* stream);
+                        const kv_trace* trace, const kv_rank_trace* rank_trace, void* ws, size_t ws_bytes,
+                        void* stream);
 
 /* ---- Decode step around the model's own attention (fused decode attention + score) ----
  * A decoder that attends the cache anyway can take the step's score from its attention (Eq. 1 is the softmax
@@ -167,10 +193,11 @@ kv_status kv_attend_score(const kv_shape* shape, int32_t layer0, int32_t layer_c
 
 /* Steps 2-3 of kv_evict_step after the attention calls: on refresh steps (Eq. 5) the layer fold of the
  * emitted scores of ALL layers (Eq. 4 by params->rule), then the top-B selection and compaction over the n
- * cached tokens (n = n_in + 1 of the step).  *n_out (HOST) = min(B, n); keep_out / s_out as kv_evict_step. */
+ * cached tokens (n = n_in + 1 of the step).  *n_out (HOST) = min(B, n); keep_out / s_out / rank_trace as
+ * kv_evict_step. */
 kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n, void* k, void* v,
-                          float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out, void* ws,
-                          size_t ws_bytes, void* stream);
+                          float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
+                          const kv_rank_trace* rank_trace, void* ws, size_t ws_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* kv_status_string(kv_status status);

@@ -23,7 +23,8 @@ KV_PHASES = 5
 PHASES = ("append", "score", "fold", "select", "compact")
 
 EXPORTED = ("kv_workspace_bytes", "kv_score_ema", "kv_topk_select", "kv_compact", "kv_evict_step",
-            "kv_append", "kv_attend_score", "kv_evict_finish", "kv_status_string")
+            "kv_append", "kv_attend_score", "kv_evict_finish", "kv_rank_trace_state_bytes", "kv_status_string")
+KV_TRACE_COUNTS = 10
 
 
 class KVError(RuntimeError):
@@ -49,6 +50,11 @@ class KvTrace(ctypes.Structure):
     _fields_ = [("begin", ctypes.c_void_p * KV_PHASES), ("end", ctypes.c_void_p * KV_PHASES)]
 
 
+class KvRankTrace(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_int32), ("max_pos", ctypes.c_int32), ("state", ctypes.c_void_p),
+                ("counts", ctypes.c_void_p), ("raw_keep", ctypes.c_void_p), ("ema_keep", ctypes.c_void_p)]
+
+
 _lib = None
 
 
@@ -62,15 +68,18 @@ def load_library(path: str = LIB_PATH):
     lib = ctypes.CDLL(path)
     vp, i32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
     shp, prm, trc = ctypes.POINTER(KvShape), ctypes.POINTER(KvParams), ctypes.POINTER(KvTrace)
+    rtr = ctypes.POINTER(KvRankTrace)
     lib.kv_workspace_bytes.argtypes = [shp, i32, ctypes.POINTER(sz)]
     lib.kv_score_ema.argtypes = [shp, i32, vp, vp, vp, i32, f32, f32, i32, vp, vp, vp, sz, vp]
     lib.kv_topk_select.argtypes = [shp, i32, i32, vp, vp, vp, vp, sz, vp]
     lib.kv_compact.argtypes = [shp, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.kv_evict_step.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
-                                  ctypes.POINTER(i32), vp, vp, trc, vp, sz, vp]
+                                  ctypes.POINTER(i32), vp, vp, trc, rtr, vp, sz, vp]
     lib.kv_append.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
     lib.kv_attend_score.argtypes = [shp, i32, i32, i32, vp, vp, vp, vp, i32, f32, i32, i32, vp, vp, sz, vp]
-    lib.kv_evict_finish.argtypes = [shp, prm, i32, i32, vp, vp, vp, vp, ctypes.POINTER(i32), vp, vp, vp, sz, vp]
+    lib.kv_evict_finish.argtypes = [shp, prm, i32, i32, vp, vp, vp, vp, ctypes.POINTER(i32), vp, vp, rtr, vp, sz,
+                                    vp]
+    lib.kv_rank_trace_state_bytes.argtypes = [i32, i32, ctypes.POINTER(sz)]
     for fn in EXPORTED[:-1]:
         getattr(lib, fn).restype = i32
     lib.kv_status_string.argtypes = [i32]
@@ -150,15 +159,30 @@ def kv_compact(shape, n, budget, keep, k, v, u, pos, ws, stream=None):
 
 
 def kv_evict_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, ws, keep_out=None,
-                  s_out=None, trace: KvTrace | None = None, stream=None) -> int:
+                  s_out=None, trace: KvTrace | None = None, rank_trace: KvRankTrace | None = None,
+                  stream=None) -> int:
     """Returns n_out = min(B, n_in + 1)."""
     n_out = ctypes.c_int32(-1)
     _check("kv_evict_step", load_library().kv_evict_step(
         ctypes.byref(shape), ctypes.byref(params), int(t), int(n_in), int(new_pos), _ptr(q), _ptr(k_new),
         _ptr(v_new), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out),
-        ctypes.byref(trace) if trace is not None else None, _ptr(ws),
+        ctypes.byref(trace) if trace is not None else None,
+        ctypes.byref(rank_trace) if rank_trace is not None else None, _ptr(ws),
         ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
     return n_out.value
+
+
+def kv_rank_trace_state_bytes(batch: int, max_pos: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check("kv_rank_trace_state_bytes", load_library().kv_rank_trace_state_bytes(int(batch), int(max_pos),
+                                                                                  ctypes.byref(out)))
+    return out.value
+
+
+def make_rank_trace(k, max_pos, state, counts, raw_keep=None, ema_keep=None) -> KvRankTrace:
+    """state: a zero-filled device tensor of kv_rank_trace_state_bytes() bytes; counts: int32 device tensor
+    [batch][KV_TRACE_COUNTS].  Keep the tensors alive while the struct is in use."""
+    return KvRankTrace(int(k), int(max_pos), _ptr(state), _ptr(counts), _ptr(raw_keep), _ptr(ema_keep))
 
 
 def _ws_bytes(ws):
@@ -179,12 +203,14 @@ def kv_attend_score(shape, layer0, layer_count, n, q, k, v, pos, cur_pos, recenc
         _ws_bytes(ws), _stream(stream)))
 
 
-def kv_evict_finish(shape, params, t, n, k, v, u, pos, ws, keep_out=None, s_out=None, stream=None) -> int:
+def kv_evict_finish(shape, params, t, n, k, v, u, pos, ws, keep_out=None, s_out=None,
+                    rank_trace: KvRankTrace | None = None, stream=None) -> int:
     """Returns n_out = min(B, n)."""
     n_out = ctypes.c_int32(-1)
     _check("kv_evict_finish", load_library().kv_evict_finish(
         ctypes.byref(shape), ctypes.byref(params), int(t), int(n), _ptr(k), _ptr(v), _ptr(u), _ptr(pos),
-        ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out), _ptr(ws), _ws_bytes(ws), _stream(stream)))
+        ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out),
+        ctypes.byref(rank_trace) if rank_trace is not None else None, _ptr(ws), _ws_bytes(ws), _stream(stream)))
     return n_out.value
 
 

@@ -14,7 +14,8 @@ struct Layout {
     int n_stride;
     int max_pairs;
     ScorePlan plan;
-    size_t r_off, z_off, part_off, opart_off, vn_off, vinv_off, eta_off, pdst_off, psrc_off, np_off, total;
+    size_t r_off, z_off, part_off, opart_off, vn_off, vinv_off, eta_off, pdst_off, psrc_off, np_off;
+    size_t raw_off, rmask_off, emask_off, kmask_off, tdst_off, tsrc_off, tnp_off, total;
 };
 
 int esize(const kv_shape& s) { return s.dtype == KV_F32 ? 4 : 2; }
@@ -73,6 +74,22 @@ Layout layout_for(const kv_shape& s, int n) {
     L.psrc_off = off;
     off = align256(off + (size_t)s.batch * L.max_pairs * sizeof(int32_t));
     L.np_off = off;
+    off = align256(off + (size_t)s.batch * sizeof(int32_t));
+    // rank trace: raw score, the three decisions, and a private selection plan (the eviction's stays intact)
+    const size_t slots = (size_t)s.batch * s.capacity;
+    L.raw_off = off;
+    off = align256(off + slots * sizeof(float));
+    L.rmask_off = off;
+    off = align256(off + slots);
+    L.emask_off = off;
+    off = align256(off + slots);
+    L.kmask_off = off;
+    off = align256(off + slots);
+    L.tdst_off = off;
+    off = align256(off + (size_t)s.batch * L.max_pairs * sizeof(int32_t));
+    L.tsrc_off = off;
+    off = align256(off + (size_t)s.batch * L.max_pairs * sizeof(int32_t));
+    L.tnp_off = off;
     off = align256(off + (size_t)s.batch * sizeof(int32_t));
     L.total = off;
     return L;
@@ -274,14 +291,63 @@ kv_status run_append(const kv_shape& s, const kv_params& p, int t, int n_in, int
     return rc;
 }
 
-// Top-B selection over the n cached tokens and, when tokens are dropped, the compaction.
+size_t trace_words(int max_pos) { return ((size_t)max_pos + 31) / 32; }
+
+kv_status check_rank_trace(const kv_rank_trace* rt) {
+    if (!rt) return KV_OK;
+    if (rt->k < 1 || rt->max_pos < 1 || !rt->state || !rt->counts) return KV_ERR_INVALID_ARG;
+    if (!aligned(rt->state, 4) || !aligned(rt->counts, 4)) return KV_ERR_UNSUPPORTED;
+    return KV_OK;
+}
+
+// Top-B selection over the n cached tokens and, when tokens are dropped, the compaction.  With a rank trace
+// on a refresh step, the two traced top-k decisions and their statistics are taken first, on the
+// pre-compaction slots.
 kv_status run_select_compact(const kv_shape& s, const Layout& L, int n, int budget, void* k, void* v, float* u,
-                             int32_t* pos, uint8_t* keep_out, void* ws, hipStream_t st, const kv_trace* tr) {
+                             int32_t* pos, uint8_t* keep_out, const kv_rank_trace* rt, bool refresh, void* ws,
+                             hipStream_t st, const kv_trace* tr) {
+    TraceArgs ta{};
+    kv_status rc = KV_OK;
+    const bool traced = rt && refresh;
+    if (rt) {
+        ta.r = at<float>(ws, L.r_off);
+        ta.raw = at<float>(ws, L.raw_off);
+        ta.pos = pos;
+        ta.raw_keep = rt->raw_keep ? rt->raw_keep : at<uint8_t>(ws, L.rmask_off);
+        ta.ema_keep = rt->ema_keep ? rt->ema_keep : at<uint8_t>(ws, L.emask_off);
+        ta.keep = keep_out ? keep_out : at<uint8_t>(ws, L.kmask_off);
+        ta.state = rt->state;
+        ta.counts = rt->counts;
+        ta.batch = s.batch;
+        ta.layers = s.layers;
+        ta.hkv = s.n_kv_heads;
+        ta.cap = s.capacity;
+        ta.n = n;
+        ta.n_stride = L.n_stride;
+        ta.max_pos = rt->max_pos;
+        ta.words = (int)trace_words(rt->max_pos);
+        ta.inv_kh = (float)(1.0 / ((double)s.layers * s.n_q_heads));
+        if (!traced) {
+            if ((rc = hip_status(launch_trace_stats(ta, true, st))) != KV_OK) return rc;
+        } else {
+            if ((rc = hip_status(launch_trace_raw(ta, st))) != KV_OK) return rc;
+            for (int which = 0; which < 2; ++which) {
+                SelectArgs a = select_args(s, L, n, rt->k, which == 0 ? ta.raw : u, pos, ws);
+                a.pair_dst = at<int32_t>(ws, L.tdst_off);
+                a.pair_src = at<int32_t>(ws, L.tsrc_off);
+                a.npairs = at<int32_t>(ws, L.tnp_off);
+                a.keep_out = const_cast<uint8_t*>(which == 0 ? ta.raw_keep : ta.ema_keep);
+                if ((rc = hip_status(launch_select(a, false, st))) != KV_OK) return rc;
+            }
+            keep_out = const_cast<uint8_t*>(ta.keep);
+        }
+    }
     if (n <= budget && !keep_out) return KV_OK;
     SelectArgs a = select_args(s, L, n, budget, u, pos, ws);
     a.keep_out = keep_out;
     record(tr, 3, true, st);
-    kv_status rc = hip_status(launch_select(a, false, st));
+    rc = hip_status(launch_select(a, false, st));
+    if (rc == KV_OK && traced) rc = hip_status(launch_trace_stats(ta, false, st));
     record(tr, 3, false, st);
     if (rc != KV_OK || n <= budget) return rc;
     record(tr, 4, true, st);
@@ -361,11 +427,13 @@ kv_status kv_compact(const kv_shape* shape, int32_t n, int32_t budget, const uin
 kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in,
                         int32_t new_pos, const void* q, const void* k_new, const void* v_new, void* k, void* v,
                         float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
-                        const kv_trace* trace, void* ws, size_t ws_bytes, void* stream) {
+                        const kv_trace* trace, const kv_rank_trace* rank_trace, void* ws, size_t ws_bytes,
+                        void* stream) {
     kv_status rc = check_shape(shape);
     if (rc != KV_OK) return rc;
     const kv_shape& s = *shape;
     if ((rc = check_params(params)) != KV_OK) return rc;
+    if ((rc = check_rank_trace(rank_trace)) != KV_OK) return rc;
     const kv_params& p = *params;
     if (!n_out) return KV_ERR_INVALID_ARG;
     if (t < 1 || n_in < 0 || n_in + 1 > s.capacity || new_pos < 0) return KV_ERR_INVALID_ARG;
@@ -379,7 +447,8 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
     hipStream_t st = static_cast<hipStream_t>(stream);
 
     if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, st, trace)) != KV_OK) return rc;
-    if (is_refresh(p, t)) {
+    const bool refresh = is_refresh(p, t);
+    if (refresh) {
         record(trace, 1, true, st);
         rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, ws, st, trace);
         if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, ws, st);
@@ -387,7 +456,8 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
         if (rc == KV_OK) rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, ws, st, trace);
         if (rc != KV_OK) return rc;
     }
-    if ((rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, ws, st, trace)) != KV_OK) return rc;
+    rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, trace);
+    if (rc != KV_OK) return rc;
     *n_out = n < p.budget ? n : p.budget;
     return KV_OK;
 }
@@ -447,12 +517,13 @@ kv_status kv_attend_score(const kv_shape* shape, int32_t layer0, int32_t layer_c
 }
 
 kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n, void* k, void* v,
-                          float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out, void* ws,
-                          size_t ws_bytes, void* stream) {
+                          float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
+                          const kv_rank_trace* rank_trace, void* ws, size_t ws_bytes, void* stream) {
     kv_status rc = check_shape(shape);
     if (rc != KV_OK) return rc;
     const kv_shape& s = *shape;
     if ((rc = check_params(params)) != KV_OK) return rc;
+    if ((rc = check_rank_trace(rank_trace)) != KV_OK) return rc;
     const kv_params& p = *params;
     if (!n_out || t < 1 || n < 1 || n > s.capacity) return KV_ERR_INVALID_ARG;
     if (!k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
@@ -461,13 +532,21 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
     const Layout L = layout_for(s, n);
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if (is_refresh(p, t)) {
+    const bool refresh = is_refresh(p, t);
+    if (refresh) {
         if ((rc = run_variants(s, L, n, v, p.score_variant, ws, st)) != KV_OK) return rc;
         if ((rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, ws, st, nullptr)) != KV_OK)
             return rc;
     }
-    if ((rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, ws, st, nullptr)) != KV_OK) return rc;
+    rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, nullptr);
+    if (rc != KV_OK) return rc;
     *n_out = n < p.budget ? n : p.budget;
+    return KV_OK;
+}
+
+kv_status kv_rank_trace_state_bytes(int32_t batch, int32_t max_pos, size_t* bytes) {
+    if (batch < 1 || max_pos < 1 || !bytes) return KV_ERR_INVALID_ARG;
+    *bytes = (size_t)batch * (4 + 2 * trace_words(max_pos)) * sizeof(uint32_t);
     return KV_OK;
 }
 

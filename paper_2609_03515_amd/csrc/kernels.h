@@ -90,6 +90,23 @@ struct VariantArgs {
 hipError_t launch_vnorm(int dtype, int head_dim, const VariantArgs& a, hipStream_t s);
 hipError_t launch_entropy(const VariantArgs& a, hipStream_t s);
 
+// Rank trace (appendix "Mechanistic Diagnostics"): the raw step score and the per-sequence set statistics.
+constexpr int kTraceCounts = 10;
+struct TraceArgs {
+    const float* r;          // group sums of the step
+    float* raw;              // [batch][cap] mean over layers of the pooled score
+    const int32_t* pos;      // positions before compaction
+    const uint8_t* raw_keep; // [batch][cap] top-k of raw
+    const uint8_t* ema_keep; // [batch][cap] top-k of u
+    const uint8_t* keep;     // [batch][cap] the step's retention decision
+    uint32_t* state;         // per sequence: header (4 words) + raw bitmap + ema bitmap
+    int32_t* counts;         // [batch][kTraceCounts]
+    int batch, layers, hkv, cap, n, n_stride, max_pos, words;  // words: bitmap words per set
+    float inv_kh;            // 1 / (layers * n_q)
+};
+hipError_t launch_trace_raw(const TraceArgs& a, hipStream_t s);
+hipError_t launch_trace_stats(const TraceArgs& a, bool skip, hipStream_t s);
+
 // Selection + compaction plan, one workgroup per sequence.
 struct SelectArgs {
     const float* u;

@@ -119,8 +119,8 @@ def _step(s, p, t=1, n_in=10, n_out=True, **kw):
     out = ctypes.c_int32(-7)
     rc = lib_().kv_evict_step(ctypes.byref(s), ctypes.byref(p) if p is not None else None, t, n_in, 5,
                               args["q"], args["k_new"], args["v_new"], args["k"], args["v"], args["u"], args["pos"],
-                              ctypes.byref(out) if n_out else None, None, None, None, args["ws"], args["ws_bytes"],
-                              None)
+                              ctypes.byref(out) if n_out else None, None, None, None, args.get("rt"), args["ws"],
+                              args["ws_bytes"], None)
     return rc, out.value
 
 
@@ -198,7 +198,7 @@ def test_finish_validation(lib):
 
     def call(p=good, t=1, n=10, k=FAKE, n_out=True, ws=None, ws_bytes=0):
         return L.kv_evict_finish(ctypes.byref(s), ctypes.byref(p) if p is not None else None, t, n, k, FAKE, FAKE,
-                                 FAKE, ctypes.byref(out) if n_out else None, None, None, ws, ws_bytes, None)
+                                 FAKE, ctypes.byref(out) if n_out else None, None, None, None, ws, ws_bytes, None)
     assert call(p=None) == B.KV_ERR_INVALID_ARG
     assert call(t=0) == B.KV_ERR_INVALID_ARG
     assert call(n=0) == B.KV_ERR_INVALID_ARG
@@ -207,3 +207,18 @@ def test_finish_validation(lib):
     assert call(k=FAKE + 8) == B.KV_ERR_UNSUPPORTED
     assert call() == B.KV_ERR_WORKSPACE and out.value == -7
 
+
+
+def test_rank_trace_validation(lib):
+    s = shape()
+    good = B.make_params(0.9, 20)
+    need = B.kv_workspace_bytes(s, 11)
+    assert B.kv_rank_trace_state_bytes(2, 64) == 2 * (4 + 2 * 2) * 4
+    assert B.kv_rank_trace_state_bytes(1, 65) == (4 + 2 * 3) * 4
+    with pytest.raises(B.KVError):
+        B.kv_rank_trace_state_bytes(0, 10)
+    for bad in (B.KvRankTrace(0, 100, FAKE, FAKE), B.KvRankTrace(5, 0, FAKE, FAKE), B.KvRankTrace(5, 100, None, FAKE),
+                B.KvRankTrace(5, 100, FAKE, None)):
+        assert _step(s, good, rt=ctypes.byref(bad), ws=FAKE, ws_bytes=need)[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, good, rt=ctypes.byref(B.KvRankTrace(5, 100, FAKE + 2, FAKE)), ws=FAKE,
+                 ws_bytes=need)[0] == B.KV_ERR_UNSUPPORTED
