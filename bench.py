@@ -48,7 +48,8 @@ def step_bytes(cfg, n):
 
 
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "score_llama8b_32k_steady_traffic.txt")
-SCORER_SOURCES = ("paper_2609_03515_amd/csrc/score.hip", "paper_2609_03515_amd/csrc/kv_common.h")
+SCORER_SOURCES = ("paper_2609_03515_amd/csrc/score.hip", "paper_2609_03515_amd/csrc/stream_lane.h",
+                  "paper_2609_03515_amd/csrc/kv_common.h")
 
 
 def counter_traffic():
@@ -106,6 +107,98 @@ def cpu_baseline(cfg, seqs: int, steps: int):
             "seconds_measured": dt}
 
 
+def extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, full_ms):
+    """Further rows of the path on the same trajectory, KF steps each (host wall clock around the launches):
+    the decode step around the model's own attention (attention fused with the score vs attention followed by
+    the separate scoring step), the scorer perturbations and the rank trace."""
+    import torch
+
+    def params(**kw):
+        return B.make_params(cfg.alpha, cfg.budget, 1, False, "mean", cfg.recency_bias, cfg.recency_window, **kw)
+
+    full = params()
+    o = torch.empty_like(inputs[0]["q"])
+    L = cfg.layers
+
+    def attend(n, q, emit, per_layer):
+        if per_layer:
+            for l in range(L):
+                B.kv_attend_score(shape, l, 1, n, q[l], k, v, pos, inputs[state["t"] - 1]["new_pos"],
+                                  cfg.recency_bias, cfg.recency_window, emit, o[l], ws)
+        else:
+            B.kv_attend_score(shape, 0, L, n, q, k, v, pos, inputs[state["t"] - 1]["new_pos"], cfg.recency_bias,
+                              cfg.recency_window, emit, o, ws)
+
+    def fused_step(per_layer):
+        state["t"] += 1
+        si = inputs[state["t"] - 1]
+        n = state["n"]
+        B.kv_append(shape, full, state["t"], n, si["new_pos"], si["k_new"], si["v_new"], k, v, u, pos)
+        attend(n + 1, si["q"], 1, per_layer)
+        state["n"] = B.kv_evict_finish(shape, full, state["t"], n + 1, k, v, u, pos, ws)
+
+    def separate_step(per_layer):
+        state["t"] += 1
+        si = inputs[state["t"] - 1]
+        state["n"] = B.kv_evict_step(shape, full, state["t"], state["n"], si["new_pos"], si["q"], si["k_new"],
+                                     si["v_new"], k, v, u, pos, ws)
+        attend(state["n"] + 1, si["q"], 0, per_layer)
+
+    def attention_only(per_layer):
+        state["t"] += 1
+        attend(state["n"] + 1, inputs[state["t"] - 1]["q"], 0, per_layer)
+
+    def plain_step(p, rank_trace=None):
+        state["t"] += 1
+        si = inputs[state["t"] - 1]
+        state["n"] = B.kv_evict_step(shape, p, state["t"], state["n"], si["new_pos"], si["q"], si["k_new"],
+                                     si["v_new"], k, v, u, pos, ws, rank_trace=rank_trace)
+
+    def ms_of(fn, *a, **kw):
+        fn(*a, **kw)  # one untimed call (first use of a configuration)
+        torch.cuda.synchronize()
+        h0 = time.perf_counter()
+        for _ in range(KF - 1):
+            fn(*a, **kw)
+        torch.cuda.synchronize()
+        return 1e3 * (time.perf_counter() - h0) / (KF - 1)
+
+    res = {}
+    kv_bytes = 2 * cfg.layers * cfg.batch * cfg.n_kv_heads * (cfg.budget + 1) * cfg.head_dim * 2
+    for per_layer in (True, False):
+        a_ms = ms_of(attention_only, per_layer)
+        f_ms = ms_of(fused_step, per_layer)
+        s_ms = ms_of(separate_step, per_layer)
+        res["per_layer_calls" if per_layer else "all_layers_one_call"] = {
+            "attention_only_ms": round(a_ms, 4), "attention_GBps_K_V": round(kv_bytes / (a_ms * 1e-3) / 1e9, 1),
+            "fused_decode_step_ms": round(f_ms, 4), "separate_decode_step_ms": round(s_ms, 4),
+            "fused_steps_per_s": round(1e3 / f_ms, 2), "separate_steps_per_s": round(1e3 / s_ms, 2),
+            "eviction_overhead_fused_pct": round(100 * (f_ms - a_ms) / a_ms, 1),
+            "eviction_overhead_separate_pct": round(100 * (s_ms - a_ms) / a_ms, 1)}
+    fused = {"what": "one decode step of attention over every layer (32 per-layer calls, or one call) plus the "
+                     "eviction step; fused = attention emits the score (kv_append, kv_attend_score, "
+                     "kv_evict_finish), separate = attention without score + kv_evict_step's own scoring pass",
+             **res}
+    variants = {"attention_ms": round(full_ms, 4)}
+    for name, kw in (("vnorm", dict(vnorm=True)), ("entropy", dict(entropy=True)),
+                     ("vnorm_entropy", dict(vnorm=True, entropy=True))):
+        variants[name + "_ms"] = round(ms_of(plain_step, params(**kw)), 4)
+    max_pos = inputs[-1]["new_pos"] + 1
+    tstate = torch.zeros(B.kv_rank_trace_state_bytes(cfg.batch, max_pos) // 4, dtype=torch.int32,
+                         device=u.device)
+    counts = torch.zeros(cfg.batch, B.KV_TRACE_COUNTS, dtype=torch.int32, device=u.device)
+    rt = B.make_rank_trace(cfg.budget, max_pos, tstate, counts)
+    tr_ms = ms_of(plain_step, full, rt)
+    c = counts.cpu().numpy().astype(float)
+    churn = lambda i, a, p: 1 - c[:, i] / (c[:, a] + c[:, p] - c[:, i])  # noqa: E731
+    trace = {"ms_per_step": round(tr_ms, 4), "overhead_pct": round(100 * (tr_ms - full_ms) / full_ms, 1),
+             "k": cfg.budget, "last_step_mean_over_sequences": {
+                 "raw_churn": round(float(churn(4, 1, 8).mean()), 5), "ema_churn": round(float(churn(5, 2, 9).mean()), 5),
+                 "raw_ema_jaccard": round(float((c[:, 6] / (c[:, 1] + c[:, 2] - c[:, 6])).mean()), 5),
+                 "raw_top_evicted": round(float((c[:, 7] / c[:, 1]).mean()), 6)}}
+    return {"fused_attention": fused, "score_variants": variants, "rank_trace": trace}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,7 +233,8 @@ def main():
     lazy8 = B.make_params(cfg.alpha, cfg.budget, 8, False, "min", cfg.recency_bias, cfg.recency_window)
     ws = B.workspace(shape, cap, device=dev)
     K, W = args.steps, args.warmup
-    total = 1 + W + 3 * K
+    KF = min(K, 50)   # steps per configuration of the extra measurements (fused attention, variants, trace)
+    total = 1 + W + 3 * K + 10 * KF
     inputs = [w.step_inputs(t) for t in range(1, total + 1)]
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
@@ -198,6 +292,8 @@ def main():
     lz4_s, _, lz4_score = timed(lazy4)
     lz8_s, _, _ = timed(lazy8)
 
+    extra = extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, ms_per_step)
+
     n = cfg.budget + 1
     by = step_bytes(cfg, n)
     score_avg_ms = sum(score_ms) / len(score_ms)
@@ -240,6 +336,7 @@ def main():
                          "(Qwen2.5-7B), 64k context, 90% compression, NVIDIA H100/H200; context only",
         "setup_s": round(setup_s, 1),
     }
+    out.update(extra)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seqs, args.cpu_steps)
     print(json.dumps(out), flush=True)
