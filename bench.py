@@ -257,7 +257,21 @@ def main():
         state["n"] = B.kv_evict_step(shape, params, state["t"], state["n"], si["new_pos"], si["q"], si["k_new"],
                                      si["v_new"], k, v, u, pos, ws, trace=trace)
 
-    # decode step 1: the whole 32k prefill is scored and compacted to B tokens
+    # decode step 1: the whole 32k prefill is scored and compacted to B tokens.  A first run on a copy of the
+    # prefill pays the one-time costs (first touch of the workspace, kernel loading) and is reported apart.
+    def step1_on(kk, vv, uu, pp):
+        si = inputs[0]
+        e0, e1 = B.HipEvent(), B.HipEvent()
+        e0.record()
+        B.kv_evict_step(shape, full, 1, st["n"], si["new_pos"], si["q"], si["k_new"], si["v_new"], kk, vv, uu, pp,
+                        ws)
+        e1.record()
+        return e0.elapsed_ms(e1)
+
+    copies = [x.clone() for x in (k, v, u, pos)]
+    step1_cold_ms = step1_on(*copies)
+    del copies
+    torch.cuda.empty_cache()
     e0, e1 = B.HipEvent(), B.HipEvent()
     e0.record()
     step(full)
@@ -327,6 +341,7 @@ def main():
                      "bytes_per_launch": by["score"], "avg_launch_ms": round(score_avg_ms, 5),
                      "launches_timed": len(score_ms)},
         "step1_ms": round(step1_ms, 3),
+        "step1_cold_ms": round(step1_cold_ms, 3),
         "lazy_r4": {"value": round(K / lz4_s, 2), "unit": "evict-steps/s", "ms_per_step": round(1e3 * lz4_s / K, 4),
                     "refresh_steps": len(lz4_score), "nonrefresh_init": "min"},
         "lazy_r8": {"value": round(K / lz8_s, 2), "unit": "evict-steps/s", "ms_per_step": round(1e3 * lz8_s / K, 4),

@@ -131,10 +131,12 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     constexpr int kStep = kWaves * kWave;
     const int mine = nunits > ln.wave ? (nunits - ln.wave + kWaves - 1) / kWaves : 0;
     const bool write_z = a.emit && a.nchunk > 1;
-    float* zrow = a.z + ((size_t)lb * a.hq + (size_t)g * a.group + ln.hh) * a.n_stride + row0;
+    const __amdgpu_buffer_rsrc_t zrs =
+        raw_rsrc(a.z + ((size_t)lb * a.hq + (size_t)g * a.group + ln.hh) * a.n_stride + row0, nrows * 4);
     float ssum = 0.0f;
     auto expo = [&](float z, int unit) {
-        if (write_z && z != -INFINITY) zrow[ln.unit_row(unit)] = z;  // -inf: padded head or row past the end
+        // -inf: padded head or row past the end
+        if (write_z && z != -INFINITY) store_stream(zrs, ln.unit_row(unit) * 4, z);
         return z == -INFINITY ? 0.0f : __expf(z - m);
     };
     int i = 0;
@@ -269,11 +271,10 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
             if (ln.hh == 0) zs[(ln.wave + i * kWaves) * kWave + ln.kk * L::NG + ln.grp] = sum;
         }
         __syncthreads();
-        float* rrow = a.r + (size_t)s * a.n_stride;
+        const __amdgpu_buffer_rsrc_t rrs = raw_rsrc(a.r + (size_t)s * a.n_stride, a.n_stride * 4);
         for (int j = threadIdx.x; j * 4 < nrows; j += kThreads) {
             const int row = j * 4;
-            *reinterpret_cast<f32x4*>(rrow + row) =
-                *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]);
+            store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]));
         }
     }
 }

@@ -143,10 +143,10 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWavesLds))) void scor
     for (; i < mine; ++i) emit(ln.wave + i * kWaves, group_allsum<GP>(prob(zl[i * kStep])));
     __syncthreads();
     // rows [4j, 4j + 4) lie in one unit (RPW is a multiple of 4); rows up to the padded stride are scratch
+    const __amdgpu_buffer_rsrc_t rrs = raw_rsrc(rrow, a.n_stride * 4);
     for (int j = threadIdx.x; j * 4 < n; j += kThreads) {
         const int row = j * 4;
-        const f32x4 v = *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]);
-        *reinterpret_cast<f32x4*>(rrow + row) = v;
+        store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]));
     }
 }
 
@@ -184,7 +184,8 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWavesSplit))) void sc
 
     // the logits leave the workgroup, so the (max, sum) pair is kept online
     MaxSum ms{kFloor, 0.0f};
-    float* zrow = a.z + (((size_t)l * a.batch + b) * a.hq + (size_t)g * a.group + ln.hh) * a.n_stride;
+    const __amdgpu_buffer_rsrc_t zrs = raw_rsrc(
+        a.z + (((size_t)l * a.batch + b) * a.hq + (size_t)g * a.group + ln.hh) * a.n_stride, a.n_stride * 4);
     for (int it = 0; it < nit; it += kNbuf) {
 #pragma unroll
         for (int j = 0; j < kNbuf; ++j) {
@@ -196,7 +197,7 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWavesSplit))) void sc
                 const float m_new = fmaxf(ms.m, z);
                 ms.s = fmaf(ms.s, __expf(ms.m - m_new), __expf(z - m_new));
                 ms.m = m_new;
-                if (z != -INFINITY) zrow[row] = z;
+                if (z != -INFINITY) store_stream(zrs, row * 4, z);
             }
         }
     }

@@ -32,9 +32,23 @@ constexpr float kFloor = -1.0e30f;  // finite start of running maxima: exp(-inf 
 constexpr int kNonTemporal = 2;     // buffer-load cache policy: K is streamed once, no reuse to cache for
 constexpr int kRsrcConfig = 0x00020000;  // raw (unformatted, stride 0) buffer resource, gfx9 family
 
+// Cache policy of the results written while K is still streaming (group sums, logits): device scope (sc1).
+// Writes interleaved with the saturated read stream cost far more than their bytes; measured at the 8B shape,
+// the 27 MB of group sums cost ~40 us of a 290 us launch with the default policy, ~24 us with this one
+// (non-temporal: ~30 us).
+constexpr int kStoreStream = 16;
+
 // Raw buffer resource over `bytes` bytes at `base` (reads at offsets >= bytes return zero).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, int bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kRsrcConfig);
+}
+
+// 16- and 4-byte stores at byte offset `off` of a raw buffer resource, with the streaming-result cache policy.
+__device__ __forceinline__ void store_stream(__amdgpu_buffer_rsrc_t rs, int off, const f32x4& v) {
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rs, off, 0, kStoreStream);
+}
+__device__ __forceinline__ void store_stream(__amdgpu_buffer_rsrc_t rs, int off, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rs, off, 0, kStoreStream);
 }
 
 template <typename T, int D, int GP>
