@@ -15,7 +15,8 @@
  * Conventions for every call
  *  - Buffer pointers are DEVICE pointers owned by the caller; the library never allocates, frees or
  *    synchronises device memory and never reads them on the host.  Scratch comes from a caller workspace of
- *    at least kv_workspace_bytes() bytes, 256-byte aligned.
+ *    at least kv_workspace_bytes() bytes, 256-byte aligned (contents need no initialisation); calls that
+ *    share a workspace must not overlap in time.
  *  - Work is queued asynchronously on `stream` (a hipStream_t; NULL = the default stream) in stream order.
  *  - Arguments are validated on the host before anything is queued; an invalid call returns a negative
  *    kv_status and queues nothing.  KV_ERR_HIP reports a failed launch (hipGetLastError).

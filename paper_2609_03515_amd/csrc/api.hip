@@ -507,13 +507,7 @@ kv_status kv_attend_score(const kv_shape* shape, int32_t layer0, int32_t layer_c
     a.chunk_rows = plan.chunk_rows;
     a.nchunk = plan.nchunk;
     a.emit = emit_scores != 0;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    if ((rc = hip_status(launch_attend(s.dtype, s.head_dim, plan, a, st))) != KV_OK) return rc;
-    if (plan.split) {
-        if ((rc = hip_status(launch_attend_finish(s.dtype, s.head_dim, a, st))) != KV_OK) return rc;
-        if (a.emit && (rc = hip_status(launch_split_finish(a, st))) != KV_OK) return rc;
-    }
-    return KV_OK;
+    return hip_status(launch_attend(s.dtype, s.head_dim, plan, a, static_cast<hipStream_t>(stream)));
 }
 
 kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n, void* k, void* v,

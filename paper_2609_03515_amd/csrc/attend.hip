@@ -14,7 +14,7 @@
 //   4. cross-lane / cross-wave reduction in a fixed order (deterministic), then either the normalised
 //      output (one chunk per slab) or the chunk's unnormalised partial output with its per-head (max, sum);
 //   5. when the score is wanted: the group probability sums r of the rows (one chunk), or the raw logits
-//      for the scorer's finish kernel (several chunks).
+//      (several chunks), which a combine kernel turns into outputs and scores.
 // Chunks exist so that one layer's slabs (batch x KV heads, e.g. 64) still fill 256 CUs.
 #include "stream_lane.h"
 
@@ -44,6 +44,54 @@ __device__ __forceinline__ void read_probs(const float* src, float (&e)[GP]) {
     } else {
 #pragma unroll
         for (int i = 0; i < GP; ++i) e[i] = src[i];
+    }
+}
+
+// Several chunks per slab: one workgroup per slab combines them after the chunks' launch.
+//   o_h = sum_c exp(m_c - M_h) o_c / sum_c exp(m_c - M_h) S_c,  M_h = max_c m_c;
+//   r(row) = sum_{h in group} exp(z_h(row) - M_h) / S_h from the logits the chunks wrote (when emitting).
+// (Electing the last chunk inside the attention kernel instead needs a device-scope release/acquire fence in
+// every chunk, which lowers to a full L2 write-back and invalidate: measured 5x slower per layer.)
+template <typename T, int D, int GP>
+__global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
+    __shared__ float cm[GP], ci[GP];
+    const int s = blockIdx.x;  // slab: (l * batch + b) * hkv + g, l relative to the call
+    const size_t head0 = (size_t)(s / a.hkv) * a.hq + (size_t)(s % a.hkv) * a.group;
+    if (threadIdx.x < a.group) {
+        const float2* pp = a.part + (head0 + threadIdx.x) * a.nchunk;
+        float mx = -INFINITY;
+        for (int c = 0; c < a.nchunk; ++c) mx = fmaxf(mx, pp[c].x);
+        float tot = 0.0f;
+        for (int c = 0; c < a.nchunk; ++c) tot = fmaf(__expf(pp[c].x - mx), pp[c].y, tot);
+        cm[threadIdx.x] = mx;
+        ci[threadIdx.x] = tot > 0.0f ? 1.0f / tot : 0.0f;
+    }
+    __syncthreads();
+    T* ob = static_cast<T*>(a.o) + head0 * D;
+    for (int idx = threadIdx.x; idx < a.group * D; idx += kThreads) {
+        const int h = idx / D;
+        const float2* pp = a.part + (head0 + h) * a.nchunk;
+        const float* op = a.opart + (head0 + h) * a.nchunk * D + idx % D;
+        float acc = 0.0f;
+        for (int c = 0; c < a.nchunk; ++c) acc = fmaf(__expf(pp[c].x - cm[h]), op[(size_t)c * D], acc);
+        Elem<T>::store(ob + idx, acc * ci[h]);
+    }
+    if (a.emit) {
+        // rows are padded to a multiple of 64: 4 rows per thread and pass, rows >= n are scratch
+        const float* zb = a.z + head0 * a.n_stride;
+        float* rb = a.r + (size_t)s * a.n_stride;
+        for (int row = threadIdx.x * 4; row < a.n; row += kThreads * 4) {
+            f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            for (int h = 0; h < a.group; ++h) {
+                const f32x4 z = *reinterpret_cast<const f32x4*>(zb + (size_t)h * a.n_stride + row);
+                const float m = cm[h], inv = ci[h];
+                acc.x += __expf(z.x - m) * inv;
+                acc.y += __expf(z.y - m) * inv;
+                acc.z += __expf(z.z - m) * inv;
+                acc.w += __expf(z.w - m) * inv;
+            }
+            *reinterpret_cast<f32x4*>(rb + row) = acc;
+        }
     }
 }
 
@@ -258,6 +306,7 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
         if (threadIdx.x < a.group)
             a.part[(head0 + threadIdx.x) * a.nchunk + chunk] =
                 make_float2(head_max(threadIdx.x), head_sum(threadIdx.x));
+        return;
     }
 
     // 5. one chunk: the score's group probability sums, staged in each unit's first RPW words (only this
@@ -279,23 +328,6 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     }
 }
 
-// Several chunks per slab: o_h = sum_c exp(m_c - M) o_c / sum_c exp(m_c - M) S_c with M = max_c m_c.
-template <typename T>
-__global__ __launch_bounds__(128) void attend_finish_kernel(ScoreArgs a, int d) {
-    const size_t head = blockIdx.x;  // (l * batch + b) * n_q + h
-    const float2* pp = a.part + head * a.nchunk;
-    float mx = -INFINITY;
-    for (int c = 0; c < a.nchunk; ++c) mx = fmaxf(mx, pp[c].x);
-    const float* op = a.opart + head * a.nchunk * d + threadIdx.x;
-    float tot = 0.0f, acc = 0.0f;
-    for (int c = 0; c < a.nchunk; ++c) {
-        const float w = __expf(pp[c].x - mx);
-        tot = fmaf(w, pp[c].y, tot);
-        acc = fmaf(w, op[(size_t)c * d], acc);
-    }
-    Elem<T>::store(static_cast<T*>(a.o) + head * d + threadIdx.x, tot > 0.0f ? acc / tot : 0.0f);
-}
-
 template <typename T, int D, int GP>
 hipError_t launch_attend_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
     if constexpr (Geometry<T, D, 1>::kLpr < GP) {
@@ -312,6 +344,12 @@ hipError_t launch_attend_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream
             }
         }
         hipLaunchKernelGGL(kern, dim3(plan.grid), dim3(kThreads), plan.lds_bytes, s, a);
+        if (plan.split) {
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            hipLaunchKernelGGL((attend_combine_kernel<T, D, GP>), dim3(plan.grid / plan.nchunk), dim3(kThreads), 0,
+                               s, a);
+        }
         return hipGetLastError();
     }
 }
@@ -375,15 +413,6 @@ hipError_t launch_attend(int dtype, int head_dim, const ScorePlan& plan, const S
         if (head_dim == 128) return launch_attend_d<bf16_t, 128>(plan, a, s);
     }
     return hipErrorInvalidValue;
-}
-
-hipError_t launch_attend_finish(int dtype, int head_dim, const ScoreArgs& a, hipStream_t s) {
-    const dim3 grid((unsigned)((size_t)a.layers * a.batch * a.hq));
-    if (dtype == 0)
-        hipLaunchKernelGGL(attend_finish_kernel<float>, grid, dim3(head_dim), 0, s, a, head_dim);
-    else
-        hipLaunchKernelGGL(attend_finish_kernel<bf16_t>, grid, dim3(head_dim), 0, s, a, head_dim);
-    return hipGetLastError();
 }
 
 }  // namespace ikv

@@ -49,7 +49,8 @@ hipError_t launch_split_finish(const ScoreArgs& a, hipStream_t s);
 
 // Decode attention fused with the score: o_h = sum_i a_h(i) v_i for every query head, and (when emit) the
 // same r as the scorer.  The plan cuts each slab into nchunk row ranges so that `slabs` slabs fill the chip;
-// with nchunk > 1 the chunks write partial outputs / logits that the finish kernels combine.
+// with nchunk > 1 the chunks write partial outputs / logits and a combine kernel (one workgroup per slab)
+// produces the outputs and scores.
 bool attend_plan(int dtype, int head_dim, int group, int n, int slabs, ScorePlan* plan);
 // Workspace bound over every call of 1..layers layers on n rows: the largest (layers of the call) x nchunk,
 // and whether any such call splits.
@@ -59,7 +60,6 @@ struct AttendBound {
 };
 AttendBound attend_bound(int dtype, int head_dim, int group, int n, int slabs_per_layer, int layers);
 hipError_t launch_attend(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s);
-hipError_t launch_attend_finish(int dtype, int head_dim, const ScoreArgs& a, hipStream_t s);
 
 // Layer fold (Eq. 2-4): u <- prior_w * u + sum_l w_l s_l with s_l = (1/H) sum_g r_{l,g}.
 struct FoldArgs {
