@@ -177,8 +177,10 @@ kv_status run_variants(const kv_shape& s, const Layout& L, int n, const void* v,
 
 // Layer fold of the workspace r into u (Eq. 2-4 by `rule`).
 kv_status run_fold(const kv_shape& s, const Layout& L, int n, float* u, float* s_out, int rule, float alpha,
-                   int variant, void* ws, hipStream_t st, const kv_trace* tr) {
+                   int variant, bool raw_out, void* ws, hipStream_t st, const kv_trace* tr) {
     FoldArgs f{};
+    f.raw = raw_out ? at<float>(ws, L.raw_off) : nullptr;
+    f.raw_scale = (float)(1.0 / ((double)s.layers * s.n_q_heads));
     f.r = at<float>(ws, L.r_off);
     f.vnorm = (variant & KV_SCORE_VNORM) ? at<float>(ws, L.vn_off) : nullptr;
     f.vnorm_inv_mean = at<float>(ws, L.vinv_off);
@@ -301,8 +303,8 @@ kv_status check_rank_trace(const kv_rank_trace* rt) {
 }
 
 // Top-B selection over the n cached tokens and, when tokens are dropped, the compaction.  With a rank trace
-// on a refresh step, the two traced top-k decisions and their statistics are taken first, on the
-// pre-compaction slots.
+// on a refresh step, the traced top-k decisions (raw score from the fold; the EMA set is the retention
+// decision itself when k = B) and their statistics are taken before the compaction, on the same slots.
 kv_status run_select_compact(const kv_shape& s, const Layout& L, int n, int budget, void* k, void* v, float* u,
                              int32_t* pos, uint8_t* keep_out, const kv_rank_trace* rt, bool refresh, void* ws,
                              hipStream_t st, const kv_trace* tr) {
@@ -310,36 +312,18 @@ kv_status run_select_compact(const kv_shape& s, const Layout& L, int n, int budg
     kv_status rc = KV_OK;
     const bool traced = rt && refresh;
     if (rt) {
-        ta.r = at<float>(ws, L.r_off);
-        ta.raw = at<float>(ws, L.raw_off);
         ta.pos = pos;
-        ta.raw_keep = rt->raw_keep ? rt->raw_keep : at<uint8_t>(ws, L.rmask_off);
-        ta.ema_keep = rt->ema_keep ? rt->ema_keep : at<uint8_t>(ws, L.emask_off);
-        ta.keep = keep_out ? keep_out : at<uint8_t>(ws, L.kmask_off);
         ta.state = rt->state;
         ta.counts = rt->counts;
         ta.batch = s.batch;
-        ta.layers = s.layers;
-        ta.hkv = s.n_kv_heads;
         ta.cap = s.capacity;
         ta.n = n;
-        ta.n_stride = L.n_stride;
         ta.max_pos = rt->max_pos;
         ta.words = (int)trace_words(rt->max_pos);
-        ta.inv_kh = (float)(1.0 / ((double)s.layers * s.n_q_heads));
         if (!traced) {
             if ((rc = hip_status(launch_trace_stats(ta, true, st))) != KV_OK) return rc;
-        } else {
-            if ((rc = hip_status(launch_trace_raw(ta, st))) != KV_OK) return rc;
-            for (int which = 0; which < 2; ++which) {
-                SelectArgs a = select_args(s, L, n, rt->k, which == 0 ? ta.raw : u, pos, ws);
-                a.pair_dst = at<int32_t>(ws, L.tdst_off);
-                a.pair_src = at<int32_t>(ws, L.tsrc_off);
-                a.npairs = at<int32_t>(ws, L.tnp_off);
-                a.keep_out = const_cast<uint8_t*>(which == 0 ? ta.raw_keep : ta.ema_keep);
-                if ((rc = hip_status(launch_select(a, false, st))) != KV_OK) return rc;
-            }
-            keep_out = const_cast<uint8_t*>(ta.keep);
+        } else if (!keep_out) {
+            keep_out = at<uint8_t>(ws, L.kmask_off);  // the statistics need the decision
         }
     }
     if (n <= budget && !keep_out) return KV_OK;
@@ -347,7 +331,21 @@ kv_status run_select_compact(const kv_shape& s, const Layout& L, int n, int budg
     a.keep_out = keep_out;
     record(tr, 3, true, st);
     rc = hip_status(launch_select(a, false, st));
-    if (rc == KV_OK && traced) rc = hip_status(launch_trace_stats(ta, false, st));
+    if (rc == KV_OK && traced) {
+        ta.keep = keep_out;
+        ta.raw_keep = rt->raw_keep ? rt->raw_keep : at<uint8_t>(ws, L.rmask_off);
+        const bool ema_is_keep = rt->k == budget && !rt->ema_keep;
+        ta.ema_keep = ema_is_keep ? keep_out : (rt->ema_keep ? rt->ema_keep : at<uint8_t>(ws, L.emask_off));
+        for (int which = 0; which < (ema_is_keep ? 1 : 2) && rc == KV_OK; ++which) {
+            SelectArgs t = select_args(s, L, n, rt->k, which == 0 ? at<float>(ws, L.raw_off) : u, pos, ws);
+            t.pair_dst = at<int32_t>(ws, L.tdst_off);
+            t.pair_src = at<int32_t>(ws, L.tsrc_off);
+            t.npairs = at<int32_t>(ws, L.tnp_off);
+            t.keep_out = const_cast<uint8_t*>(which == 0 ? ta.raw_keep : ta.ema_keep);
+            rc = hip_status(launch_select(t, false, st));
+        }
+        if (rc == KV_OK) rc = hip_status(launch_trace_stats(ta, false, st));
+    }
     record(tr, 3, false, st);
     if (rc != KV_OK || n <= budget) return rc;
     record(tr, 4, true, st);
@@ -388,7 +386,7 @@ kv_status kv_score_ema(const kv_shape* shape, int32_t n, const void* q, const vo
     hipStream_t st = static_cast<hipStream_t>(stream);
     if ((rc = run_score(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws, st, nullptr)) != KV_OK)
         return rc;
-    return run_fold(s, L, n, u, s_out, KV_RULE_EMA, alpha, 0, ws, st, nullptr);
+    return run_fold(s, L, n, u, s_out, KV_RULE_EMA, alpha, 0, false, ws, st, nullptr);
 }
 
 kv_status kv_topk_select(const kv_shape* shape, int32_t n, int32_t budget, const float* u, const int32_t* pos,
@@ -453,7 +451,8 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
         rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, ws, st, trace);
         if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, ws, st);
         record(trace, 1, false, st);
-        if (rc == KV_OK) rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, ws, st, trace);
+        if (rc == KV_OK)
+            rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, rank_trace != nullptr, ws, st, trace);
         if (rc != KV_OK) return rc;
     }
     rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, trace);
@@ -529,8 +528,8 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
     const bool refresh = is_refresh(p, t);
     if (refresh) {
         if ((rc = run_variants(s, L, n, v, p.score_variant, ws, st)) != KV_OK) return rc;
-        if ((rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, ws, st, nullptr)) != KV_OK)
-            return rc;
+        rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, rank_trace != nullptr, ws, st, nullptr);
+        if (rc != KV_OK) return rc;
     }
     rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, nullptr);
     if (rc != KV_OK) return rc;

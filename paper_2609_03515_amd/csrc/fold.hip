@@ -18,11 +18,13 @@ constexpr int kThreads = kQuads * kSlices;
 
 __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
     __shared__ float partial[kSlices][kQuads * 4];
+    __shared__ float partial_raw[kSlices][kQuads * 4];
     const int quad = threadIdx.x % kQuads;
     const int slice = threadIdx.x / kQuads;
     const int b = blockIdx.y;
     const int tok0 = blockIdx.x * (kQuads * 4) + quad * 4;  // r rows are padded to a multiple of 64
     f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    f32x4 racc = {0.0f, 0.0f, 0.0f, 0.0f};  // rank trace: sum over layers of the plain group sums
     if (tok0 < a.n) {
         for (int l = slice; l < a.layers; l += kSlices) {
             const float* rl = a.r + ((size_t)(l * a.batch + b) * a.hkv) * a.n_stride + tok0;
@@ -32,15 +34,19 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
                 // (factor 1 where the slab's norms are all zero)
                 const float* nl = a.vnorm + ((size_t)(l * a.batch + b) * a.hkv) * a.n_stride + tok0;
                 const float* il = a.vnorm_inv_mean + (size_t)(l * a.batch + b) * a.hkv;
+                f32x4 plain = {0.0f, 0.0f, 0.0f, 0.0f};
                 for (int g = 0; g < a.hkv; ++g) {
                     const f32x4 rg = *reinterpret_cast<const f32x4*>(rl + (size_t)g * a.n_stride);
                     const float im = il[g];
                     const f32x4 f = im > 0.0f ? *reinterpret_cast<const f32x4*>(nl + (size_t)g * a.n_stride) * im
                                               : f32x4{1.0f, 1.0f, 1.0f, 1.0f};
                     s += rg * f;
+                    plain += rg;
                 }
+                racc += plain;
             } else {
                 for (int g = 0; g < a.hkv; ++g) s += *reinterpret_cast<const f32x4*>(rl + (size_t)g * a.n_stride);
+                racc += s;
             }
             s *= a.inv_hq;
             if (a.entropy) s *= a.entropy[l * a.batch + b];  // entropy weighting: one factor per layer and sequence
@@ -54,7 +60,10 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
         }
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) partial[slice][quad * 4 + j] = acc[j];
+    for (int j = 0; j < 4; ++j) {
+        partial[slice][quad * 4 + j] = acc[j];
+        partial_raw[slice][quad * 4 + j] = racc[j];
+    }
     __syncthreads();
     if (threadIdx.x < kQuads * 4) {
         const int tok = blockIdx.x * (kQuads * 4) + threadIdx.x;
@@ -63,6 +72,11 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
             for (int sl = 0; sl < kSlices; ++sl) tot += partial[sl][threadIdx.x];
             float* up = a.u + (size_t)b * a.cap + tok;
             *up = fmaf(a.prior_w, *up, tot);
+            if (a.raw) {
+                float rt = 0.0f;
+                for (int sl = 0; sl < kSlices; ++sl) rt += partial_raw[sl][threadIdx.x];
+                a.raw[(size_t)b * a.cap + tok] = rt * a.raw_scale;
+            }
         }
     }
 }

@@ -67,6 +67,8 @@ struct FoldArgs {
     const float* vnorm;           // nullable: [layers][batch][n_kv][n_stride] value-row l2 norms
     const float* vnorm_inv_mean;  // [layers][batch][n_kv] 1 / mean norm (0: all norms zero, factor 1)
     const float* entropy;         // nullable: [layers][batch] normalised entropy of the layer's attention
+    float* raw;                   // nullable: [batch][cap] rank trace's raw score (plain scores, layer mean)
+    float raw_scale;              // 1 / (layers * n_q)
     float* u;
     float* s_out;  // nullable [layers][batch][n]
     int batch, layers, hkv, n, n_stride, cap;
@@ -90,21 +92,18 @@ struct VariantArgs {
 hipError_t launch_vnorm(int dtype, int head_dim, const VariantArgs& a, hipStream_t s);
 hipError_t launch_entropy(const VariantArgs& a, hipStream_t s);
 
-// Rank trace (appendix "Mechanistic Diagnostics"): the raw step score and the per-sequence set statistics.
+// Rank trace (appendix "Mechanistic Diagnostics"): per-sequence set statistics (the raw step score comes from
+// the fold).
 constexpr int kTraceCounts = 10;
 struct TraceArgs {
-    const float* r;          // group sums of the step
-    float* raw;              // [batch][cap] mean over layers of the pooled score
     const int32_t* pos;      // positions before compaction
     const uint8_t* raw_keep; // [batch][cap] top-k of raw
     const uint8_t* ema_keep; // [batch][cap] top-k of u
     const uint8_t* keep;     // [batch][cap] the step's retention decision
     uint32_t* state;         // per sequence: header (4 words) + raw bitmap + ema bitmap
     int32_t* counts;         // [batch][kTraceCounts]
-    int batch, layers, hkv, cap, n, n_stride, max_pos, words;  // words: bitmap words per set
-    float inv_kh;            // 1 / (layers * n_q)
+    int batch, cap, n, max_pos, words;  // words: bitmap words per set
 };
-hipError_t launch_trace_raw(const TraceArgs& a, hipStream_t s);
 hipError_t launch_trace_stats(const TraceArgs& a, bool skip, hipStream_t s);
 
 // Selection + compaction plan, one workgroup per sequence.

@@ -2,7 +2,7 @@
 // a refresh step over the n tokens cached before eviction:
 //   R_t = top-k of the raw step score (the per-layer pooled score of Eq. 1 averaged over layers, no memory),
 //   E_t = top-k of the folded utility, both by (value descending, position ascending), identified by position.
-// The two top-k decisions come from the selection kernel; this file computes the raw score and, per
+// The raw score comes from the fold and the top-k decisions from the selection kernel; this file computes, per
 // sequence, the sizes |R_t|, |E_t|, |R_t & R_t-1|, |E_t & E_t-1|, |R_t & E_t|, |R_t & evicted_t| against the
 // previous traced step's sets, which persist between steps as position bitmaps in caller-owned state.
 #include "kernels.h"
@@ -11,26 +11,16 @@
 namespace ikv {
 namespace {
 
-constexpr int kRawThreads = 256;
 constexpr int kStatThreads = 1024;
 constexpr int kHeader = 4;  // state words per sequence before the bitmaps: has_prev, |R_t-1|, |E_t-1|, spare
 
-__global__ __launch_bounds__(kRawThreads) void trace_raw_kernel(TraceArgs a) {
-    const int b = blockIdx.y;
-    const int i = blockIdx.x * kRawThreads + threadIdx.x;
-    if (i >= a.n) return;
-    float s = 0.0f;
-    for (int l = 0; l < a.layers; ++l) {
-        const float* rl = a.r + ((size_t)(l * a.batch + b) * a.hkv) * a.n_stride + i;
-        for (int g = 0; g < a.hkv; ++g) s += rl[(size_t)g * a.n_stride];
-    }
-    a.raw[(size_t)b * a.cap + i] = s * a.inv_kh;
-}
-
 // One workgroup per sequence.  Counting reads the previous bitmaps; after a barrier the bitmaps are cleared
-// and refilled with this step's sets (atomic ORs: several positions share a word).  Positions outside
-// [0, max_pos) are not recorded and flag the step (counts[0] = -2).
+// and refilled with this step's sets (atomic ORs: several positions share a word).  When both bitmaps fit,
+// they are worked on in LDS and copied in and out with coalesced accesses.  Positions outside [0, max_pos)
+// are not recorded and flag the step (counts[0] = -2).
+template <bool kLds>
 __global__ __launch_bounds__(kStatThreads) void trace_stats_kernel(TraceArgs a, int skip) {
+    extern __shared__ uint32_t lbm[];
     __shared__ int cnt[7];
     const int b = blockIdx.x;
     int32_t* out = a.counts + (size_t)b * kTraceCounts;
@@ -39,13 +29,15 @@ __global__ __launch_bounds__(kStatThreads) void trace_stats_kernel(TraceArgs a, 
         return;
     }
     uint32_t* st = a.state + (size_t)b * (kHeader + 2 * (size_t)a.words);
-    uint32_t* bm_r = st + kHeader;
-    uint32_t* bm_e = bm_r + a.words;
+    uint32_t* gbm = st + kHeader;  // raw bitmap, then EMA bitmap
+    uint32_t* bm = kLds ? lbm : gbm;
     const int32_t* pb = a.pos + (size_t)b * a.cap;
     const uint8_t* rk = a.raw_keep + (size_t)b * a.cap;
     const uint8_t* ek = a.ema_keep + (size_t)b * a.cap;
     const uint8_t* kp = a.keep + (size_t)b * a.cap;
     if (threadIdx.x < 7) cnt[threadIdx.x] = 0;
+    if (kLds)
+        for (int w = threadIdx.x; w < 2 * a.words; w += kStatThreads) lbm[w] = gbm[w];
     __syncthreads();
     const bool has_prev = st[0] != 0;
     int c_r = 0, c_e = 0, c_rr = 0, c_ee = 0, c_re = 0, c_rev = 0, oob = 0;
@@ -60,8 +52,8 @@ __global__ __launch_bounds__(kStatThreads) void trace_stats_kernel(TraceArgs a, 
             oob |= in_r || in_e;
         } else if (has_prev) {
             const uint32_t bit = 1u << (p & 31);
-            c_rr += in_r && (bm_r[p >> 5] & bit);
-            c_ee += in_e && (bm_e[p >> 5] & bit);
+            c_rr += in_r && (bm[p >> 5] & bit);
+            c_ee += in_e && (bm[a.words + (p >> 5)] & bit);
         }
     }
     atomicAdd(&cnt[0], c_r);
@@ -72,15 +64,19 @@ __global__ __launch_bounds__(kStatThreads) void trace_stats_kernel(TraceArgs a, 
     atomicAdd(&cnt[5], c_rev);
     atomicOr(&cnt[6], oob);
     __syncthreads();  // every read of the previous sets is done
-    for (int w = threadIdx.x; w < 2 * a.words; w += kStatThreads) bm_r[w] = 0u;
-    __threadfence();
+    for (int w = threadIdx.x; w < 2 * a.words; w += kStatThreads) bm[w] = 0u;
+    if (!kLds) __threadfence();
     __syncthreads();
     for (int i = threadIdx.x; i < a.n; i += kStatThreads) {
         const int p = pb[i];
         if (p < 0 || p >= a.max_pos) continue;
         const uint32_t bit = 1u << (p & 31);
-        if (rk[i]) atomicOr(&bm_r[p >> 5], bit);
-        if (ek[i]) atomicOr(&bm_e[p >> 5], bit);
+        if (rk[i]) atomicOr(&bm[p >> 5], bit);
+        if (ek[i]) atomicOr(&bm[a.words + (p >> 5)], bit);
+    }
+    if (kLds) {
+        __syncthreads();
+        for (int w = threadIdx.x; w < 2 * a.words; w += kStatThreads) gbm[w] = lbm[w];
     }
     if (threadIdx.x == 0) {
         out[0] = cnt[6] ? -2 : 1;
@@ -101,14 +97,12 @@ __global__ __launch_bounds__(kStatThreads) void trace_stats_kernel(TraceArgs a, 
 
 }  // namespace
 
-hipError_t launch_trace_raw(const TraceArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(trace_raw_kernel, dim3((a.n + kRawThreads - 1) / kRawThreads, a.batch), dim3(kRawThreads),
-                       0, s, a);
-    return hipGetLastError();
-}
-
 hipError_t launch_trace_stats(const TraceArgs& a, bool skip, hipStream_t s) {
-    hipLaunchKernelGGL(trace_stats_kernel, dim3(a.batch), dim3(kStatThreads), 0, s, a, skip ? 1 : 0);
+    const size_t lds = 2 * (size_t)a.words * sizeof(uint32_t);
+    if (!skip && lds <= 64 * 1024)
+        hipLaunchKernelGGL(trace_stats_kernel<true>, dim3(a.batch), dim3(kStatThreads), lds, s, a, 0);
+    else
+        hipLaunchKernelGGL(trace_stats_kernel<false>, dim3(a.batch), dim3(kStatThreads), 0, s, a, skip ? 1 : 0);
     return hipGetLastError();
 }
 

@@ -12,17 +12,20 @@
 namespace ikv {
 namespace {
 
-constexpr int kVThreads = 256;
+constexpr int kVThreads = 512;
 
 // One workgroup per (layer, sequence, KV head) slab: a value row is read as 16-byte chunks by an aligned
-// group of LPR lanes, the sum of squares is reduced over the group, and the group's first lane stores the
-// norm; the norms are summed in a fixed order for the mean.
+// group of LPR lanes (kRows rows per lane and pass, loads issued together), the sum of squares is reduced
+// over the group, and the group's first lane stores the norm; the norms are summed in a fixed order for the
+// mean.
+constexpr int kRows = 4;
+
 template <typename T, int D>
 __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
     using E = Elem<T>;
     using chunk_t = typename E::chunk_t;
     constexpr int EPC = E::kPerChunk, CH = D / EPC, LPR = CH >= 16 ? 16 : CH, CPL = CH / LPR;
-    constexpr int RPI = kVThreads / LPR;
+    constexpr int RPI = kVThreads / LPR;  // rows per pass and row slot
     __shared__ float part[kVThreads / kWave];
     const size_t slab = blockIdx.x;
     const T* vs = static_cast<const T*>(a.v) + slab * a.cap * D;
@@ -30,25 +33,32 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
     const int rsub = threadIdx.x / LPR;
     float* out = a.vnorm + slab * a.n_stride;
     float sum = 0.0f;
-    for (int base = 0; base < a.n; base += RPI) {  // uniform trip count: every lane joins the shuffles
-        const int row = base + rsub;
-        const bool valid = row < a.n;
-        float ss = 0.0f;
-        if (valid) {
+    for (int base = 0; base < a.n; base += RPI * kRows) {  // uniform trip count: every lane joins the shuffles
+        chunk_t c[kRows][CPL];
 #pragma unroll
-            for (int c = 0; c < CPL; ++c) {
+        for (int k = 0; k < kRows; ++k) {
+            const int row = min(base + k * RPI + rsub, a.n - 1);  // clamped: the duplicate is not stored
+#pragma unroll
+            for (int cc = 0; cc < CPL; ++cc)
+                c[k][cc] = *reinterpret_cast<const chunk_t*>(vs + (size_t)row * D + (p + cc * LPR) * EPC);
+        }
+#pragma unroll
+        for (int k = 0; k < kRows; ++k) {
+            float ss = 0.0f;
+#pragma unroll
+            for (int cc = 0; cc < CPL; ++cc) {
                 float f[EPC];
-                E::unpack(*reinterpret_cast<const chunk_t*>(vs + (size_t)row * D + (p + c * LPR) * EPC), f);
+                E::unpack(c[k][cc], f);
 #pragma unroll
                 for (int x = 0; x < EPC; ++x) ss = fmaf(f[x], f[x], ss);
             }
-        }
-#pragma unroll
-        for (int o = 1; o < LPR; o <<= 1) ss += __shfl_xor(ss, o, kWave);
-        if (valid && p == 0) {
-            const float nrm = sqrtf(ss);
-            out[row] = nrm;
-            sum += nrm;
+            ss = group_allsum<LPR>(ss);  // DPP inside the row's aligned lane group
+            const int row = base + k * RPI + rsub;
+            if (row < a.n && p == 0) {
+                const float nrm = sqrtf(ss);
+                out[row] = nrm;
+                sum += nrm;
+            }
         }
     }
 #pragma unroll
@@ -63,18 +73,27 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
 }
 
 // One workgroup per (layer, sequence): s(i) = (1/H) sum_g r_g(i); with S = sum_i s(i) the entropy of
-// p = s / S is ln S - (1/S) sum_i s(i) ln s(i); divided by ln n (factor 1 when n = 1 or S = 0).
-__global__ __launch_bounds__(kVThreads) void entropy_kernel(VariantArgs a) {
-    __shared__ float ps[kVThreads / kWave], pe[kVThreads / kWave];
+// p = s / S is ln S - (1/S) sum_i s(i) ln s(i); divided by ln n (factor 1 when n = 1 or S = 0).  Each thread
+// reads 4 consecutive tokens of every KV head per pass (rows are padded to a multiple of 64; the padding is
+// masked), so a 32k-token slab takes 8 passes.
+constexpr int kEThreads = 1024;
+
+__global__ __launch_bounds__(kEThreads) void entropy_kernel(VariantArgs a) {
+    __shared__ float ps[kEThreads / kWave], pe[kEThreads / kWave];
     const size_t lb = blockIdx.x;
     const float* rb = a.r + lb * a.hkv * a.n_stride;
     float S = 0.0f, E = 0.0f;
-    for (int i = threadIdx.x; i < a.n; i += kVThreads) {
-        float s = 0.0f;
-        for (int g = 0; g < a.hkv; ++g) s += rb[(size_t)g * a.n_stride + i];
+    for (int i = threadIdx.x * 4; i < a.n; i += kEThreads * 4) {
+        f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int g = 0; g < a.hkv; ++g) s += *reinterpret_cast<const f32x4*>(rb + (size_t)g * a.n_stride + i);
         s *= a.inv_hq;
-        S += s;
-        if (s > 0.0f) E = fmaf(s, logf(s), E);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (i + j < a.n) {
+                S += s[j];
+                if (s[j] > 0.0f) E = fmaf(s[j], logf(s[j]), E);
+            }
+        }
     }
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
@@ -88,7 +107,7 @@ __global__ __launch_bounds__(kVThreads) void entropy_kernel(VariantArgs a) {
     __syncthreads();
     if (threadIdx.x == 0) {
         float st = 0.0f, et = 0.0f;
-        for (int w = 0; w < kVThreads / kWave; ++w) {
+        for (int w = 0; w < kEThreads / kWave; ++w) {
             st += ps[w];
             et += pe[w];
         }
@@ -111,7 +130,7 @@ hipError_t launch_vnorm(int dtype, int head_dim, const VariantArgs& a, hipStream
 }
 
 hipError_t launch_entropy(const VariantArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(entropy_kernel, dim3((unsigned)((size_t)a.layers * a.batch)), dim3(kVThreads), 0, s, a);
+    hipLaunchKernelGGL(entropy_kernel, dim3((unsigned)((size_t)a.layers * a.batch)), dim3(kEThreads), 0, s, a);
     return hipGetLastError();
 }
 

@@ -85,6 +85,7 @@ CASES = {
     "tiny_kB": (TINY, 8, TINY.budget, False),
     "llama8b_reduced_kB": (LLAMA8B.scaled(batch=2, layers=3, prefill_len=1200, budget=120), 5, 120, False),
     "llama8b_reduced_k30": (LLAMA8B.scaled(batch=2, layers=3, prefill_len=1200, budget=120), 5, 30, False),
+    # bitmaps too large for LDS (positions < 300,000): the statistics work on them in global memory
     "lazy_r4_min": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=800, budget=80), 9, 80, False),
     "fused_tiny_kB": (TINY, 6, TINY.budget, True),
     "fused_llama8b_reduced_k40": (LLAMA8B.scaled(batch=2, layers=3, prefill_len=1200, budget=120), 4, 40, True),
@@ -94,7 +95,7 @@ CASES = {
 @pytest.mark.parametrize("name", list(CASES))
 def test_rank_trace_lockstep(name):
     cfg, steps, k, fused = CASES[name]
-    m = run_trace(cfg, steps, k, fused)
+    m = run_trace(cfg, steps, k, fused, max_pos=300_000 if name == "lazy_r4_min" else None)
     steady = [x["ema_churn"] for x in m[cfg.batch:]]
     print(f"{name}: EMA churn {np.nanmean(steady):.4g}, raw churn {np.nanmean([x['raw_churn'] for x in m]):.4g}")
 
