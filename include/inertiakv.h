@@ -155,7 +155,8 @@ kv_status kv_compact(const kv_shape* shape, int32_t n, int32_t budget, const uin
  *     n_in existing utilities;
  *  2. refresh steps only: kv_score_ema over the n_in + 1 tokens with q, cur_pos = new_pos;
  *  3. if n_in + 1 > B: select the top B (stale utilities on non-refresh steps) and compact as kv_compact.
- * *n_out (HOST pointer) receives min(B, n_in + 1).  keep_out (nullable) receives the decision over the
+ * *n_out (HOST pointer) receives min(B, n_in + 1); cache rows at and beyond *n_out are unspecified
+ * afterwards.  keep_out (nullable) receives the decision over the
  * n_in + 1 slots before compaction; s_out (nullable) the per-layer scores of a refresh step; trace (nullable)
  * timing events; rank_trace (nullable) the diagnostics above. */
 kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in,

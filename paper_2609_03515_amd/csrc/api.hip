@@ -269,9 +269,8 @@ kv_status check_params(const kv_params* params) {
 // Refresh set (Eq. 5); Score-Free refreshes only at the first decode step.
 bool is_refresh(const kv_params& p, int t) { return p.score_free ? (t == 1) : ((t - 1) % p.refresh_period == 0); }
 
-kv_status run_append(const kv_shape& s, const kv_params& p, int t, int n_in, int new_pos, const void* k_new,
-                     const void* v_new, void* k, void* v, float* u, int32_t* pos, hipStream_t st,
-                     const kv_trace* tr) {
+AppendArgs append_args(const kv_shape& s, const kv_params& p, int t, int n_in, int new_pos, const void* k_new,
+                       const void* v_new, void* k, void* v, float* u, int32_t* pos) {
     AppendArgs ap{};
     ap.k = k;
     ap.v = v;
@@ -287,6 +286,13 @@ kv_status run_append(const kv_shape& s, const kv_params& p, int t, int n_in, int
     ap.n_in = n_in;
     ap.new_pos = new_pos;
     ap.init_mode = is_refresh(p, t) ? 0 : (p.nonrefresh_init == KV_INIT_MEAN ? 1 : 2);
+    return ap;
+}
+
+kv_status run_append(const kv_shape& s, const kv_params& p, int t, int n_in, int new_pos, const void* k_new,
+                     const void* v_new, void* k, void* v, float* u, int32_t* pos, hipStream_t st,
+                     const kv_trace* tr) {
+    AppendArgs ap = append_args(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos);
     record(tr, 0, true, st);
     kv_status rc = hip_status(launch_append(ap, st));
     record(tr, 0, false, st);
@@ -300,6 +306,14 @@ kv_status check_rank_trace(const kv_rank_trace* rt) {
     if (rt->k < 1 || rt->max_pos < 1 || !rt->state || !rt->counts) return KV_ERR_INVALID_ARG;
     if (!aligned(rt->state, 4) || !aligned(rt->counts, 4)) return KV_ERR_UNSUPPORTED;
     return KV_OK;
+}
+
+// A step that is not traced (not a refresh step) still writes its counts: row 0 of each sequence = 0.
+kv_status mark_untraced(const kv_shape& s, const kv_rank_trace* rt, hipStream_t st) {
+    TraceArgs ta{};
+    ta.counts = rt->counts;
+    ta.batch = s.batch;
+    return hip_status(launch_trace_stats(ta, true, st));
 }
 
 // Top-B selection over the n cached tokens and, when tokens are dropped, the compaction.  With a rank trace
@@ -321,7 +335,7 @@ kv_status run_select_compact(const kv_shape& s, const Layout& L, int n, int budg
         ta.max_pos = rt->max_pos;
         ta.words = (int)trace_words(rt->max_pos);
         if (!traced) {
-            if ((rc = hip_status(launch_trace_stats(ta, true, st))) != KV_OK) return rc;
+            if ((rc = mark_untraced(s, rt, st)) != KV_OK) return rc;
         } else if (!keep_out) {
             keep_out = at<uint8_t>(ws, L.kmask_off);  // the statistics need the decision
         }
@@ -444,8 +458,19 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
 
-    if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, st, trace)) != KV_OK) return rc;
     const bool refresh = is_refresh(p, t);
+    if (!refresh && n_in <= p.budget) {
+        // every Lazy / Score-Free step after the first: one kernel per sequence
+        AppendArgs ap = append_args(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos);
+        if (rank_trace && (rc = mark_untraced(s, rank_trace, st)) != KV_OK) return rc;
+        record(trace, 0, true, st);
+        rc = hip_status(launch_nonrefresh(ap, keep_out, p.budget, st));
+        record(trace, 0, false, st);
+        if (rc != KV_OK) return rc;
+        *n_out = n < p.budget ? n : p.budget;
+        return KV_OK;
+    }
+    if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, st, trace)) != KV_OK) return rc;
     if (refresh) {
         record(trace, 1, true, st);
         rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, ws, st, trace);

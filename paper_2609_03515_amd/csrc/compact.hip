@@ -87,7 +87,121 @@ __global__ __launch_bounds__(kThreads) void append_kernel(AppendArgs a) {
     reinterpret_cast<u32x4*>(dst)[c] = reinterpret_cast<const u32x4*>(src)[c];
 }
 
+// A whole non-refresh step of one sequence whose cache holds n_in <= B tokens (every Lazy / Score-Free step
+// after the first): the newcomer's prior from the n_in utilities (mean or min, as append_kernel), the single
+// eviction among the n_in + 1 tokens (minimum under (u ascending, position descending), as select_kernel's
+// one-eviction case) and the newcomer's K/V rows written straight into the slot it takes: the evicted one
+// (the same cache, u and pos as append + select + hole-fill), or slot n_in when nothing is evicted.  When the
+// newcomer itself is evicted nothing is written.
+constexpr int kNrThreads = 1024;
+constexpr int kNrWaves = kNrThreads / kWave;
+
+__global__ __launch_bounds__(kNrThreads) void nonrefresh_kernel(AppendArgs a, uint8_t* keep_out, int budget) {
+    __shared__ float red[kNrWaves];
+    __shared__ uint32_t best_key[kNrWaves];
+    __shared__ int best_pos[kNrWaves], best_idx[kNrWaves];
+    __shared__ float prior_sh;
+    __shared__ int slot_sh;
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    float* ub = a.u + (size_t)b * a.cap;
+    int32_t* pb = a.pos + (size_t)b * a.cap;
+    const int n = a.n_in;
+
+    float v = a.init_mode == 2 ? INFINITY : 0.0f;
+    for (int i = tid; i < n; i += kNrThreads) v = a.init_mode == 2 ? fminf(v, ub[i]) : v + ub[i];
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) {
+        const float w = __shfl_xor(v, o, kWave);
+        v = a.init_mode == 2 ? fminf(v, w) : v + w;
+    }
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    if (tid == 0) {
+        float r = red[0];
+        for (int w = 1; w < kNrWaves; ++w) r = a.init_mode == 2 ? fminf(r, red[w]) : r + red[w];
+        prior_sh = n > 0 ? (a.init_mode == 2 ? r : r / (float)n) : 0.0f;
+    }
+    __syncthreads();
+    const float prior = prior_sh;
+
+    int slot = n;  // no eviction: the newcomer takes slot n
+    if (n + 1 > budget) {
+        // argmin over the n cached tokens and the newcomer (index n)
+        uint32_t bk = 0xffffffffu;
+        int bp = -1, bi = -1;
+        for (int i = tid; i <= n; i += kNrThreads) {
+            const uint32_t key = float_key(i < n ? ub[i] : prior);
+            const int ps = i < n ? pb[i] : a.new_pos;
+            if (bi < 0 || key < bk || (key == bk && ps > bp)) {
+                bk = key;
+                bp = ps;
+                bi = i;
+            }
+        }
+#pragma unroll
+        for (int o = kWave / 2; o >= 1; o >>= 1) {
+            const uint32_t ok = __shfl_xor(bk, o, kWave);
+            const int op = __shfl_xor(bp, o, kWave);
+            const int oi = __shfl_xor(bi, o, kWave);
+            if (oi >= 0 && (bi < 0 || ok < bk || (ok == bk && op > bp))) {
+                bk = ok;
+                bp = op;
+                bi = oi;
+            }
+        }
+        if (lane == 0) {
+            best_key[wave] = bk;
+            best_pos[wave] = bp;
+            best_idx[wave] = bi;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            bk = best_key[0];
+            bp = best_pos[0];
+            bi = best_idx[0];
+            for (int w = 1; w < kNrWaves; ++w) {
+                const int oi = best_idx[w];
+                if (oi >= 0 && (bi < 0 || best_key[w] < bk || (best_key[w] == bk && best_pos[w] > bp))) {
+                    bk = best_key[w];
+                    bp = best_pos[w];
+                    bi = oi;
+                }
+            }
+            slot_sh = bi;
+        }
+        __syncthreads();
+        slot = slot_sh;
+        if (keep_out)
+            for (int i = tid; i <= n; i += kNrThreads) keep_out[(size_t)b * a.cap + i] = i != slot;
+        if (slot == n) return;  // the newcomer is evicted at once
+    } else if (keep_out) {
+        for (int i = tid; i <= n; i += kNrThreads) keep_out[(size_t)b * a.cap + i] = 1;
+    }
+    if (tid == 0) {
+        ub[slot] = prior;
+        pb[slot] = a.new_pos;
+    }
+    const int lpr = a.row_bytes / 16;
+    const int rows = a.layers * a.hkv * 2;
+    for (int c = tid; c < rows * lpr; c += kNrThreads) {
+        const int chunk = c % lpr;
+        const int r = c / lpr;
+        const int tensor = r / (a.layers * a.hkv);
+        const int lg = r % (a.layers * a.hkv);  // l * hkv + g
+        const size_t row = ((size_t)(lg / a.hkv) * a.batch + b) * a.hkv + lg % a.hkv;  // (l, b, g)
+        const char* src = static_cast<const char*>(tensor ? a.v_new : a.k_new) + row * a.row_bytes;
+        char* dst = static_cast<char*>(tensor ? a.v : a.k) + (row * a.cap + slot) * a.row_bytes;
+        reinterpret_cast<u32x4*>(dst)[chunk] = reinterpret_cast<const u32x4*>(src)[chunk];
+    }
+}
+
 }  // namespace
+
+hipError_t launch_nonrefresh(const AppendArgs& a, uint8_t* keep_out, int budget, hipStream_t s) {
+    hipLaunchKernelGGL(nonrefresh_kernel, dim3(a.batch), dim3(kNrThreads), 0, s, a, keep_out, budget);
+    return hipGetLastError();
+}
 
 hipError_t launch_move(const MoveArgs& a, hipStream_t s) {
     const long long threads = (long long)a.batch * a.layers * a.hkv * 2 * a.max_pairs * (a.row_bytes / 16);

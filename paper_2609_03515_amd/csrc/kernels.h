@@ -146,5 +146,8 @@ struct AppendArgs {
     int init_mode;  // 0: zero (refresh step), 1: mean, 2: min of u[0, n_in)
 };
 hipError_t launch_append(const AppendArgs& a, hipStream_t s);
+// Append + single eviction + the newcomer's rows into the freed slot, one workgroup per sequence, for a
+// non-refresh step on a cache of n_in <= budget tokens (init_mode 1 or 2).
+hipError_t launch_nonrefresh(const AppendArgs& a, uint8_t* keep_out, int budget, hipStream_t s);
 
 }  // namespace ikv

@@ -70,6 +70,8 @@ CASES = {
     "qwen_reduced": (QWEN.scaled(batch=3, layers=3, prefill_len=1000, budget=250), 5),
     "qwen_split_step1": (QWEN.scaled(batch=1, layers=2, prefill_len=3000, budget=750), 3),
     "under_budget": (TINY.scaled(prefill_len=40, budget=45), 8),
+    # Lazy steps that first only append (cache under budget), then evict one token each
+    "lazy_under_budget": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=40, budget=44, nonrefresh_init="mean"), 9),
 }
 
 
