@@ -4,10 +4,11 @@ from __future__ import annotations
 import numpy as np
 import torch
 
-from oracle import Cache, Params
+from oracle import Cache, Params, to_f64
 from workload import raw_numpy
 
 REL_TOL = 1e-3        # scores and utilities
+O_REL = 1e-3          # attention outputs, relative to sum_i a(i) |v_i|
 ABS_TOL = 1e-12
 BAND = 1e-4           # retention sets may differ only for utilities this close to the B-th value
 
@@ -72,3 +73,14 @@ def lockstep_adopter(keep_gpu_rows: np.ndarray, budget: int, what: str, counter:
         counter.append(flips)
         return np.asarray(keep_gpu_rows[:, :n], dtype=bool)
     return adopt
+
+
+def assert_o(o_gpu, o_ref, scale, dtype, what):
+    """Attention outputs: |o_gpu - o_ref| <= 1e-3 * sum_i a(i)|v_i| (+ 2^-8 |o_ref| for a bf16 output)."""
+    got = to_f64(raw_numpy(o_gpu), dtype)
+    assert got.shape == o_ref.shape, (what, got.shape, o_ref.shape)
+    lim = O_REL * scale + (2.0 ** -8 if dtype == "bf16" else 0.0) * np.abs(o_ref) + 1e-12
+    err = np.abs(got - o_ref)
+    bad = np.nonzero(err > lim)
+    assert len(bad[0]) == 0, (f"{what}: {len(bad[0])} of {err.size} outputs outside tolerance; worst "
+                              f"err/scale {np.max(err / (scale + 1e-30)):.3e} at {tuple(b[0] for b in bad)}")

@@ -13,25 +13,12 @@ import pytest
 import torch
 
 from oracle import attention_output, evict_step, layer_scores, refresh_due, to_f64
-from parity import assert_close, lockstep_adopter, oracle_cache, oracle_params, to_device
+from parity import assert_close, assert_o, lockstep_adopter, oracle_cache, oracle_params, to_device
 from workload import LLAMA8B, LLAMA8B_LAZY, QWEN, TINY, Workload, raw_numpy
 
 pytestmark = pytest.mark.gpu
 
 B = pytest.importorskip("paper_2609_03515_amd.binding")
-
-O_REL = 1e-3
-
-
-def assert_o(o_gpu, o_ref, scale, dtype, what):
-    got = to_f64(raw_numpy(o_gpu), dtype)
-    assert got.shape == o_ref.shape, (what, got.shape, o_ref.shape)
-    lim = O_REL * scale + (2.0 ** -8 if dtype == "bf16" else 0.0) * np.abs(o_ref) + 1e-12
-    err = np.abs(got - o_ref)
-    bad = np.nonzero(err > lim)
-    assert len(bad[0]) == 0, (f"{what}: {len(bad[0])} of {err.size} outputs outside tolerance; worst "
-                              f"err/scale {np.max(err / (scale + 1e-30)):.3e} at {tuple(b[0] for b in bad)}")
-
 
 def attend_layers(shape, cfg, n, q, k, v, pos, cur_pos, emit, ws, per_layer):
     o = torch.empty_like(q)
