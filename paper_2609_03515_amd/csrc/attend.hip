@@ -24,6 +24,9 @@ namespace {
 #ifndef IKV_ATTN_TARGET
 #define IKV_ATTN_TARGET 512
 #endif
+#ifndef IKV_ATTN_NBUF
+#define IKV_ATTN_NBUF 0
+#endif
 #ifndef IKV_ATTN_MIN_ROWS
 #define IKV_ATTN_MIN_ROWS 256
 #endif
@@ -103,7 +106,7 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     constexpr int RPG = L::RPG, CPL = L::CPL, RPW = L::RPW, LPR = L::LPR, EPC = L::EPC;
     // K/V loads of two units in flight, one when a lane's share of a unit is already large (a single head
     // per KV head: 16 rows per lane), which would otherwise spill
-    constexpr int kNbuf = RPG * CPL > 8 ? 1 : 2;
+    constexpr int kNbuf = IKV_ATTN_NBUF > 0 ? IKV_ATTN_NBUF : (RPG * CPL > 8 ? 1 : 2);
 
     extern __shared__ float zs[];
     __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
@@ -165,6 +168,16 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
         }
     }
 
+    // the V stream's first loads are issued now, so their latency overlaps the K pass's epilogue (barriers
+    // wait for LDS only, not for these loads)
+    chunk_t vbuf[kNbuf][RPG][CPL];
+    int vunit[kNbuf];
+#pragma unroll
+    for (int j = 0; j < kNbuf - 1; ++j) {
+        vunit[j] = claim(1);
+        ln.load_rows(vrs, vunit[j], vbuf[j]);
+    }
+
     // 2. per-head max, exponentials in place, per-head sums; several chunks: the logits go to HBM for the
     //    score's finish kernel
 #pragma unroll
@@ -218,13 +231,7 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
 #pragma unroll
             for (int x = 0; x < EPC; ++x) acc[h][c][x] = 0.0f;
     {
-        chunk_t vbuf[kNbuf][RPG][CPL];
-        int ubuf[kNbuf];
-#pragma unroll
-        for (int j = 0; j < kNbuf - 1; ++j) {
-            ubuf[j] = claim(1);
-            ln.load_rows(vrs, ubuf[j], vbuf[j]);
-        }
+        int (&ubuf)[kNbuf] = vunit;
         bool more = true;
         while (more) {
 #pragma unroll
