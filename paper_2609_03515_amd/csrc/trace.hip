@@ -56,13 +56,26 @@ __global__ __launch_bounds__(kStatThreads) void trace_stats_kernel(TraceArgs a, 
             c_ee += in_e && (bm[a.words + (p >> 5)] & bit);
         }
     }
-    atomicAdd(&cnt[0], c_r);
-    atomicAdd(&cnt[1], c_e);
-    atomicAdd(&cnt[2], c_rr);
-    atomicAdd(&cnt[3], c_ee);
-    atomicAdd(&cnt[4], c_re);
-    atomicAdd(&cnt[5], c_rev);
-    atomicOr(&cnt[6], oob);
+    // one LDS atomic per wave and counter (a thousand same-address atomics would serialise)
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) {
+        c_r += __shfl_xor(c_r, o, kWave);
+        c_e += __shfl_xor(c_e, o, kWave);
+        c_rr += __shfl_xor(c_rr, o, kWave);
+        c_ee += __shfl_xor(c_ee, o, kWave);
+        c_re += __shfl_xor(c_re, o, kWave);
+        c_rev += __shfl_xor(c_rev, o, kWave);
+        oob |= __shfl_xor(oob, o, kWave);
+    }
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+        atomicAdd(&cnt[0], c_r);
+        atomicAdd(&cnt[1], c_e);
+        atomicAdd(&cnt[2], c_rr);
+        atomicAdd(&cnt[3], c_ee);
+        atomicAdd(&cnt[4], c_re);
+        atomicAdd(&cnt[5], c_rev);
+        atomicOr(&cnt[6], oob);
+    }
     __syncthreads();  // every read of the previous sets is done
     for (int w = threadIdx.x; w < 2 * a.words; w += kStatThreads) bm[w] = 0u;
     if (!kLds) __threadfence();

@@ -6,8 +6,7 @@
 //          over ln(n), one factor per layer and sequence.
 // These kernels produce the norms (with the reciprocal of each slab's mean) and the entropy factors; the
 // fold applies them while it sums the group sums r (which stay the plain attention).
-#include "kernels.h"
-#include "kv_common.h"
+#include "stream_lane.h"
 
 namespace ikv {
 namespace {
@@ -15,9 +14,10 @@ namespace {
 constexpr int kVThreads = 512;
 
 // One workgroup per (layer, sequence, KV head) slab: a value row is read as 16-byte chunks by an aligned
-// group of LPR lanes (kRows rows per lane and pass, loads issued together), the sum of squares is reduced
-// over the group, and the group's first lane stores the norm; the norms are summed in a fixed order for the
-// mean.
+// group of LPR lanes, kRows rows per lane and pass; the next pass's loads are issued before the current pass
+// is reduced (raw buffer loads over the slab's live rows: reads past the end return zero and are not
+// stored).  The sum of squares is reduced over the lane group with DPP, the group's first lane stores the
+// norm, and the norms are summed in a fixed order for the mean.
 constexpr int kRows = 4;
 
 template <typename T, int D>
@@ -26,22 +26,25 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
     using chunk_t = typename E::chunk_t;
     constexpr int EPC = E::kPerChunk, CH = D / EPC, LPR = CH >= 16 ? 16 : CH, CPL = CH / LPR;
     constexpr int RPI = kVThreads / LPR;  // rows per pass and row slot
+    constexpr int kRowBytes = D * (int)sizeof(T);
     __shared__ float part[kVThreads / kWave];
     const size_t slab = blockIdx.x;
-    const T* vs = static_cast<const T*>(a.v) + slab * a.cap * D;
+    const __amdgpu_buffer_rsrc_t vrs =
+        raw_rsrc(static_cast<const T*>(a.v) + slab * a.cap * D, a.n * kRowBytes);
     const int p = threadIdx.x % LPR;
     const int rsub = threadIdx.x / LPR;
-    float* out = a.vnorm + slab * a.n_stride;
-    float sum = 0.0f;
-    for (int base = 0; base < a.n; base += RPI * kRows) {  // uniform trip count: every lane joins the shuffles
-        chunk_t c[kRows][CPL];
+    const __amdgpu_buffer_rsrc_t out = raw_rsrc(a.vnorm + slab * a.n_stride, a.n_stride * 4);
+    auto load = [&](int base, chunk_t (&c)[kRows][CPL]) {
 #pragma unroll
-        for (int k = 0; k < kRows; ++k) {
-            const int row = min(base + k * RPI + rsub, a.n - 1);  // clamped: the duplicate is not stored
+        for (int k = 0; k < kRows; ++k)
 #pragma unroll
             for (int cc = 0; cc < CPL; ++cc)
-                c[k][cc] = *reinterpret_cast<const chunk_t*>(vs + (size_t)row * D + (p + cc * LPR) * EPC);
-        }
+                c[k][cc] = __builtin_bit_cast(
+                    chunk_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                 vrs, (base + k * RPI + rsub) * kRowBytes + (p + cc * LPR) * 16, 0, kNonTemporal));
+    };
+    float sum = 0.0f;
+    auto reduce = [&](int base, const chunk_t (&c)[kRows][CPL]) {
 #pragma unroll
         for (int k = 0; k < kRows; ++k) {
             float ss = 0.0f;
@@ -56,10 +59,19 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
             const int row = base + k * RPI + rsub;
             if (row < a.n && p == 0) {
                 const float nrm = sqrtf(ss);
-                out[row] = nrm;
+                store_stream(out, row * 4, nrm);  // written while V streams: streaming-result policy
                 sum += nrm;
             }
         }
+    };
+    constexpr int kPass = RPI * kRows;
+    chunk_t c0[kRows][CPL], c1[kRows][CPL];
+    load(0, c0);
+    for (int base = 0; base < a.n; base += 2 * kPass) {  // uniform trip count: every lane joins the DPP sums
+        load(base + kPass, c1);
+        reduce(base, c0);
+        load(base + 2 * kPass, c0);
+        reduce(base + kPass, c1);
     }
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) sum += __shfl_xor(sum, o, kWave);
