@@ -464,7 +464,8 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
         AppendArgs ap = append_args(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos);
         if (rank_trace && (rc = mark_untraced(s, rank_trace, st)) != KV_OK) return rc;
         record(trace, 0, true, st);
-        rc = hip_status(launch_nonrefresh(ap, keep_out, p.budget, st));
+        // the per-sequence pair counts of the workspace are free on this path: they carry the newcomer's slot
+        rc = hip_status(launch_nonrefresh(ap, keep_out, p.budget, at<int32_t>(ws, L.np_off), st));
         record(trace, 0, false, st);
         if (rc != KV_OK) return rc;
         *n_out = n < p.budget ? n : p.budget;

@@ -87,119 +87,152 @@ __global__ __launch_bounds__(kThreads) void append_kernel(AppendArgs a) {
     reinterpret_cast<u32x4*>(dst)[c] = reinterpret_cast<const u32x4*>(src)[c];
 }
 
-// A whole non-refresh step of one sequence whose cache holds n_in <= B tokens (every Lazy / Score-Free step
-// after the first): the newcomer's prior from the n_in utilities (mean or min, as append_kernel), the single
-// eviction among the n_in + 1 tokens (minimum under (u ascending, position descending), as select_kernel's
-// one-eviction case) and the newcomer's K/V rows written straight into the slot it takes: the evicted one
-// (the same cache, u and pos as append + select + hole-fill), or slot n_in when nothing is evicted.  When the
-// newcomer itself is evicted nothing is written.
+// Decision of a non-refresh step of one sequence whose cache holds n_in <= B tokens (every Lazy / Score-Free
+// step after the first), in one pass over u and pos: the newcomer's prior (mean or min of the n_in utilities,
+// as append_kernel) and the minimum of the cached tokens under (u ascending, position descending); the
+// newcomer is then compared with that minimum (select_kernel's one-eviction rule over the n_in + 1 tokens).
+// The newcomer takes the evicted slot (the same cache, u and pos as append + select + hole-fill), slot n_in
+// when nothing is evicted, or no slot when it is itself evicted (slot[b] = -1); its rows are copied here
+// (copy_rows) or by newcomer_rows_kernel.
 constexpr int kNrThreads = 1024;
 constexpr int kNrWaves = kNrThreads / kWave;
 
-__global__ __launch_bounds__(kNrThreads) void nonrefresh_kernel(AppendArgs a, uint8_t* keep_out, int budget) {
+struct Cand {  // eviction candidate: order key of u, position, slot
+    uint32_t key;
+    int pos, idx;
+};
+__device__ __forceinline__ bool evicts_before(const Cand& a, const Cand& b) {  // a leaves before b
+    return b.idx < 0 || (a.idx >= 0 && (a.key < b.key || (a.key == b.key && a.pos > b.pos)));
+}
+
+__global__ __launch_bounds__(kNrThreads) void nonrefresh_kernel(AppendArgs a, uint8_t* keep_out, int budget,
+                                                                int* slot_out, int copy_rows) {
     __shared__ float red[kNrWaves];
-    __shared__ uint32_t best_key[kNrWaves];
-    __shared__ int best_pos[kNrWaves], best_idx[kNrWaves];
-    __shared__ float prior_sh;
+    __shared__ Cand best[kNrWaves];
     __shared__ int slot_sh;
     const int b = blockIdx.x;
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     float* ub = a.u + (size_t)b * a.cap;
     int32_t* pb = a.pos + (size_t)b * a.cap;
     const int n = a.n_in;
+    const bool use_min = a.init_mode == 2;
 
-    float v = a.init_mode == 2 ? INFINITY : 0.0f;
-    for (int i = tid; i < n; i += kNrThreads) v = a.init_mode == 2 ? fminf(v, ub[i]) : v + ub[i];
+    float v = use_min ? INFINITY : 0.0f;
+    Cand c{0xffffffffu, -1, -1};
+    for (int i = tid; i < n; i += kNrThreads) {
+        const float ui = ub[i];
+        v = use_min ? fminf(v, ui) : v + ui;
+        const Cand o{float_key(ui), pb[i], i};
+        if (evicts_before(o, c)) c = o;
+    }
 #pragma unroll
     for (int o = kWave / 2; o >= 1; o >>= 1) {
         const float w = __shfl_xor(v, o, kWave);
-        v = a.init_mode == 2 ? fminf(v, w) : v + w;
+        v = use_min ? fminf(v, w) : v + w;
+        const Cand x{(uint32_t)__shfl_xor((int)c.key, o, kWave), __shfl_xor(c.pos, o, kWave),
+                     __shfl_xor(c.idx, o, kWave)};
+        if (evicts_before(x, c)) c = x;
     }
-    if (lane == 0) red[wave] = v;
+    if (lane == 0) {
+        red[wave] = v;
+        best[wave] = c;
+    }
     __syncthreads();
     if (tid == 0) {
         float r = red[0];
-        for (int w = 1; w < kNrWaves; ++w) r = a.init_mode == 2 ? fminf(r, red[w]) : r + red[w];
-        prior_sh = n > 0 ? (a.init_mode == 2 ? r : r / (float)n) : 0.0f;
+        c = best[0];
+        for (int w = 1; w < kNrWaves; ++w) {
+            r = use_min ? fminf(r, red[w]) : r + red[w];
+            if (evicts_before(best[w], c)) c = best[w];
+        }
+        const float prior = n > 0 ? (use_min ? r : r / (float)n) : 0.0f;
+        int slot = n;  // room left: the newcomer is appended
+        if (n + 1 > budget) {
+            const Cand mine{float_key(prior), a.new_pos, n};
+            slot = evicts_before(mine, c) ? -1 : c.idx;
+        }
+        if (slot >= 0) {
+            ub[slot] = prior;
+            pb[slot] = a.new_pos;
+        }
+        slot_out[b] = slot;
+        slot_sh = slot;
     }
     __syncthreads();
-    const float prior = prior_sh;
-
-    int slot = n;  // no eviction: the newcomer takes slot n
-    if (n + 1 > budget) {
-        // argmin over the n cached tokens and the newcomer (index n)
-        uint32_t bk = 0xffffffffu;
-        int bp = -1, bi = -1;
-        for (int i = tid; i <= n; i += kNrThreads) {
-            const uint32_t key = float_key(i < n ? ub[i] : prior);
-            const int ps = i < n ? pb[i] : a.new_pos;
-            if (bi < 0 || key < bk || (key == bk && ps > bp)) {
-                bk = key;
-                bp = ps;
-                bi = i;
+    const int slot = slot_sh;
+    if (keep_out) {
+        const int evicted = slot < 0 ? n : (slot < n ? slot : -1);
+        for (int i = tid; i <= n; i += kNrThreads) keep_out[(size_t)b * a.cap + i] = i != evicted;
+    }
+    if (!copy_rows || slot < 0) return;
+    // rows r = (tensor, l, g) in [0, 2 L hkv), 16-byte chunk ch; quotients by float reciprocals (exact: the
+    // numerators are far below 2^22 and the +0.5 keeps them off integer boundaries)
+    const int lpr = a.row_bytes / 16;
+    const int total = a.layers * a.hkv * 2 * lpr;
+    const float inv_lpr = 1.0f / (float)lpr, inv_hkv = 1.0f / (float)a.hkv, inv_lg = 1.0f / (float)(a.layers * a.hkv);
+    constexpr int kCopy = 8;
+    for (int c0 = tid; c0 < total; c0 += kNrThreads * kCopy) {
+        u32x4 buf[kCopy];
+        size_t dsto[kCopy];
+#pragma unroll
+        for (int j = 0; j < kCopy; ++j) {
+            const int c = c0 + j * kNrThreads;
+            if (c < total) {
+                const int r = (int)(((float)c + 0.5f) * inv_lpr);
+                const int ch = c - r * lpr;
+                const int tensor = (int)(((float)r + 0.5f) * inv_lg);
+                const int lg = r - tensor * a.layers * a.hkv;
+                const int l = (int)(((float)lg + 0.5f) * inv_hkv);
+                const size_t row = ((size_t)l * a.batch + b) * a.hkv + (lg - l * a.hkv);
+                buf[j] = reinterpret_cast<const u32x4*>(static_cast<const char*>(tensor ? a.v_new : a.k_new) +
+                                                        row * a.row_bytes)[ch];
+                dsto[j] = ((row * a.cap + slot) * a.row_bytes) / 16 + ch + (tensor ? (size_t)1 << 62 : 0);
             }
         }
 #pragma unroll
-        for (int o = kWave / 2; o >= 1; o >>= 1) {
-            const uint32_t ok = __shfl_xor(bk, o, kWave);
-            const int op = __shfl_xor(bp, o, kWave);
-            const int oi = __shfl_xor(bi, o, kWave);
-            if (oi >= 0 && (bi < 0 || ok < bk || (ok == bk && op > bp))) {
-                bk = ok;
-                bp = op;
-                bi = oi;
+        for (int j = 0; j < kCopy; ++j) {
+            const int c = c0 + j * kNrThreads;
+            if (c < total) {
+                const bool isv = (dsto[j] >> 62) != 0;
+                reinterpret_cast<u32x4*>(isv ? a.v : a.k)[dsto[j] & (((size_t)1 << 62) - 1)] = buf[j];
             }
         }
-        if (lane == 0) {
-            best_key[wave] = bk;
-            best_pos[wave] = bp;
-            best_idx[wave] = bi;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            bk = best_key[0];
-            bp = best_pos[0];
-            bi = best_idx[0];
-            for (int w = 1; w < kNrWaves; ++w) {
-                const int oi = best_idx[w];
-                if (oi >= 0 && (bi < 0 || best_key[w] < bk || (best_key[w] == bk && best_pos[w] > bp))) {
-                    bk = best_key[w];
-                    bp = best_pos[w];
-                    bi = oi;
-                }
-            }
-            slot_sh = bi;
-        }
-        __syncthreads();
-        slot = slot_sh;
-        if (keep_out)
-            for (int i = tid; i <= n; i += kNrThreads) keep_out[(size_t)b * a.cap + i] = i != slot;
-        if (slot == n) return;  // the newcomer is evicted at once
-    } else if (keep_out) {
-        for (int i = tid; i <= n; i += kNrThreads) keep_out[(size_t)b * a.cap + i] = 1;
     }
-    if (tid == 0) {
-        ub[slot] = prior;
-        pb[slot] = a.new_pos;
-    }
+}
+
+// The newcomer's K/V rows of every (layer, KV head) into its slot (nothing where slot[b] < 0).
+__global__ __launch_bounds__(kThreads) void newcomer_rows_kernel(AppendArgs a, const int* slot) {
     const int lpr = a.row_bytes / 16;
-    const int rows = a.layers * a.hkv * 2;
-    for (int c = tid; c < rows * lpr; c += kNrThreads) {
-        const int chunk = c % lpr;
-        const int r = c / lpr;
-        const int tensor = r / (a.layers * a.hkv);
-        const int lg = r % (a.layers * a.hkv);  // l * hkv + g
-        const size_t row = ((size_t)(lg / a.hkv) * a.batch + b) * a.hkv + lg % a.hkv;  // (l, b, g)
-        const char* src = static_cast<const char*>(tensor ? a.v_new : a.k_new) + row * a.row_bytes;
-        char* dst = static_cast<char*>(tensor ? a.v : a.k) + (row * a.cap + slot) * a.row_bytes;
-        reinterpret_cast<u32x4*>(dst)[chunk] = reinterpret_cast<const u32x4*>(src)[chunk];
-    }
+    const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    const long long total = (long long)a.layers * a.batch * a.hkv * 2 * lpr;
+    if (gid >= total) return;
+    const int ch = (int)(gid % lpr);
+    long long row = gid / lpr;  // (tensor, l, b, g) with tensor outermost
+    const int tensor = (int)(row / ((long long)a.layers * a.batch * a.hkv));
+    row %= (long long)a.layers * a.batch * a.hkv;  // == (l * batch + b) * hkv + g
+    const int s = slot[(row / a.hkv) % a.batch];
+    if (s < 0) return;
+    const char* src = static_cast<const char*>(tensor ? a.v_new : a.k_new) + (size_t)row * a.row_bytes;
+    char* dst = static_cast<char*>(tensor ? a.v : a.k) + ((size_t)row * a.cap + s) * a.row_bytes;
+    reinterpret_cast<u32x4*>(dst)[ch] = reinterpret_cast<const u32x4*>(src)[ch];
 }
 
 }  // namespace
 
-hipError_t launch_nonrefresh(const AppendArgs& a, uint8_t* keep_out, int budget, hipStream_t s) {
-    hipLaunchKernelGGL(nonrefresh_kernel, dim3(a.batch), dim3(kNrThreads), 0, s, a, keep_out, budget);
+// Where the newcomer's rows are copied depends on the prior policy.  Under the minimum prior the newcomer
+// ties the lowest utility and, holding the newest position, is normally evicted at once: the decision kernel
+// copies the rows itself when needed (6.0 us per step at the 8B shape, against 8.0 with a second launch that
+// then has nothing to do).  Under the mean prior the newcomer is normally kept: one workgroup per sequence
+// copies 128 KB of rows slowly, a kernel over all rows does it in a fraction (8.6 us against 11.0).
+hipError_t launch_nonrefresh(const AppendArgs& a, uint8_t* keep_out, int budget, int* slot, hipStream_t s) {
+    const int copy_in_decision = a.init_mode == 2;
+    hipLaunchKernelGGL(nonrefresh_kernel, dim3(a.batch), dim3(kNrThreads), 0, s, a, keep_out, budget, slot,
+                       copy_in_decision);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || copy_in_decision) return e;
+    const long long threads = (long long)a.layers * a.batch * a.hkv * 2 * (a.row_bytes / 16);
+    hipLaunchKernelGGL(newcomer_rows_kernel, dim3((unsigned)((threads + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                       s, a, slot);
     return hipGetLastError();
 }
 

@@ -146,8 +146,9 @@ struct AppendArgs {
     int init_mode;  // 0: zero (refresh step), 1: mean, 2: min of u[0, n_in)
 };
 hipError_t launch_append(const AppendArgs& a, hipStream_t s);
-// Append + single eviction + the newcomer's rows into the freed slot, one workgroup per sequence, for a
-// non-refresh step on a cache of n_in <= budget tokens (init_mode 1 or 2).
-hipError_t launch_nonrefresh(const AppendArgs& a, uint8_t* keep_out, int budget, hipStream_t s);
+// A non-refresh step on a cache of n_in <= budget tokens (init_mode 1 or 2): the newcomer's prior, the single
+// eviction and the newcomer's slot (one workgroup per sequence; slot[batch] in device memory), then its rows
+// copied into that slot by a kernel over every (layer, KV head) row.
+hipError_t launch_nonrefresh(const AppendArgs& a, uint8_t* keep_out, int budget, int* slot, hipStream_t s);
 
 }  // namespace ikv

@@ -72,6 +72,7 @@ CASES = {
     "under_budget": (TINY.scaled(prefill_len=40, budget=45), 8),
     # Lazy steps that first only append (cache under budget), then evict one token each
     "lazy_under_budget": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=40, budget=44, nonrefresh_init="mean"), 9),
+    "lazy_under_budget_min": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=40, budget=44), 9),
 }
 
 
@@ -105,3 +106,46 @@ def test_scorer_variants_lockstep(name, vnorm, entropy):
     """Sec. 5.1 scorer perturbations through kv_evict_step, in lockstep with the oracle."""
     cfg, steps = VARIANT_CASES[name]
     run_lockstep(cfg, steps, vnorm=vnorm, entropy=entropy)
+
+
+@pytest.mark.parametrize("init", ["min", "mean"])
+def test_nonrefresh_newcomer_kept_on_position_tie(init):
+    """Non-refresh step where the newcomer survives: under the min prior it ties the lowest utility, and the
+    cached token holding that utility has a higher position than the newcomer (positions need not grow), so
+    that token is evicted and the newcomer's rows must land in its slot."""
+    cfg = LLAMA8B_LAZY.scaled(batch=2, layers=3, prefill_len=60, budget=60, nonrefresh_init=init)
+    w = Workload(cfg)
+    cap = cfg.prefill_len + 1
+    st = w.prefill(capacity=cap)
+    rng = np.random.default_rng(5)
+    u = rng.uniform(0.1, 1.0, (cfg.batch, cap))
+    low = [7, 33]                                   # per sequence: the unique minimum
+    for b, j in enumerate(low):
+        u[b, j] = 0.01
+    st["u"] = torch.tensor(u, dtype=torch.float32)
+    pos = np.tile(np.arange(cap, dtype=np.int64) * 10, (cfg.batch, 1))
+    pos[0, low[0]] = 10_000                          # higher than the newcomer's position below
+    pos[1, low[1]] = 10_000
+    st["pos"] = torch.tensor(pos, dtype=torch.int32)
+    oc = oracle_cache(st, cfg.dtype)
+    dev = to_device(st)
+    shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
+    params = B.make_params(cfg.alpha, cfg.budget, 4, False, init, cfg.recency_bias, cfg.recency_window)
+    ws = B.workspace(shape, cap)
+    si = w.step_inputs(2)
+    new_pos = 5_000
+    keep = torch.zeros(cfg.batch, cap, dtype=torch.uint8, device="cuda")
+    sig = to_device(si)
+    n_out = B.kv_evict_step(shape, params, 2, st["n"], new_pos, sig["q"], sig["k_new"], sig["v_new"], dev["k"],
+                            dev["v"], dev["u"], dev["pos"], ws, keep_out=keep)
+    torch.cuda.synchronize()
+    ref = evict_step(oc, raw_numpy(si["q"]), raw_numpy(si["k_new"]), raw_numpy(si["v_new"]), 2, new_pos,
+                     oracle_params(cfg, refresh_period=4, nonrefresh_init=init))
+    assert n_out == ref.n_out == cfg.budget
+    np.testing.assert_array_equal(keep.cpu().numpy()[:, : cfg.budget + 1].astype(bool), ref.keep)
+    if init == "min":
+        assert not ref.keep[0, low[0]] and not ref.keep[1, low[1]] and ref.keep[:, -1].all()
+    assert_close(dev["u"][:, :n_out].cpu().numpy(), oc.u[:, :n_out], f"{init} utilities")
+    np.testing.assert_array_equal(dev["pos"][:, :n_out].cpu().numpy(), oc.pos[:, :n_out])
+    np.testing.assert_array_equal(raw_numpy(dev["k"])[:, :, :, :n_out], oc.k[:, :, :, :n_out])
+    np.testing.assert_array_equal(raw_numpy(dev["v"])[:, :, :, :n_out], oc.v[:, :, :, :n_out])
