@@ -107,6 +107,141 @@ def cpu_baseline(cfg, seqs: int, steps: int):
             "seconds_measured": dt}
 
 
+def step1_bytes(cfg, n, holes):
+    """Algorithmic HBM bytes of decode step 1 on n tokens with `holes` rows moved per sequence: K read once,
+    queries and positions, the split scorer's logits (written and read back) and group sums (written and
+    read by the fold), the fold's utilities, the selection's reads, and the compaction's moves (K and V rows
+    of every layer and KV head read and written, with their utility and position)."""
+    e = 2 if cfg.dtype == "bf16" else 4
+    L, b, hq, hkv, d = cfg.layers, cfg.batch, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
+    score = L * b * hkv * n * d * e + L * b * hq * d * e + b * n * 4
+    logits = 2 * L * b * hq * n * 4
+    sums = 2 * L * b * hkv * n * 4
+    fold = 2 * b * n * 4
+    select = 2 * b * n * 4
+    moves = sum(holes) * (2 * 2 * L * hkv * d * e + 4 * 4)
+    append = 2 * 2 * L * b * hkv * d * e
+    return score + logits + sums + fold + select + moves + append
+
+
+def secondary_workloads(B, dev, K, W):
+    """The other configurations of the measurement plan, one after another on the freed device:
+    Score-Free at 131,072 tokens (step-1 rate, then non-refresh steps), the Qwen-shaped workload (steady
+    full-refresh steps) and the Tiny workload (launch-bound steps)."""
+    import torch
+
+    from workload import QWEN, SCOREFREE128K, TINY, Workload
+
+    out = {}
+
+    def setup(cfg):
+        w = Workload(cfg, device=dev)
+        st = w.prefill()
+        shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.capacity,
+                             cfg.dtype)
+        params = B.make_params(cfg.alpha, cfg.budget, cfg.refresh_period, cfg.score_free, cfg.nonrefresh_init,
+                               cfg.recency_bias, cfg.recency_window)
+        return w, st, shape, params, B.workspace(shape, cfg.capacity, device=dev)
+
+    def run(w, st, shape, params, ws, t, keep=None, trace=None):
+        si = w_inputs[t]
+        st["n"] = B.kv_evict_step(shape, params, t, st["n"], si["new_pos"], si["q"], si["k_new"], si["v_new"],
+                                  st["k"], st["v"], st["u"], st["pos"], ws, keep_out=keep, trace=trace)
+
+    def timed_first_step(cfg, w, st, shape, params, ws):
+        keep = torch.zeros(cfg.batch, cfg.capacity, dtype=torch.uint8, device=dev)
+        n = st["n"] + 1
+        torch.cuda.synchronize()
+        a, z = B.HipEvent(), B.HipEvent()
+        a.record()
+        run(w, st, shape, params, ws, 1, keep=keep)
+        z.record()
+        ms = a.elapsed_ms(z)
+        holes = (keep[:, : cfg.budget] == 0).sum(dim=1).tolist()
+        by = step1_bytes(cfg, n, holes)
+        return {"ms": round(ms, 3), "n_scored": n, "algorithmic_bytes": by, "GBps": round(by / (ms * 1e-3) / 1e9, 1),
+                "pct_peak": round(100 * by / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 1), "rows_moved_per_seq": holes}
+
+    # Score-Free, 131,072-token prefill, B = 13,107, min prior
+    cfg = SCOREFREE128K
+    w, st, shape, params, ws = setup(cfg)
+    nsteps = min(cfg.steps - 1, K)
+    w_inputs = {t: w.step_inputs(t) for t in range(1, 2 + 2 * nsteps)}
+    first = timed_first_step(cfg, w, st, shape, params, ws)
+    torch.cuda.synchronize()
+    h0 = time.perf_counter()
+    for t in range(2, 2 + nsteps):
+        run(w, st, shape, params, ws, t)
+    torch.cuda.synchronize()
+    host_ms = 1e3 * (time.perf_counter() - h0) / nsteps
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for t in range(2 + nsteps, 2 + 2 * nsteps):
+            run(w, st, shape, params, ws, t)
+    torch.cuda.synchronize()
+    a, z = B.HipEvent(), B.HipEvent()
+    a.record()
+    g.replay()
+    z.record()
+    graph_ms = a.elapsed_ms(z) / nsteps
+    out["scorefree_128k"] = {"config": {"batch": cfg.batch, "layers": cfg.layers, "context": cfg.prefill_len,
+                                        "budget": cfg.budget, "nonrefresh_init": cfg.nonrefresh_init},
+                             "step1": first, "nonrefresh_steps": nsteps,
+                             "nonrefresh_ms_per_step": round(host_ms, 4),
+                             "nonrefresh_steps_per_s": round(1e3 / host_ms, 1),
+                             "nonrefresh_graph_ms_per_step": round(graph_ms, 4),
+                             "nonrefresh_graph_steps_per_s": round(1e3 / graph_ms, 1)}
+    del w, st, ws, g, w_inputs
+    torch.cuda.empty_cache()
+
+    # Qwen-shaped: batch 32, 28 layers, 28 / 4 heads (G = 7), 8k prefill, B = 2,048, full refresh
+    cfg = QWEN
+    w, st, shape, params, ws = setup(cfg)
+    kq = min(K, 100)
+    w_inputs = {t: w.step_inputs(t) for t in range(1, 2 + W + kq)}
+    first = timed_first_step(cfg, w, st, shape, params, ws)
+    for t in range(2, 2 + W):
+        run(w, st, shape, params, ws, t)
+    pairs = [(B.HipEvent(), B.HipEvent()) for _ in range(kq)]
+    torch.cuda.synchronize()
+    h0 = time.perf_counter()
+    for i, t in enumerate(range(2 + W, 2 + W + kq)):
+        run(w, st, shape, params, ws, t, trace=B.make_trace({"score": pairs[i]}))
+    torch.cuda.synchronize()
+    host_s = time.perf_counter() - h0
+    score_ms = sum(p[0].elapsed_ms(p[1]) for p in pairs) / kq
+    by = step_bytes(cfg, cfg.budget + 1)
+    out["qwen_8k"] = {"config": {"batch": cfg.batch, "layers": cfg.layers, "n_q_heads": cfg.n_q_heads,
+                                 "n_kv_heads": cfg.n_kv_heads, "context": cfg.prefill_len, "budget": cfg.budget},
+                      "step1": first, "steady_steps_per_s": round(kq / host_s, 1),
+                      "steady_ms_per_step": round(1e3 * host_s / kq, 4),
+                      "steady_GBps": round(by["total"] * kq / host_s / 1e9, 1),
+                      "score_kernel_ms": round(score_ms, 4),
+                      "score_kernel_GBps": round(by["score"] / (score_ms * 1e-3) / 1e9, 1),
+                      "score_kernel_pct_peak": round(100 * by["score"] / (score_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 1)}
+    del w, st, ws, w_inputs
+    torch.cuda.empty_cache()
+
+    # Tiny (parity-sized, launch-bound): 16 full-refresh steps
+    cfg = TINY
+    w, st, shape, params, ws = setup(cfg)
+    st = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in st.items()}
+    w_inputs = {t: {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in w.step_inputs(t).items()}
+                for t in range(1, cfg.steps + 1)}
+    run(w, st, shape, params, ws, 1)
+    torch.cuda.synchronize()
+    h0 = time.perf_counter()
+    for t in range(2, cfg.steps + 1):
+        run(w, st, shape, params, ws, t)
+    torch.cuda.synchronize()
+    tiny_ms = 1e3 * (time.perf_counter() - h0) / (cfg.steps - 1)
+    out["tiny"] = {"steps_per_s": round(1e3 / tiny_ms, 1), "ms_per_step": round(tiny_ms, 4),
+                   "note": "launch-bound: a few kernels of a few microseconds each per step"}
+    del w, st, ws, w_inputs
+    torch.cuda.empty_cache()
+    return out
+
+
 def extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, full_ms):
     """Further rows of the path on the same trajectory, KF steps each (host wall clock around the launches):
     the decode step around the model's own attention (attention fused with the score vs attention followed by
@@ -207,6 +342,7 @@ def main():
     ap.add_argument("--cpu-seqs", type=int, default=8, help="sequences of the batch the CPU oracle times")
     ap.add_argument("--cpu-steps", type=int, default=12, help="consecutive steps the CPU oracle times")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true", help="skip the Score-Free 128k / Qwen / Tiny sections")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
                     help="run a plain device copy of this size first (counter calibration)")
     args = ap.parse_args()
@@ -325,6 +461,9 @@ def main():
     lz8_graph_ms = graphed(lazy8)
 
     extra = extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, ms_per_step)
+    del st, k, v, u, pos, ws, inputs
+    torch.cuda.empty_cache()
+    other = secondary_workloads(B, dev, K, W) if not args.no_secondary else {}
 
     n = cfg.budget + 1
     by = step_bytes(cfg, n)
@@ -374,6 +513,8 @@ def main():
         "setup_s": round(setup_s, 1),
     }
     out.update(extra)
+    if other:
+        out["other_workloads"] = other
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seqs, args.cpu_steps)
     print(json.dumps(out), flush=True)
