@@ -52,7 +52,7 @@ Layout layout_for(const kv_shape& s, int n) {
     const size_t heads = (size_t)s.layers * s.batch * s.n_q_heads;
     const size_t logits = heads * L.n_stride * sizeof(float);
     const size_t z_bytes = (L.plan.split || ab.may_split) ? logits : 0;
-    const size_t part_score = L.plan.split ? heads * L.plan.nchunk * sizeof(float2) : 0;
+    // chunk partials of long slabs (scorer) and of the attention: the attention's bound covers both
     const size_t part_attn = (size_t)ab.chunk_layers * s.batch * s.n_q_heads * sizeof(float2);
     size_t off = 0;
     L.r_off = off;
@@ -60,7 +60,7 @@ Layout layout_for(const kv_shape& s, int n) {
     L.z_off = off;
     off = align256(off + z_bytes);
     L.part_off = off;
-    off = align256(off + (part_score > part_attn ? part_score : part_attn));
+    off = align256(off + part_attn);
     L.opart_off = off;
     off = align256(off + (size_t)ab.chunk_layers * s.batch * s.n_q_heads * s.head_dim * sizeof(float));
     L.vn_off = off;
@@ -143,13 +143,24 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
                     int cur_pos, float recency_bias, int recency_window, void* ws, hipStream_t st,
                     const kv_trace* tr) {
     ScoreArgs a = score_args(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws);
-    a.chunk_rows = L.plan.chunk_rows;
-    a.nchunk = L.plan.nchunk;
     ScorePlan plan = L.plan;
-    plan.grid = s.layers * s.batch * s.n_kv_heads * plan.nchunk;
-    kv_status rc = hip_status(launch_score(s.dtype, s.head_dim, plan, a, st));
-    if (rc == KV_OK && plan.split) rc = hip_status(launch_split_finish(a, st));
-    return rc;
+    if (plan.split) {
+        // long slabs: LDS-resident chunks of the attention kernel's K pass, then the finish kernel
+        const int group = s.n_q_heads / s.n_kv_heads;
+        if (!attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &plan) || !plan.split)
+            return KV_ERR_UNSUPPORTED;  // (a slab too long for one workgroup's LDS always splits)
+        a.v = k;  // not read: the kernel's V stream is compiled out
+        a.chunk_rows = plan.chunk_rows;
+        a.nchunk = plan.nchunk;
+        a.emit = 1;
+        kv_status rc = hip_status(launch_score_chunks(s.dtype, s.head_dim, plan, a, st));
+        if (rc == KV_OK) rc = hip_status(launch_split_finish(a, st));
+        return rc;
+    }
+    a.chunk_rows = plan.chunk_rows;
+    a.nchunk = plan.nchunk;
+    plan.grid = s.layers * s.batch * s.n_kv_heads;
+    return hip_status(launch_score(s.dtype, s.head_dim, plan, a, st));
 }
 
 // Scorer perturbations (Sec. 5.1) of a refresh step: value-row norms and entropy factors for the fold.

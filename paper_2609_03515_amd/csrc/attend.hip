@@ -100,7 +100,9 @@ __global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
     }
 }
 
-template <typename T, int D, int GP>
+// kV = false: score only (no V pass, no output), for scoring long slabs in chunks: the chunks write their
+// logits and per-head (max, sum) for the scorer's finish kernel.
+template <typename T, int D, int GP, bool kV>
 __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     using L = Lane<T, D, GP>;
     using E = Elem<T>;
@@ -112,7 +114,7 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
 
     extern __shared__ float zs[];
     __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
-    __shared__ float obuf[GP * D];
+    __shared__ float obuf[kV ? GP * D : 1];
     __shared__ int next_unit[2];
 
     const L ln;
@@ -174,10 +176,12 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     // wait for LDS only, not for these loads)
     chunk_t vbuf[kNbuf][RPG][CPL];
     int vunit[kNbuf];
+    if constexpr (kV) {
 #pragma unroll
-    for (int j = 0; j < kNbuf - 1; ++j) {
-        vunit[j] = claim(1);
-        ln.load_rows(vrs, vunit[j], vbuf[j]);
+        for (int j = 0; j < kNbuf - 1; ++j) {
+            vunit[j] = claim(1);
+            ln.load_rows(vrs, vunit[j], vbuf[j]);
+        }
     }
 
     // 2. per-head max, exponentials in place, per-head sums; several chunks: the logits go to HBM for the
@@ -223,6 +227,19 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
     if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;
     __syncthreads();  // also publishes every exponential to the V pass
+    if constexpr (!kV) {
+        if (threadIdx.x < a.group) {
+            const size_t h = (size_t)lb * a.hq + (size_t)g * a.group + threadIdx.x;
+            float mx = red_m[0][threadIdx.x], tot = red_s[0][threadIdx.x];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) {
+                mx = fmaxf(mx, red_m[w][threadIdx.x]);
+                tot += red_s[w][threadIdx.x];
+            }
+            a.part[h * a.nchunk + chunk] = make_float2(mx, tot);
+        }
+        return;
+    } else {
 
     // 3. V pass: acc[h][c][x] = sum over this lane's rows of e_h(row) * v(row)[(p + c LPR) EPC + x]
     float acc[GP][CPL][EPC];
@@ -335,6 +352,7 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
             store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]));
         }
     }
+    }  // kV
 }
 
 template <typename T, int D, int GP>
@@ -342,7 +360,7 @@ hipError_t launch_attend_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream
     if constexpr (Geometry<T, D, 1>::kLpr < GP) {
         return hipErrorInvalidValue;
     } else {
-        auto kern = attend_kernel<T, D, GP>;
+        auto kern = attend_kernel<T, D, GP, true>;
         if (plan.lds_bytes > 64 * 1024) {
             static bool raised = false;  // idempotent attribute; a benign race between threads
             if (!raised) {
@@ -360,6 +378,38 @@ hipError_t launch_attend_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream
                                s, a);
         }
         return hipGetLastError();
+    }
+}
+
+template <typename T, int D, int GP>
+hipError_t launch_chunks_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
+    if constexpr (Geometry<T, D, 1>::kLpr < GP) {
+        return hipErrorInvalidValue;
+    } else {
+        auto kern = attend_kernel<T, D, GP, false>;
+        if (plan.lds_bytes > 64 * 1024) {
+            static bool raised = false;  // idempotent attribute; a benign race between threads
+            if (!raised) {
+                hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax);
+                if (e != hipSuccess) return e;
+                raised = true;
+            }
+        }
+        hipLaunchKernelGGL(kern, dim3(plan.grid), dim3(kThreads), plan.lds_bytes, s, a);
+        return hipGetLastError();
+    }
+}
+
+template <typename T, int D>
+hipError_t launch_chunks_d(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
+    switch (plan.group_pad) {
+        case 1: return launch_chunks_gp<T, D, 1>(plan, a, s);
+        case 2: return launch_chunks_gp<T, D, 2>(plan, a, s);
+        case 4: return launch_chunks_gp<T, D, 4>(plan, a, s);
+        case 8: return launch_chunks_gp<T, D, 8>(plan, a, s);
+        case 16: return launch_chunks_gp<T, D, 16>(plan, a, s);
+        default: return hipErrorInvalidValue;
     }
 }
 
@@ -411,6 +461,17 @@ AttendBound attend_bound(int dtype, int head_dim, int group, int n, int slabs_pe
     r.chunk_layers = by_target < by_size ? by_target : by_size;
     r.may_split = c0 > 1 || (by_rows > 1 && want1 > 1);
     return r;
+}
+
+hipError_t launch_score_chunks(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
+    if (dtype == 0) {
+        if (head_dim == 64) return launch_chunks_d<float, 64>(plan, a, s);
+        if (head_dim == 128) return launch_chunks_d<float, 128>(plan, a, s);
+    } else {
+        if (head_dim == 64) return launch_chunks_d<bf16_t, 64>(plan, a, s);
+        if (head_dim == 128) return launch_chunks_d<bf16_t, 128>(plan, a, s);
+    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_attend(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {

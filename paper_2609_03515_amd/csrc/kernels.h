@@ -10,9 +10,10 @@ namespace ikv {
 constexpr int kMaxLayers = 256;
 constexpr int kMaxGroup = 16;
 
-// Scoring of one step (Eq. 1).  Fast path: one workgroup streams a whole (layer, sequence, KV head) slab
-// and keeps its logits in LDS, writing the group probability sums r.  Split path: several workgroups per
-// slab write logits z and per-head partial (max, sum) pairs; a finish kernel turns them into r.
+// Scoring of one step (Eq. 1).  One workgroup streams a whole (layer, sequence, KV head) slab and keeps its
+// logits in LDS, writing the group probability sums r.  Slabs too long for that are cut into chunks
+// (launch_score_chunks): the chunks write logits z and per-head partial (max, sum) pairs, and a finish kernel
+// turns them into r.
 struct ScoreArgs {
     const void* q;
     const void* k;
@@ -33,7 +34,7 @@ struct ScoreArgs {
 };
 
 struct ScorePlan {
-    bool split;
+    bool split;        // the slab is cut into chunks (planned by attend_plan)
     int group_pad;     // group size rounded up to a power of two
     int waves;         // waves per workgroup
     int rows_per_iter; // rows one workgroup covers per loop iteration
@@ -60,6 +61,9 @@ struct AttendBound {
 };
 AttendBound attend_bound(int dtype, int head_dim, int group, int n, int slabs_per_layer, int layers);
 hipError_t launch_attend(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s);
+// Scoring of long slabs in LDS-resident chunks (the attention kernel without its V pass): logits and per-chunk
+// (max, sum) for launch_split_finish; plan from attend_plan.
+hipError_t launch_score_chunks(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s);
 
 // Layer fold (Eq. 2-4): u <- prior_w * u + sum_l w_l s_l with s_l = (1/H) sum_g r_{l,g}.
 struct FoldArgs {

@@ -10,10 +10,10 @@
 // a power of two), producing RPG * GP = LPR partial dot products; a DPP reduce-scatter over the group leaves
 // each lane with one complete (row, head) logit.
 //
-// LDS path (a whole slab's logits fit in LDS): one workgroup per slab keeps its logits in LDS; after the
-// per-head (max, sum) reduction it writes r(row) = sum over the group's heads of exp(z - max) / sum.  Split
-// path (long first steps): several workgroups per slab write their logits and per-head partial (max, sum);
-// a finish kernel combines them.
+// One workgroup per slab keeps the slab's logits in LDS; after the per-head (max, sum) reduction it writes
+// r(row) = sum over the group's heads of exp(z - max) / sum.  Slabs too long for one workgroup's LDS (long
+// first steps) are scored in chunks by the attention kernel's K pass (attend.hip), which writes logits and
+// per-chunk (max, sum); the finish kernel below combines them.
 #include "stream_lane.h"
 
 namespace ikv {
@@ -150,72 +150,6 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWavesLds))) void scor
     }
 }
 
-template <typename T, int D, int GP>
-__global__ __launch_bounds__(kThreads)
-__attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWavesSplit))) void score_split_kernel(ScoreArgs a) {
-    using L = Lane<T, D, GP>;
-    using chunk_t = typename L::chunk_t;
-    constexpr int RPG = L::RPG, CPL = L::CPL, RPI = L::RPI;
-    constexpr int kNbuf = Geometry<T, D, GP>::kNbufSplit;
-    __shared__ MaxSum red[kWaves][GP];
-
-    const L ln;
-    int bid = blockIdx.x;
-    const int chunk = bid % a.nchunk;
-    bid /= a.nchunk;
-    const int g = bid % a.hkv;
-    bid /= a.hkv;
-    const int b = bid % a.batch;
-    const int l = bid / a.batch;
-    const size_t slab = ((size_t)l * a.batch + b) * a.hkv + g;
-    const int row0 = chunk * a.chunk_rows;
-    const int row_end = min(a.n, row0 + a.chunk_rows);
-    const int nit = row_end > row0 ? (row_end - row0 + RPI - 1) / RPI : 0;
-    const T* kslab = static_cast<const T*>(a.k) + slab * a.cap * D;
-    const __amdgpu_buffer_rsrc_t krs = raw_rsrc(kslab, row_end * L::kRowBytes);
-    const __amdgpu_buffer_rsrc_t prs = raw_rsrc(a.pos + (size_t)b * a.cap, row_end * 4);
-
-    chunk_t qv[GP][CPL];
-    chunk_t kbuf[kNbuf][RPG][CPL];
-    int pbuf[kNbuf];
-    ln.load_q(a, (size_t)l * a.batch + b, g, qv);
-#pragma unroll
-    for (int j = 0; j < kNbuf - 1; ++j) ln.load(krs, prs, row0, j, kbuf[j], pbuf[j]);
-
-    // the logits leave the workgroup, so the (max, sum) pair is kept online
-    MaxSum ms{kFloor, 0.0f};
-    const __amdgpu_buffer_rsrc_t zrs = raw_rsrc(
-        a.z + (((size_t)l * a.batch + b) * a.hq + (size_t)g * a.group + ln.hh) * a.n_stride, a.n_stride * 4);
-    for (int it = 0; it < nit; it += kNbuf) {
-#pragma unroll
-        for (int j = 0; j < kNbuf; ++j) {
-            ln.load(krs, prs, row0, it + j + kNbuf - 1, kbuf[(j + kNbuf - 1) % kNbuf],
-                    pbuf[(j + kNbuf - 1) % kNbuf]);
-            if (it + j < nit) {
-                const int row = ln.owned_row(row0, it + j);
-                const float z = ln.logit(a, kbuf[j], qv, pbuf[j], row, row_end);
-                const float m_new = fmaxf(ms.m, z);
-                ms.s = fmaf(ms.s, __expf(ms.m - m_new), __expf(z - m_new));
-                ms.m = m_new;
-                if (z != -INFINITY) store_stream(zrs, row * 4, z);
-            }
-        }
-    }
-#pragma unroll
-    for (int o = GP; o < kWave; o <<= 1) {
-        MaxSum other{__shfl_xor(ms.m, o, kWave), __shfl_xor(ms.s, o, kWave)};
-        ms = ms_combine(ms, other);
-    }
-    if (ln.lane < GP) red[ln.wave][ln.lane] = ms;
-    __syncthreads();
-    MaxSum tot = red[0][ln.hh];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) tot = ms_combine(tot, red[w][ln.hh]);
-    if (threadIdx.x < a.group)
-        a.part[(((size_t)l * a.batch + b) * a.hq + (size_t)g * a.group + threadIdx.x) * a.nchunk + chunk] =
-            make_float2(tot.m, tot.s);
-}
-
 // Combine the split partials per head and emit r(row) = sum_{h in group} exp(z_h - M_h) / S_h.  A workgroup
 // covers kFinishRows rows of one (layer, sequence, KV head): each thread handles 4 consecutive rows per pass
 // with 16-byte loads (logit rows are padded to a multiple of 64).
@@ -277,8 +211,7 @@ hipError_t launch_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
         return hipErrorInvalidValue;
     } else {
         if (!plan.split) return launch_lds<T, D, GP>(plan, a, s);
-        hipLaunchKernelGGL((score_split_kernel<T, D, GP>), dim3(plan.grid), dim3(kThreads), 0, s, a);
-        return hipGetLastError();
+        return hipErrorInvalidValue;  // long slabs are scored in chunks (launch_score_chunks)
     }
 }
 
@@ -316,14 +249,10 @@ bool score_plan(int dtype, int head_dim, int group, int n, ScorePlan* plan) {
         plan->chunk_rows = nit * rpi;
         plan->nchunk = 1;
         plan->lds_bytes = lds;
-    } else {
-        const int target = rpi * kSplitIters;
-        int nchunk = (n + target - 1) / target;
-        int rows = (n + nchunk - 1) / nchunk;
-        rows = (rows + rpi - 1) / rpi * rpi;
+    } else {  // scored in chunks, planned by attend_plan
         plan->split = true;
-        plan->chunk_rows = rows;
-        plan->nchunk = (n + rows - 1) / rows;
+        plan->chunk_rows = 0;
+        plan->nchunk = 0;
         plan->lds_bytes = 0;
     }
     plan->grid = 0;

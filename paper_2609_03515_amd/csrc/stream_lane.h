@@ -27,7 +27,6 @@ namespace {
 constexpr size_t kFastLdsMax = 80 * 1024;  // keep >= 2 workgroups per CU (160 KiB LDS)
 constexpr int kWaves = IKV_SCORE_WAVES;
 constexpr int kThreads = kWaves * kWave;
-constexpr int kSplitIters = 16;
 constexpr float kFloor = -1.0e30f;  // finite start of running maxima: exp(-inf - floor) = 0, no NaN
 constexpr int kNonTemporal = 2;     // buffer-load cache policy: K is streamed once, no reuse to cache for
 constexpr int kRsrcConfig = 0x00020000;  // raw (unformatted, stride 0) buffer resource, gfx9 family
@@ -63,12 +62,9 @@ struct Geometry {
     static constexpr int kRpw = kNg * kRpg;
     static constexpr int kRpi = kWaves * kRpw;
     static_assert(kRpg * GP == kLpr, "group must not exceed the lanes of a row");
-    // K loads of this many loop iterations are in flight per lane.  The LDS path claims its rows dynamically
-    // and measured best with 2 (more buffers cost occupancy without raising the stream rate).  The split path
-    // streams static chunks and measured best with 4 when a lane loads four 16-byte chunks per iteration, 3 for
-    // wider groups (more arithmetic per byte), 2 when a lane loads more than four chunks per iteration.
+    // K loads of this many units are in flight per lane.  Rows are claimed dynamically and 2 measured best
+    // (more buffers cost occupancy without raising the stream rate).
     static constexpr int kNbufLds = IKV_NBUF > 0 ? IKV_NBUF : 2;
-    static constexpr int kNbufSplit = IKV_NBUF > 0 ? IKV_NBUF : (kRpg * kCpl > 4 ? 2 : (GP <= 4 ? 4 : 3));
     // Registers of the streaming loop: the K buffers in flight, the queries, the partial dot products and
     // bookkeeping.  LDS holds about 3 workgroups per CU at the graded shapes, so ask the compiler for the
     // matching waves per SIMD when the loop fits that register budget; otherwise leave it unconstrained
@@ -82,7 +78,6 @@ struct Geometry {
 #endif
     }
     static constexpr int kMinWavesLds = min_waves(kNbufLds);
-    static constexpr int kMinWavesSplit = min_waves(kNbufSplit);
 };
 
 // Per-lane streaming machinery shared by both paths.
