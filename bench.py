@@ -264,18 +264,18 @@ def extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, full_
             B.kv_attend_score(shape, 0, L, n, q, k, v, pos, inputs[state["t"] - 1]["new_pos"], cfg.recency_bias,
                               cfg.recency_window, emit, o, ws)
 
-    def fused_step(per_layer):
+    def fused_step(per_layer, p=full, emit=B.KV_EMIT_SCORES):
         state["t"] += 1
         si = inputs[state["t"] - 1]
         n = state["n"]
-        B.kv_append(shape, full, state["t"], n, si["new_pos"], si["k_new"], si["v_new"], k, v, u, pos)
-        attend(n + 1, si["q"], 1, per_layer)
-        state["n"] = B.kv_evict_finish(shape, full, state["t"], n + 1, k, v, u, pos, ws)
+        B.kv_append(shape, p, state["t"], n, si["new_pos"], si["k_new"], si["v_new"], k, v, u, pos)
+        attend(n + 1, si["q"], emit, per_layer)
+        state["n"] = B.kv_evict_finish(shape, p, state["t"], n + 1, k, v, u, pos, ws)
 
-    def separate_step(per_layer):
+    def separate_step(per_layer, p=full):
         state["t"] += 1
         si = inputs[state["t"] - 1]
-        state["n"] = B.kv_evict_step(shape, full, state["t"], state["n"], si["new_pos"], si["q"], si["k_new"],
+        state["n"] = B.kv_evict_step(shape, p, state["t"], state["n"], si["new_pos"], si["q"], si["k_new"],
                                      si["v_new"], k, v, u, pos, ws)
         attend(state["n"] + 1, si["q"], 0, per_layer)
 
@@ -310,6 +310,12 @@ def extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, full_
             "fused_steps_per_s": round(1e3 / f_ms, 2), "separate_steps_per_s": round(1e3 / s_ms, 2),
             "eviction_overhead_fused_pct": round(100 * (f_ms - a_ms) / a_ms, 1),
             "eviction_overhead_separate_pct": round(100 * (s_ms - a_ms) / a_ms, 1)}
+    # VNorm (f3) around the model's attention: norms emitted by the attention's V pass vs read again from V
+    vn_fused = params(vnorm=True, norms_emitted=True)
+    vn_sep = params(vnorm=True)
+    res["all_layers_one_call"]["fused_vnorm_decode_step_ms"] = round(
+        ms_of(fused_step, False, vn_fused, B.KV_EMIT_SCORES | B.KV_EMIT_VNORMS), 4)
+    res["all_layers_one_call"]["separate_vnorm_decode_step_ms"] = round(ms_of(separate_step, False, vn_sep), 4)
     fused = {"what": "one decode step of attention over every layer (32 per-layer calls, or one call) plus the "
                      "eviction step; fused = attention emits the score (kv_append, kv_attend_score, "
                      "kv_evict_finish), separate = attention without score + kv_evict_step's own scoring pass",
@@ -370,7 +376,7 @@ def main():
     ws = B.workspace(shape, cap, device=dev)
     K, W = args.steps, args.warmup
     KF = min(K, 50)   # steps per configuration of the extra measurements (fused attention, variants, trace)
-    total = 1 + W + 5 * K + 10 * KF
+    total = 1 + W + 5 * K + 12 * KF
     inputs = [w.step_inputs(t) for t in range(1, total + 1)]
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup

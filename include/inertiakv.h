@@ -68,7 +68,14 @@ typedef enum { KV_RULE_EMA = 0, KV_RULE_SINGLE_STEP = 1, KV_RULE_CUMULATIVE = 2 
  *  KV_SCORE_ENTROPY: the layer's pooled score is multiplied by the entropy of the layer's pooled attention
  *                    distribution (before VNorm) divided by ln n, one factor per layer and sequence (1 if
  *                    n = 1).  s_out then holds the perturbed scores that were folded. */
-typedef enum { KV_SCORE_ATTENTION = 0, KV_SCORE_VNORM = 1, KV_SCORE_ENTROPY = 2 } kv_score_variant;
+typedef enum {
+    KV_SCORE_ATTENTION = 0,
+    KV_SCORE_VNORM = 1,
+    KV_SCORE_ENTROPY = 2,
+    /* kv_evict_finish only, with KV_SCORE_VNORM: the step's attention calls emitted the value norms
+     * (KV_EMIT_VNORMS), so V is not read again */
+    KV_SCORE_NORMS_EMITTED = 4
+} kv_score_variant;
 
 typedef struct {
     int32_t batch;      /* sequences                                   >= 1              */
@@ -181,13 +188,17 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
 kv_status kv_append(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in, int32_t new_pos,
                     const void* k_new, const void* v_new, void* k, void* v, float* u, int32_t* pos, void* stream);
 
+/* What kv_attend_score records in the workspace besides the output (bit mask): the layers' pooled scores
+ * (Eq. 1), and the value-row norms that VNorm weights them by (read from V while the attention streams it). */
+typedef enum { KV_EMIT_SCORES = 1, KV_EMIT_VNORMS = 2 } kv_emit;
+
 /* Decode attention of layers [layer0, layer0 + layer_count) over the n cached tokens, for every sequence and
  * query head: a_h = softmax_i(z_h(i)) with z_h(i) = q_h . k_i / sqrt(d) (+ recency_bias if
  * pos[i] >= cur_pos - (recency_window - 1)), o_h = sum_i a_h(i) v_i.  q and o are [layer_count][batch]
  * [n_q_heads][d] in the cache dtype (o rounded to nearest); k, v are the whole caches (layer 0 at the
- * pointer).  emit_scores != 0 additionally records these layers' pooled scores (Eq. 1) in the workspace for
- * kv_evict_finish; layers whose scores are not emitted keep whatever the workspace held.  Layers may be
- * attended in any number of calls (one per layer in a decoder). */
+ * pointer).  emit_scores (kv_emit bits) additionally records these layers' pooled scores (Eq. 1) and/or value
+ * norms in the workspace for kv_evict_finish; layers whose scores are not emitted keep whatever the workspace
+ * held.  Layers may be attended in any number of calls (one per layer in a decoder). */
 kv_status kv_attend_score(const kv_shape* shape, int32_t layer0, int32_t layer_count, int32_t n, const void* q,
                           const void* k, const void* v, const int32_t* pos, int32_t cur_pos, float recency_bias,
                           int32_t recency_window, int32_t emit_scores, void* o, void* ws, size_t ws_bytes,

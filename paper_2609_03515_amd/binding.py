@@ -18,7 +18,8 @@ KV_OK, KV_ERR_INVALID_ARG, KV_ERR_UNSUPPORTED, KV_ERR_WORKSPACE, KV_ERR_HIP = 0,
 KV_F32, KV_BF16 = 0, 1
 KV_INIT_MEAN, KV_INIT_MIN = 0, 1
 KV_RULE_EMA, KV_RULE_SINGLE_STEP, KV_RULE_CUMULATIVE = 0, 1, 2
-KV_SCORE_ATTENTION, KV_SCORE_VNORM, KV_SCORE_ENTROPY = 0, 1, 2
+KV_SCORE_ATTENTION, KV_SCORE_VNORM, KV_SCORE_ENTROPY, KV_SCORE_NORMS_EMITTED = 0, 1, 2, 4
+KV_EMIT_SCORES, KV_EMIT_VNORMS = 1, 2
 KV_PHASES = 5
 PHASES = ("append", "score", "fold", "select", "compact")
 
@@ -122,12 +123,13 @@ def make_shape(batch, layers, n_q_heads, n_kv_heads, head_dim, capacity, dtype) 
 
 
 def make_params(alpha, budget, refresh_period=1, score_free=False, nonrefresh_init="mean", recency_bias=0.0,
-                recency_window=0, rule="ema", vnorm=False, entropy=False) -> KvParams:
+                recency_window=0, rule="ema", vnorm=False, entropy=False, norms_emitted=False) -> KvParams:
     init = {"mean": KV_INIT_MEAN, "min": KV_INIT_MIN}[nonrefresh_init] if isinstance(nonrefresh_init, str) \
         else int(nonrefresh_init)
     rl = {"ema": KV_RULE_EMA, "single": KV_RULE_SINGLE_STEP, "cumulative": KV_RULE_CUMULATIVE}[rule] \
         if isinstance(rule, str) else int(rule)
-    variant = (KV_SCORE_VNORM if vnorm else 0) | (KV_SCORE_ENTROPY if entropy else 0)
+    variant = (KV_SCORE_VNORM if vnorm else 0) | (KV_SCORE_ENTROPY if entropy else 0) | \
+        (KV_SCORE_NORMS_EMITTED if norms_emitted else 0)
     return KvParams(float(alpha), int(budget), int(refresh_period), int(bool(score_free)), init,
                     float(recency_bias), int(recency_window), rl, variant)
 
@@ -199,7 +201,7 @@ def kv_attend_score(shape, layer0, layer_count, n, q, k, v, pos, cur_pos, recenc
                     emit_scores, o, ws, stream=None):
     _check("kv_attend_score", load_library().kv_attend_score(
         ctypes.byref(shape), int(layer0), int(layer_count), int(n), _ptr(q), _ptr(k), _ptr(v), _ptr(pos),
-        int(cur_pos), float(recency_bias), int(recency_window), int(bool(emit_scores)), _ptr(o), _ptr(ws),
+        int(cur_pos), float(recency_bias), int(recency_window), int(emit_scores), _ptr(o), _ptr(ws),
         _ws_bytes(ws), _stream(stream)))
 
 

@@ -14,7 +14,7 @@ struct Layout {
     int n_stride;
     int max_pairs;
     ScorePlan plan;
-    size_t r_off, z_off, part_off, opart_off, vn_off, vinv_off, eta_off, pdst_off, psrc_off, np_off;
+    size_t r_off, z_off, part_off, opart_off, npart_off, vn_off, vinv_off, eta_off, pdst_off, psrc_off, np_off;
     size_t raw_off, rmask_off, emask_off, kmask_off, tdst_off, tsrc_off, tnp_off, total;
 };
 
@@ -63,6 +63,8 @@ Layout layout_for(const kv_shape& s, int n) {
     off = align256(off + part_attn);
     L.opart_off = off;
     off = align256(off + (size_t)ab.chunk_layers * s.batch * s.n_q_heads * s.head_dim * sizeof(float));
+    L.npart_off = off;
+    off = align256(off + (size_t)ab.chunk_layers * s.batch * s.n_kv_heads * sizeof(float));
     L.vn_off = off;
     off = align256(off + (size_t)s.layers * s.batch * s.n_kv_heads * L.n_stride * sizeof(float));
     L.vinv_off = off;
@@ -273,7 +275,7 @@ kv_status check_params(const kv_params* params) {
     if (p.nonrefresh_init != KV_INIT_MEAN && p.nonrefresh_init != KV_INIT_MIN) return KV_ERR_INVALID_ARG;
     if (p.rule < KV_RULE_EMA || p.rule > KV_RULE_CUMULATIVE) return KV_ERR_INVALID_ARG;
     if (p.recency_window < 0 || !isfinite(p.recency_bias)) return KV_ERR_INVALID_ARG;
-    if (p.score_variant & ~(KV_SCORE_VNORM | KV_SCORE_ENTROPY)) return KV_ERR_INVALID_ARG;
+    if (p.score_variant & ~(KV_SCORE_VNORM | KV_SCORE_ENTROPY | KV_SCORE_NORMS_EMITTED)) return KV_ERR_INVALID_ARG;
     return KV_OK;
 }
 
@@ -542,7 +544,13 @@ kv_status kv_attend_score(const kv_shape* shape, int32_t layer0, int32_t layer_c
     a.layers = layer_count;
     a.chunk_rows = plan.chunk_rows;
     a.nchunk = plan.nchunk;
-    a.emit = emit_scores != 0;
+    if (emit_scores & ~(KV_EMIT_SCORES | KV_EMIT_VNORMS)) return KV_ERR_INVALID_ARG;
+    a.emit = (emit_scores & KV_EMIT_SCORES) != 0;
+    const size_t slab0 = (size_t)layer0 * s.batch * s.n_kv_heads;
+    a.vn = at<float>(ws, L.vn_off) + slab0 * L.n_stride;
+    a.vinv = at<float>(ws, L.vinv_off) + slab0;
+    a.npart = at<float>(ws, L.npart_off);
+    a.emit_norms = (emit_scores & KV_EMIT_VNORMS) != 0;
     return hip_status(launch_attend(s.dtype, s.head_dim, plan, a, static_cast<hipStream_t>(stream)));
 }
 
@@ -564,7 +572,11 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
     hipStream_t st = static_cast<hipStream_t>(stream);
     const bool refresh = is_refresh(p, t);
     if (refresh) {
-        if ((rc = run_variants(s, L, n, v, p.score_variant, ws, st)) != KV_OK) return rc;
+        // value norms already written by the step's attention calls: only the entropy factors remain
+        const int computed = (p.score_variant & KV_SCORE_NORMS_EMITTED) ? (p.score_variant & ~KV_SCORE_VNORM)
+                                                                         : p.score_variant;
+        if ((rc = run_variants(s, L, n, v, computed & (KV_SCORE_VNORM | KV_SCORE_ENTROPY), ws, st)) != KV_OK)
+            return rc;
         rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, rank_trace != nullptr, ws, st, nullptr);
         if (rc != KV_OK) return rc;
     }

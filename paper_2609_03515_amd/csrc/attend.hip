@@ -71,6 +71,11 @@ __global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
         cm[threadIdx.x] = mx;
         ci[threadIdx.x] = tot > 0.0f ? 1.0f / tot : 0.0f;
     }
+    if (a.emit_norms && threadIdx.x == kWave) {  // (another wave than the one filling cm / ci)
+        float tot = 0.0f;
+        for (int c = 0; c < a.nchunk; ++c) tot += a.npart[(size_t)s * a.nchunk + c];
+        a.vinv[s] = tot > 0.0f ? (float)a.n / tot : 0.0f;
+    }
     __syncthreads();
     T* ob = static_cast<T*>(a.o) + head0 * D;
     for (int idx = threadIdx.x; idx < a.group * D; idx += kThreads) {
@@ -113,7 +118,7 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     constexpr int kNbuf = IKV_ATTN_NBUF > 0 ? IKV_ATTN_NBUF : (RPG * CPL > 8 ? 1 : 2);
 
     extern __shared__ float zs[];
-    __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
+    __shared__ float red_m[kWaves][GP], red_s[kWaves][GP], red_n[kWaves];
     __shared__ float obuf[kV ? GP * D : 1];
     __shared__ int next_unit[2];
 
@@ -241,7 +246,11 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
         return;
     } else {
 
-    // 3. V pass: acc[h][c][x] = sum over this lane's rows of e_h(row) * v(row)[(p + c LPR) EPC + x]
+    // 3. V pass: acc[h][c][x] = sum over this lane's rows of e_h(row) * v(row)[(p + c LPR) EPC + x]; with
+    //    emit_norms also the rows' value norms (VNorm), written out and summed
+    const __amdgpu_buffer_rsrc_t vns =
+        raw_rsrc(a.vn + (size_t)s * a.n_stride + row0, a.emit_norms ? nrows * 4 : 0);
+    float nsum = 0.0f;
     float acc[GP][CPL][EPC];
 #pragma unroll
     for (int h = 0; h < GP; ++h)
@@ -265,6 +274,7 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
                     for (int k = 0; k < RPG; ++k) {
                         float e[GP];
                         read_probs<GP>(eu + k * GP, e);
+                        float ss = 0.0f;
 #pragma unroll
                         for (int c = 0; c < CPL; ++c) {
                             float f[EPC];
@@ -273,6 +283,17 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
                             for (int h = 0; h < GP; ++h)
 #pragma unroll
                                 for (int x = 0; x < EPC; ++x) acc[h][c][x] = fmaf(e[h], f[x], acc[h][c][x]);
+#pragma unroll
+                            for (int x = 0; x < EPC; ++x) ss = fmaf(f[x], f[x], ss);
+                        }
+                        if (a.emit_norms) {  // VNorm: the row's l2 norm, summed over its lane group
+                            ss = group_allsum<LPR>(ss);
+                            const int row = ubuf[j] * RPW + k * L::NG + ln.grp;
+                            if (ln.p == 0 && row < nrows) {
+                                const float nrm = sqrtf(ss);
+                                store_stream(vns, row * 4, nrm);
+                                nsum += nrm;
+                            }
                         }
                     }
                 } else {
@@ -280,6 +301,12 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
                 }
             }
         }
+    }
+
+    if (a.emit_norms) {
+#pragma unroll
+        for (int o = kWave / 2; o >= 1; o >>= 1) nsum += __shfl_xor(nsum, o, kWave);
+        if (ln.lane == 0) red_n[ln.wave] = nsum;  // read after the barriers below
     }
 
     // 4. lanes holding the same chunk of different rows (stride LPR), then the waves in order
@@ -318,6 +345,14 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
         return t;
     };
     const size_t head0 = (size_t)lb * a.hq + (size_t)g * a.group;
+    if (a.emit_norms && threadIdx.x == 0) {
+        float tot = 0.0f;
+        for (int w = 0; w < kWaves; ++w) tot += red_n[w];
+        if (a.nchunk == 1)
+            a.vinv[s] = tot > 0.0f ? (float)a.n / tot : 0.0f;
+        else
+            a.npart[(size_t)s * a.nchunk + chunk] = tot;
+    }
     if (a.nchunk == 1) {
         T* ob = static_cast<T*>(a.o) + head0 * D;
         for (int idx = threadIdx.x; idx < a.group * D; idx += kThreads) {

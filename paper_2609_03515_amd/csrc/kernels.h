@@ -31,6 +31,12 @@ struct ScoreArgs {
     void* o;        // [layers][batch][n_q][d] attention output (dtype of q)
     float* opart;   // split: [layers][batch][n_q][nchunk][d] unnormalised partial outputs
     int emit;       // nonzero: also produce the eviction score (r)
+    // fused attention, VNorm (Sec. 5.1) norms from the V pass: value-row l2 norms [layers][batch][n_kv]
+    // [n_stride], the slab's 1 / mean norm, and per-chunk norm sums when chunked (emit_norms nonzero)
+    float* vn;
+    float* vinv;
+    float* npart;   // [layers][batch][n_kv][nchunk]
+    int emit_norms;
 };
 
 struct ScorePlan {

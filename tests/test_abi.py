@@ -143,7 +143,7 @@ def test_step_validation(lib):
     assert _step(s, bad_rule)[0] == B.KV_ERR_INVALID_ARG
     bad_variant = B.make_params(0.9, 20, vnorm=True, entropy=True)
     assert bad_variant.score_variant == B.KV_SCORE_VNORM | B.KV_SCORE_ENTROPY
-    bad_variant.score_variant = 4
+    bad_variant.score_variant = 8
     assert _step(s, bad_variant)[0] == B.KV_ERR_INVALID_ARG
     assert _step(s, good, v_new=None)[0] == B.KV_ERR_INVALID_ARG
     assert _step(s, good, k=FAKE + 2)[0] == B.KV_ERR_UNSUPPORTED
@@ -174,9 +174,10 @@ def test_attend_validation(lib):
     L = lib_()
     need = B.kv_workspace_bytes(s, 10)
 
-    def call(layer0=0, count=3, n=10, q=FAKE, o=FAKE, window=0, ws=FAKE, ws_bytes=need):
-        return L.kv_attend_score(ctypes.byref(s), layer0, count, n, q, FAKE, FAKE, FAKE, 9, 0.5, window, 1, o,
+    def call(layer0=0, count=3, n=10, q=FAKE, o=FAKE, window=0, ws=FAKE, ws_bytes=need, emit=1):
+        return L.kv_attend_score(ctypes.byref(s), layer0, count, n, q, FAKE, FAKE, FAKE, 9, 0.5, window, emit, o,
                                  ws, ws_bytes, None)
+    assert call(emit=4) == B.KV_ERR_INVALID_ARG                  # unknown emit bit
     assert call(layer0=-1) == B.KV_ERR_INVALID_ARG
     assert call(count=0) == B.KV_ERR_INVALID_ARG
     assert call(layer0=2, count=2) == B.KV_ERR_INVALID_ARG        # past the last layer

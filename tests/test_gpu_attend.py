@@ -32,7 +32,7 @@ def attend_layers(shape, cfg, n, q, k, v, pos, cur_pos, emit, ws, per_layer):
     return o
 
 
-def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False):
+def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False, emit_norms=False):
     w = Workload(cfg)
     cap = max(cfg.prefill_len, cfg.budget) + 1
     st = w.prefill(capacity=cap)
@@ -40,7 +40,8 @@ def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False):
     dev = to_device(st)
     shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
     params = B.make_params(cfg.alpha, cfg.budget, cfg.refresh_period, cfg.score_free, cfg.nonrefresh_init,
-                           cfg.recency_bias, cfg.recency_window, vnorm=vnorm, entropy=entropy)
+                           cfg.recency_bias, cfg.recency_window, vnorm=vnorm, entropy=entropy,
+                           norms_emitted=emit_norms)
     op = oracle_params(cfg, vnorm=vnorm, entropy=entropy)
     ws = B.workspace(shape, cap)
     n = st["n"]
@@ -52,7 +53,8 @@ def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False):
         print(f"{cfg.name} t={t} refresh={refresh} per_layer={per_layer} n_in={n}", flush=True)
         B.kv_append(shape, params, t, n, si["new_pos"], sig["k_new"], sig["v_new"], dev["k"], dev["v"], dev["u"],
                     dev["pos"])
-        o = attend_layers(shape, cfg, n + 1, sig["q"], dev["k"], dev["v"], dev["pos"], si["new_pos"], refresh, ws,
+        emit = (B.KV_EMIT_SCORES | (B.KV_EMIT_VNORMS if emit_norms else 0)) if refresh else 0
+        o = attend_layers(shape, cfg, n + 1, sig["q"], dev["k"], dev["v"], dev["pos"], si["new_pos"], emit, ws,
                           per_layer)
         keep = torch.zeros(cfg.batch, cap, dtype=torch.uint8, device="cuda")
         s_out = torch.full((cfg.layers, cfg.batch, n + 1), -1.0, device="cuda")
@@ -94,12 +96,16 @@ def test_fused_step_lockstep(name, per_layer):
     print(f"{name}: in-band flips {flips}")
 
 
-@pytest.mark.parametrize("name", ["tiny", "llama8b_reduced", "llama8b_split_step1"])
-def test_fused_step_scorer_variants(name):
+@pytest.mark.parametrize("emit_norms", [False, True], ids=["norms_from_v", "norms_emitted"])
+@pytest.mark.parametrize("name", ["tiny", "llama8b_reduced", "llama8b_split_step1", "qwen_reduced"])
+def test_fused_step_scorer_variants(name, emit_norms):
     """VNorm + entropy weighting on the fused path: the perturbations are applied by kv_evict_finish to the
-    scores the attention emitted."""
+    scores the attention emitted, with the value norms either read from V by the finish or emitted by the
+    attention's V pass (one and several chunks per slab)."""
     cfg, steps = CASES[name]
-    run_fused_lockstep(cfg, steps, per_layer=True, vnorm=True, entropy=True)
+    run_fused_lockstep(cfg, steps, per_layer=True, vnorm=True, entropy=True, emit_norms=emit_norms)
+    if emit_norms:
+        run_fused_lockstep(cfg, 2, per_layer=False, vnorm=True, entropy=False, emit_norms=True)
 
 
 # ---- one call on random inputs over the supported geometries -------------------------------------------
