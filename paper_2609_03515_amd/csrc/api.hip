@@ -52,15 +52,22 @@ Layout layout_for(const kv_shape& s, int n) {
     const size_t heads = (size_t)s.layers * s.batch * s.n_q_heads;
     const size_t logits = heads * L.n_stride * sizeof(float);
     const size_t z_bytes = (L.plan.split || ab.may_split) ? logits : 0;
-    // chunk partials of long slabs (scorer) and of the attention: the attention's bound covers both
-    const size_t part_attn = (size_t)ab.chunk_layers * s.batch * s.n_q_heads * sizeof(float2);
+    // chunk partials of long slabs (scorer) and of the attention
+    size_t part_bytes = (size_t)ab.chunk_layers * s.batch * s.n_q_heads * sizeof(float2);
+    if (L.plan.split) {
+        ScorePlan cp;
+        if (attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &cp, kScoreChunkLds)) {
+            const size_t sp = heads * cp.nchunk * sizeof(float2);
+            if (sp > part_bytes) part_bytes = sp;
+        }
+    }
     size_t off = 0;
     L.r_off = off;
     off = align256(off + (size_t)s.layers * s.batch * s.n_kv_heads * L.n_stride * sizeof(float));
     L.z_off = off;
     off = align256(off + z_bytes);
     L.part_off = off;
-    off = align256(off + part_attn);
+    off = align256(off + part_bytes);
     L.opart_off = off;
     off = align256(off + (size_t)ab.chunk_layers * s.batch * s.n_q_heads * s.head_dim * sizeof(float));
     L.npart_off = off;
@@ -149,7 +156,8 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
     if (plan.split) {
         // long slabs: LDS-resident chunks of the attention kernel's K pass, then the finish kernel
         const int group = s.n_q_heads / s.n_kv_heads;
-        if (!attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &plan) || !plan.split)
+        if (!attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &plan, kScoreChunkLds) ||
+            !plan.split)
             return KV_ERR_UNSUPPORTED;  // (a slab too long for one workgroup's LDS always splits)
         a.v = k;  // not read: the kernel's V stream is compiled out
         a.chunk_rows = plan.chunk_rows;

@@ -462,10 +462,11 @@ hipError_t launch_attend_d(const ScorePlan& plan, const ScoreArgs& a, hipStream_
 
 }  // namespace
 
-bool attend_plan(int dtype, int head_dim, int group, int n, int slabs, ScorePlan* plan) {
+bool attend_plan(int dtype, int head_dim, int group, int n, int slabs, ScorePlan* plan, size_t max_lds) {
     if (slabs < 1 || !score_plan(dtype, head_dim, group, 1, plan)) return false;
     const int rpw = kWave / plan->group_pad;  // rows per unit
-    const int lds_rows = (int)(kFastLdsMax / (kWave * sizeof(float))) * rpw;
+    if (max_lds == 0 || max_lds > kFastLdsMax) max_lds = kFastLdsMax;
+    const int lds_rows = (int)(max_lds / (kWave * sizeof(float))) * rpw;
     const int want = (kAttnTargetWgs + slabs - 1) / slabs;
     const int by_rows = (n + kAttnMinRows - 1) / kAttnMinRows;
     int nchunk = (n + lds_rows - 1) / lds_rows;

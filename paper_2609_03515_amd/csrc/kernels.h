@@ -58,7 +58,14 @@ hipError_t launch_split_finish(const ScoreArgs& a, hipStream_t s);
 // same r as the scorer.  The plan cuts each slab into nchunk row ranges so that `slabs` slabs fill the chip;
 // with nchunk > 1 the chunks write partial outputs / logits and a combine kernel (one workgroup per slab)
 // produces the outputs and scores.
-bool attend_plan(int dtype, int head_dim, int group, int n, int slabs, ScorePlan* plan);
+// max_lds caps the logits one chunk keeps in LDS (0: the largest a workgroup may use).
+bool attend_plan(int dtype, int head_dim, int group, int n, int slabs, ScorePlan* plan, size_t max_lds = 0);
+// LDS cap of the scorer's chunks: 52 KiB, three workgroups per CU (measured on the 32k and 128k first steps
+// against 20, 40 and 80 KiB; the attention's chunks are planned for one workgroup per CU instead)
+#ifndef IKV_SCORE_CHUNK_LDS
+#define IKV_SCORE_CHUNK_LDS (52 * 1024)
+#endif
+constexpr size_t kScoreChunkLds = IKV_SCORE_CHUNK_LDS;
 // Workspace bound over every call of 1..layers layers on n rows: the largest (layers of the call) x nchunk,
 // and whether any such call splits.
 struct AttendBound {
