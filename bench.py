@@ -27,19 +27,20 @@ PEAK_HBM_GBPS = 8000.0
 METRIC = "evict-steps/sec + achieved HBM GB/s (% peak), 8B shape, 32k ctx, 10% budget"
 
 
-def step_bytes(cfg, n):
+def step_bytes(cfg, n, merge=1):
     """Algorithmic HBM bytes of one refresh step scoring n tokens (n = B + 1 in the steady state).
 
     score : K rows read once (layers*batch*kv*n*d*2), queries, positions, group-sum scratch r written (4 B per
-            token per (layer, sequence, KV head));
+            token per (layer, sequence, block of `merge` KV heads whose sums the scorer adds in one workgroup));
     fold  : r read, u read + written;
     append: new K/V rows read + written; select: u and pos read; compact: at most one K and one V row per
             (layer, sequence, KV head) read + written, u/pos entries.
     """
     e = 2 if cfg.dtype == "bf16" else 4
     L, b, hq, hkv, d = cfg.layers, cfg.batch, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
-    score = L * b * hkv * n * d * e + L * b * hq * d * e + b * n * 4 + L * b * hkv * n * 4
-    fold = L * b * hkv * n * 4 + 2 * b * n * 4
+    rows = hkv // merge
+    score = L * b * hkv * n * d * e + L * b * hq * d * e + b * n * 4 + L * b * rows * n * 4
+    fold = L * b * rows * n * 4 + 2 * b * n * 4
     append = 2 * 2 * L * b * hkv * d * e
     select = 2 * b * n * 4
     compact = 2 * 2 * L * b * hkv * d * e + 4 * b * 4
@@ -210,7 +211,7 @@ def secondary_workloads(B, dev, K, W):
     torch.cuda.synchronize()
     host_s = time.perf_counter() - h0
     score_ms = sum(p[0].elapsed_ms(p[1]) for p in pairs) / kq
-    by = step_bytes(cfg, cfg.budget + 1)
+    by = step_bytes(cfg, cfg.budget + 1, B.kv_score_merge(shape, cfg.budget + 1, params))
     out["qwen_8k"] = {"config": {"batch": cfg.batch, "layers": cfg.layers, "n_q_heads": cfg.n_q_heads,
                                  "n_kv_heads": cfg.n_kv_heads, "context": cfg.prefill_len, "budget": cfg.budget},
                       "step1": first, "steady_steps_per_s": round(kq / host_s, 1),
@@ -472,7 +473,8 @@ def main():
     other = secondary_workloads(B, dev, K, W) if not args.no_secondary else {}
 
     n = cfg.budget + 1
-    by = step_bytes(cfg, n)
+    merge = B.kv_score_merge(shape, n, full)
+    by = step_bytes(cfg, n, merge)
     score_avg_ms = sum(score_ms) / len(score_ms)
     achieved = by["score"] / (score_avg_ms * 1e-3) / 1e9
     step_gbps = by["total"] * steps_per_s / 1e9
@@ -498,7 +500,8 @@ def main():
         "pct_peak": round(100 * step_gbps / PEAK_HBM_GBPS, 2),
         "step_bytes": by,
         "device_ms_per_step": round(dev_ms / K, 4),
-        "roofline": {"kernel": "score_kernel<bf16, d128, group 4, LDS-resident>", "bound": "hbm",
+        "roofline": {"kernel": f"score_kernel<bf16, d128, group 4, LDS-resident, {merge} KV heads per workgroup>",
+                     "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": counter_traffic(),
                      "bytes_per_launch": by["score"], "avg_launch_ms": round(score_avg_ms, 5),

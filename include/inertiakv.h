@@ -97,6 +97,12 @@ typedef struct {
     int32_t recency_window; /* positions p >= new_pos - (window - 1) get the bias                   */
     int32_t rule;           /* kv_rule                                                             */
     int32_t score_variant;  /* kv_score_variant bits (0 = the attention score of Eq. 1)             */
+    int32_t score_merge;    /* performance only, results are unchanged: KV heads of one (layer,
+                               sequence) whose group sums one scoring workgroup adds before writing
+                               them.  0 = chosen from the shape and the device; else a divisor of
+                               n_kv_heads, at most 8, and 1 with VNorm.  Applies to slabs scored in
+                               one workgroup (not to long slabs scored in chunks).  kv_evict_finish
+                               must be given the value the separate step would use.               */
 } kv_params;
 
 /* Optional timing hooks: when an entry is non-NULL, kv_evict_step records that hipEvent_t on its stream
@@ -135,6 +141,12 @@ kv_status kv_rank_trace_state_bytes(int32_t batch, int32_t max_pos, size_t* byte
 
 /* Bytes of workspace needed by every call below for any n <= n_max cached tokens (host only). */
 kv_status kv_workspace_bytes(const kv_shape* shape, int32_t n_max, size_t* bytes);
+
+/* The params->score_merge that kv_evict_step resolves for a refresh step over n cached tokens (after the
+ * append) on the current device: KV heads whose group sums one scoring workgroup adds (1 for VNorm and for
+ * slabs scored in chunks; a positive params->score_merge is returned as given when it applies).  Host only;
+ * the automatic choice reads the device's CU count.  KV_ERR_INVALID_ARG as kv_evict_step for bad params. */
+kv_status kv_score_merge(const kv_shape* shape, int32_t n, const kv_params* params, int32_t* merge);
 
 /* Scoring + fold (Eq. 1 and Eq. 4, layer-sequential).  For every layer l = 1..K, query head h and cached
  * token i < n: z_h(i) = q_h . k_i / sqrt(d) (+ recency_bias if pos[i] >= cur_pos - (recency_window - 1)),

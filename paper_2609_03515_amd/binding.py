@@ -24,7 +24,8 @@ KV_PHASES = 5
 PHASES = ("append", "score", "fold", "select", "compact")
 
 EXPORTED = ("kv_workspace_bytes", "kv_score_ema", "kv_topk_select", "kv_compact", "kv_evict_step",
-            "kv_append", "kv_attend_score", "kv_evict_finish", "kv_rank_trace_state_bytes", "kv_status_string")
+            "kv_append", "kv_attend_score", "kv_evict_finish", "kv_rank_trace_state_bytes", "kv_score_merge",
+            "kv_status_string")
 KV_TRACE_COUNTS = 10
 
 
@@ -44,7 +45,7 @@ class KvParams(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_float), ("budget", ctypes.c_int32), ("refresh_period", ctypes.c_int32),
                 ("score_free", ctypes.c_int32), ("nonrefresh_init", ctypes.c_int32),
                 ("recency_bias", ctypes.c_float), ("recency_window", ctypes.c_int32), ("rule", ctypes.c_int32),
-                ("score_variant", ctypes.c_int32)]
+                ("score_variant", ctypes.c_int32), ("score_merge", ctypes.c_int32)]
 
 
 class KvTrace(ctypes.Structure):
@@ -81,6 +82,7 @@ def load_library(path: str = LIB_PATH):
     lib.kv_evict_finish.argtypes = [shp, prm, i32, i32, vp, vp, vp, vp, ctypes.POINTER(i32), vp, vp, rtr, vp, sz,
                                     vp]
     lib.kv_rank_trace_state_bytes.argtypes = [i32, i32, ctypes.POINTER(sz)]
+    lib.kv_score_merge.argtypes = [shp, i32, prm, ctypes.POINTER(i32)]
     for fn in EXPORTED[:-1]:
         getattr(lib, fn).restype = i32
     lib.kv_status_string.argtypes = [i32]
@@ -123,7 +125,8 @@ def make_shape(batch, layers, n_q_heads, n_kv_heads, head_dim, capacity, dtype) 
 
 
 def make_params(alpha, budget, refresh_period=1, score_free=False, nonrefresh_init="mean", recency_bias=0.0,
-                recency_window=0, rule="ema", vnorm=False, entropy=False, norms_emitted=False) -> KvParams:
+                recency_window=0, rule="ema", vnorm=False, entropy=False, norms_emitted=False,
+                score_merge=0) -> KvParams:
     init = {"mean": KV_INIT_MEAN, "min": KV_INIT_MIN}[nonrefresh_init] if isinstance(nonrefresh_init, str) \
         else int(nonrefresh_init)
     rl = {"ema": KV_RULE_EMA, "single": KV_RULE_SINGLE_STEP, "cumulative": KV_RULE_CUMULATIVE}[rule] \
@@ -131,13 +134,20 @@ def make_params(alpha, budget, refresh_period=1, score_free=False, nonrefresh_in
     variant = (KV_SCORE_VNORM if vnorm else 0) | (KV_SCORE_ENTROPY if entropy else 0) | \
         (KV_SCORE_NORMS_EMITTED if norms_emitted else 0)
     return KvParams(float(alpha), int(budget), int(refresh_period), int(bool(score_free)), init,
-                    float(recency_bias), int(recency_window), rl, variant)
+                    float(recency_bias), int(recency_window), rl, variant, int(score_merge))
 
 
 def kv_workspace_bytes(shape: KvShape, n_max: int) -> int:
     out = ctypes.c_size_t(0)
     _check("kv_workspace_bytes", load_library().kv_workspace_bytes(ctypes.byref(shape), int(n_max),
                                                                     ctypes.byref(out)))
+    return out.value
+
+
+def kv_score_merge(shape: KvShape, n: int, params: KvParams) -> int:
+    out = ctypes.c_int32(0)
+    _check("kv_score_merge", load_library().kv_score_merge(ctypes.byref(shape), int(n), ctypes.byref(params),
+                                                            ctypes.byref(out)))
     return out.value
 
 

@@ -144,15 +144,26 @@ ScoreArgs score_args(const kv_shape& s, const Layout& L, int n, const void* q, c
     a.recent_from = cur_pos - (recency_window - 1);
     a.bias = recency_window > 0 ? recency_bias : 0.0f;
     a.scale = (float)(1.0 / sqrt((double)s.head_dim));
+    a.merge = 1;
     return a;
 }
 
-// Scoring (Eq. 1) of rows [0, n) of every layer into the workspace r.
-kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, const void* k, const int32_t* pos,
-                    int cur_pos, float recency_bias, int recency_window, void* ws, hipStream_t st,
-                    const kv_trace* tr) {
-    ScoreArgs a = score_args(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws);
+// The scorer's plan for a refresh step with these scorer variants: KV heads of one (layer, sequence) share a
+// workgroup and add their group sums (`merge` of them: 0 = planned) unless VNorm needs each KV head's sums
+// apart (it weights them per head).
+ScorePlan scorer_plan(const kv_shape& s, const Layout& L, int variant, int merge) {
     ScorePlan plan = L.plan;
+    if (!(variant & KV_SCORE_VNORM))
+        score_merge(&plan, s.dtype, s.head_dim, s.n_kv_heads, s.layers * s.batch, merge);
+    return plan;
+}
+
+// Scoring (Eq. 1) of rows [0, n) of every layer into the workspace r: [layers][batch][n_kv / merge] rows.
+kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, const void* k, const int32_t* pos,
+                    int cur_pos, float recency_bias, int recency_window, const ScorePlan& splan, void* ws,
+                    hipStream_t st) {
+    ScoreArgs a = score_args(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws);
+    ScorePlan plan = splan;
     if (plan.split) {
         // long slabs: LDS-resident chunks of the attention kernel's K pass, then the finish kernel
         const int group = s.n_q_heads / s.n_kv_heads;
@@ -169,13 +180,14 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
     }
     a.chunk_rows = plan.chunk_rows;
     a.nchunk = plan.nchunk;
-    plan.grid = s.layers * s.batch * s.n_kv_heads;
+    a.merge = plan.merge;
+    plan.grid = s.layers * s.batch * (s.n_kv_heads / plan.merge);
     return hip_status(launch_score(s.dtype, s.head_dim, plan, a, st));
 }
 
 // Scorer perturbations (Sec. 5.1) of a refresh step: value-row norms and entropy factors for the fold.
-kv_status run_variants(const kv_shape& s, const Layout& L, int n, const void* v, int variant, void* ws,
-                       hipStream_t st) {
+kv_status run_variants(const kv_shape& s, const Layout& L, int n, const void* v, int variant, int r_groups,
+                       int rblock, void* ws, hipStream_t st) {
     if (!variant) return KV_OK;
     VariantArgs a{};
     a.v = v;
@@ -189,6 +201,8 @@ kv_status run_variants(const kv_shape& s, const Layout& L, int n, const void* v,
     a.cap = s.capacity;
     a.n = n;
     a.n_stride = L.n_stride;
+    a.r_groups = r_groups;
+    a.rblock = rblock;
     a.inv_hq = 1.0f / (float)s.n_q_heads;
     kv_status rc = KV_OK;
     if (variant & KV_SCORE_ENTROPY) rc = hip_status(launch_entropy(a, st));
@@ -196,9 +210,11 @@ kv_status run_variants(const kv_shape& s, const Layout& L, int n, const void* v,
     return rc;
 }
 
-// Layer fold of the workspace r into u (Eq. 2-4 by `rule`).
+// Layer fold of the workspace r into u (Eq. 2-4 by `rule`): r_groups rows per (layer, sequence), added in
+// blocks of rblock.
 kv_status run_fold(const kv_shape& s, const Layout& L, int n, float* u, float* s_out, int rule, float alpha,
-                   int variant, bool raw_out, void* ws, hipStream_t st, const kv_trace* tr) {
+                   int variant, int r_groups, int rblock, bool raw_out, void* ws, hipStream_t st,
+                   const kv_trace* tr) {
     FoldArgs f{};
     f.raw = raw_out ? at<float>(ws, L.raw_off) : nullptr;
     f.raw_scale = (float)(1.0 / ((double)s.layers * s.n_q_heads));
@@ -214,6 +230,8 @@ kv_status run_fold(const kv_shape& s, const Layout& L, int n, float* u, float* s
     f.n = n;
     f.n_stride = L.n_stride;
     f.cap = s.capacity;
+    f.r_groups = r_groups;
+    f.rblock = rblock;
     f.inv_hq = 1.0f / (float)s.n_q_heads;
     // Weights of the layer-sequential rule: EMA gives alpha^K to the prior and (1-alpha) alpha^(K-l) to
     // layer l; single-step keeps only the last layer; cumulative adds every layer to the prior.
@@ -284,7 +302,13 @@ kv_status check_params(const kv_params* params) {
     if (p.rule < KV_RULE_EMA || p.rule > KV_RULE_CUMULATIVE) return KV_ERR_INVALID_ARG;
     if (p.recency_window < 0 || !isfinite(p.recency_bias)) return KV_ERR_INVALID_ARG;
     if (p.score_variant & ~(KV_SCORE_VNORM | KV_SCORE_ENTROPY | KV_SCORE_NORMS_EMITTED)) return KV_ERR_INVALID_ARG;
+    if (p.score_merge < 0 || p.score_merge > kMaxMerge) return KV_ERR_INVALID_ARG;
+    if ((p.score_variant & KV_SCORE_VNORM) && p.score_merge > 1) return KV_ERR_INVALID_ARG;
     return KV_OK;
+}
+
+kv_status check_merge(const kv_shape& s, const kv_params& p) {
+    return (p.score_merge > 0 && s.n_kv_heads % p.score_merge) ? KV_ERR_INVALID_ARG : KV_OK;
 }
 
 // Refresh set (Eq. 5); Score-Free refreshes only at the first decode step.
@@ -404,6 +428,17 @@ kv_status kv_workspace_bytes(const kv_shape* shape, int32_t n_max, size_t* bytes
     return KV_OK;
 }
 
+kv_status kv_score_merge(const kv_shape* shape, int32_t n, const kv_params* params, int32_t* merge) {
+    kv_status rc = check_shape(shape);
+    if (rc != KV_OK) return rc;
+    if ((rc = check_params(params)) != KV_OK) return rc;
+    const kv_shape& s = *shape;
+    if ((rc = check_merge(s, *params)) != KV_OK) return rc;
+    if (!merge || n < 1 || n > s.capacity) return KV_ERR_INVALID_ARG;
+    *merge = scorer_plan(s, layout_for(s, n), params->score_variant, params->score_merge).merge;
+    return KV_OK;
+}
+
 kv_status kv_score_ema(const kv_shape* shape, int32_t n, const void* q, const void* k, const int32_t* pos,
                        int32_t cur_pos, float alpha, float recency_bias, int32_t recency_window, float* u,
                        float* s_out, void* ws, size_t ws_bytes, void* stream) {
@@ -419,9 +454,11 @@ kv_status kv_score_ema(const kv_shape* shape, int32_t n, const void* q, const vo
     const Layout L = layout_for(s, n);
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if ((rc = run_score(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws, st, nullptr)) != KV_OK)
+    const ScorePlan plan = scorer_plan(s, L, 0, 0);
+    if ((rc = run_score(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, plan, ws, st)) != KV_OK)
         return rc;
-    return run_fold(s, L, n, u, s_out, KV_RULE_EMA, alpha, 0, false, ws, st, nullptr);
+    return run_fold(s, L, n, u, s_out, KV_RULE_EMA, alpha, 0, s.n_kv_heads / plan.merge, 1, false, ws, st,
+                    nullptr);
 }
 
 kv_status kv_topk_select(const kv_shape* shape, int32_t n, int32_t budget, const float* u, const int32_t* pos,
@@ -468,6 +505,7 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
     if ((rc = check_params(params)) != KV_OK) return rc;
     if ((rc = check_rank_trace(rank_trace)) != KV_OK) return rc;
     const kv_params& p = *params;
+    if ((rc = check_merge(s, p)) != KV_OK) return rc;
     if (!n_out) return KV_ERR_INVALID_ARG;
     if (t < 1 || n_in < 0 || n_in + 1 > s.capacity || new_pos < 0) return KV_ERR_INVALID_ARG;
     if (!q || !k_new || !v_new || !k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
@@ -494,12 +532,15 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
     }
     if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, st, trace)) != KV_OK) return rc;
     if (refresh) {
+        const ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
+        const int r_groups = s.n_kv_heads / plan.merge;
         record(trace, 1, true, st);
-        rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, ws, st, trace);
-        if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, ws, st);
+        rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, plan, ws, st);
+        if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st);
         record(trace, 1, false, st);
         if (rc == KV_OK)
-            rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, rank_trace != nullptr, ws, st, trace);
+            rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, r_groups, 1, rank_trace != nullptr,
+                          ws, st, trace);
         if (rc != KV_OK) return rc;
     }
     rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, trace);
@@ -571,6 +612,7 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
     if ((rc = check_params(params)) != KV_OK) return rc;
     if ((rc = check_rank_trace(rank_trace)) != KV_OK) return rc;
     const kv_params& p = *params;
+    if ((rc = check_merge(s, p)) != KV_OK) return rc;
     if (!n_out || t < 1 || n < 1 || n > s.capacity) return KV_ERR_INVALID_ARG;
     if (!k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
     if (!aligned(k, 16) || !aligned(v, 16) || !aligned(u, 4) || !aligned(pos, 4) || !aligned(s_out, 4))
@@ -583,9 +625,14 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
         // value norms already written by the step's attention calls: only the entropy factors remain
         const int computed = (p.score_variant & KV_SCORE_NORMS_EMITTED) ? (p.score_variant & ~KV_SCORE_VNORM)
                                                                          : p.score_variant;
-        if ((rc = run_variants(s, L, n, v, computed & (KV_SCORE_VNORM | KV_SCORE_ENTROPY), ws, st)) != KV_OK)
+        // the attention wrote one row of r per KV head; they are added in the blocks the scorer would merge,
+        // so the fused and the separate step give identical utilities
+        const int rblock = scorer_plan(s, L, p.score_variant, p.score_merge).merge;
+        if ((rc = run_variants(s, L, n, v, computed & (KV_SCORE_VNORM | KV_SCORE_ENTROPY), s.n_kv_heads, rblock,
+                               ws, st)) != KV_OK)
             return rc;
-        rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, rank_trace != nullptr, ws, st, nullptr);
+        rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, s.n_kv_heads, rblock,
+                      rank_trace != nullptr, ws, st, nullptr);
         if (rc != KV_OK) return rc;
     }
     rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, nullptr);

@@ -4,7 +4,8 @@
 // u <- alpha^K u + sum_l (1 - alpha) alpha^(K-l) s_l (the weights the appendix states).  The host passes the
 // prior weight and the per-layer weights (also for the single-step and cumulative rules), so the layers can
 // be reduced in parallel.  A workgroup covers 32 tokens of one sequence: each thread reads four consecutive
-// tokens (16-byte loads) of the group sums r of one layer slice for every KV head, weights them, and the
+// tokens (16-byte loads) of the group sums r of one layer slice (one row per KV head, or per block of KV heads
+// the scorer already added), weights them, and the
 // partial sums of the 32 layer slices are added in a fixed order, so the result is deterministic.
 #include "kernels.h"
 #include "kv_common.h"
@@ -27,9 +28,9 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
     f32x4 racc = {0.0f, 0.0f, 0.0f, 0.0f};  // rank trace: sum over layers of the plain group sums
     if (tok0 < a.n) {
         for (int l = slice; l < a.layers; l += kSlices) {
-            const float* rl = a.r + ((size_t)(l * a.batch + b) * a.hkv) * a.n_stride + tok0;
+            const float* rl = a.r + ((size_t)(l * a.batch + b) * a.r_groups) * a.n_stride + tok0;
             f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
-            if (a.vnorm) {
+            if (a.vnorm) {  // r_groups == hkv: one row per KV head
                 // VNorm: each KV head's group sum times the token's value-norm factor norm / mean norm
                 // (factor 1 where the slab's norms are all zero)
                 const float* nl = a.vnorm + ((size_t)(l * a.batch + b) * a.hkv) * a.n_stride + tok0;
@@ -45,7 +46,13 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
                 }
                 racc += plain;
             } else {
-                for (int g = 0; g < a.hkv; ++g) s += *reinterpret_cast<const f32x4*>(rl + (size_t)g * a.n_stride);
+                // block sums first, then the blocks in order
+                for (int g = 0; g < a.r_groups; g += a.rblock) {
+                    f32x4 t = *reinterpret_cast<const f32x4*>(rl + (size_t)g * a.n_stride);
+                    for (int j = 1; j < a.rblock; ++j)
+                        t += *reinterpret_cast<const f32x4*>(rl + (size_t)(g + j) * a.n_stride);
+                    s += t;
+                }
                 racc += s;
             }
             s *= a.inv_hq;

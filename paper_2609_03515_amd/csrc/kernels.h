@@ -9,6 +9,8 @@ namespace ikv {
 
 constexpr int kMaxLayers = 256;
 constexpr int kMaxGroup = 16;
+constexpr int kMaxMerge = 8;   // KV heads one scoring workgroup may add up
+constexpr size_t kLdsPerCu = 160 * 1024;  // gfx950
 
 // Scoring of one step (Eq. 1).  One workgroup streams a whole (layer, sequence, KV head) slab and keeps its
 // logits in LDS, writing the group probability sums r.  Slabs too long for that are cut into chunks
@@ -37,6 +39,7 @@ struct ScoreArgs {
     float* vinv;
     float* npart;   // [layers][batch][n_kv][nchunk]
     int emit_norms;
+    int merge;      // scorer: KV heads per workgroup whose group sums are added (r: [layers][batch][n_kv / merge])
 };
 
 struct ScorePlan {
@@ -46,11 +49,17 @@ struct ScorePlan {
     int rows_per_iter; // rows one workgroup covers per loop iteration
     int chunk_rows;    // rows per workgroup
     int nchunk;        // workgroups per slab
+    int merge;         // KV heads per workgroup (LDS-resident scorer; set by score_merge)
     size_t lds_bytes;  // dynamic LDS per workgroup (fast path)
     int grid;
 };
 
 bool score_plan(int dtype, int head_dim, int group, int n, ScorePlan* plan);
+// Picks how many KV heads of a (layer, sequence) one LDS-resident scoring workgroup handles (lb_count =
+// layers * batch; `forced` > 0: that many, a divisor of hkv) and grows the plan's LDS by their merged sums;
+// 1 for split plans or when the sums do not fit.  The automatic choice queries the device (CU count, and the
+// merged kernel's occupancy on first use per kernel instance).
+int score_merge(ScorePlan* plan, int dtype, int head_dim, int hkv, int lb_count, int forced);
 hipError_t launch_score(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s);
 hipError_t launch_split_finish(const ScoreArgs& a, hipStream_t s);
 
@@ -89,6 +98,9 @@ struct FoldArgs {
     float* u;
     float* s_out;  // nullable [layers][batch][n]
     int batch, layers, hkv, n, n_stride, cap;
+    // rows of r per (layer, sequence), added in blocks of rblock consecutive rows (block sums first, then the
+    // blocks in order: the order a scorer merging rblock KV heads per workgroup adds them in)
+    int r_groups, rblock;
     float inv_hq;
     float prior_w;
     float w[kMaxLayers];
@@ -104,6 +116,7 @@ struct VariantArgs {
     float* vnorm_inv_mean;  // [layers][batch][n_kv]
     float* entropy;         // [layers][batch]
     int batch, layers, hkv, cap, n, n_stride;
+    int r_groups, rblock;  // as in FoldArgs
     float inv_hq;
 };
 hipError_t launch_vnorm(int dtype, int head_dim, const VariantArgs& a, hipStream_t s);

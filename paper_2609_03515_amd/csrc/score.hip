@@ -19,13 +19,23 @@
 namespace ikv {
 namespace {
 
-// One workgroup per slab.  The slab is cut into units of RPW rows; waves claim units from an LDS counter when
-// they issue the units' loads, so a wave whose loads come back late simply processes fewer units instead of
-// holding the whole workgroup at the barrier (with a static split the last wave finished ~40% after the first).
-// Logits are stored per unit; after a barrier the epilogue walks the units in a fixed pattern.
-template <typename T, int D, int GP>
-__global__ __launch_bounds__(kThreads)
-__attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWavesLds))) void score_lds_kernel(ScoreArgs a) {
+// A workgroup scores `merge` consecutive KV heads (slabs) of one (layer, sequence) in turn.  Each slab is cut
+// into units of RPW rows; waves claim units from an LDS counter when they issue the units' loads, so a wave
+// whose loads come back late simply processes fewer units instead of holding the whole workgroup at the
+// barrier (with a static split the last wave finished ~40% after the first).  Logits are stored per unit;
+// after a barrier the epilogue walks the units in a fixed pattern.  With merge > 1 the slabs' group sums are
+// added in LDS (in KV-head order) and written once: one row of r per `merge` KV heads.
+// The merged variant's LDS also holds the sums, so it runs fewer workgroups per CU: it asks for at most the
+// waves of two workgroups per SIMD, which leaves it the registers of the slab loop.
+template <typename T, int D, int GP, bool kMerge>
+constexpr int score_waves_per_eu() {
+    constexpr int w = Geometry<T, D, GP>::kMinWavesLds;
+    return kMerge && w > 2 * kWaves / 4 ? 2 * kWaves / 4 : w;
+}
+
+template <typename T, int D, int GP, bool kMerge>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(score_waves_per_eu<T, D, GP, kMerge>())))
+void score_lds_kernel(ScoreArgs a) {
     using L = Lane<T, D, GP>;
     using chunk_t = typename L::chunk_t;
     constexpr int RPG = L::RPG, CPL = L::CPL, RPW = L::RPW;
@@ -33,27 +43,32 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWavesLds))) void scor
 
     extern __shared__ float zs[];
     __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
-    __shared__ int next_unit;
+    __shared__ int next_unit[kMaxMerge];  // one claim counter per slab
 
     const L ln;
-    const int s = blockIdx.x;
-    const int g = s % a.hkv;
-    const int b = (s / a.hkv) % a.batch;
-    const int l = s / (a.hkv * a.batch);
-    const size_t slab = (size_t)s;
+    const int merge = kMerge ? a.merge : 1;
+    const int blocks = a.hkv / merge;
+    const int lb = blockIdx.x / blocks;  // l * batch + b
+    const int gblk = blockIdx.x % blocks;
+    const int b = lb % a.batch;
     const int n = a.n;
     const int nunits = (n + RPW - 1) / RPW;
-    const T* kslab = static_cast<const T*>(a.k) + slab * a.cap * D;
-    const __amdgpu_buffer_rsrc_t krs = raw_rsrc(kslab, n * L::kRowBytes);
+    // merged group sums after the logits (sized by the plan: the logits' units rounded up to whole iterations)
+    float* racc = zs + (size_t)((nunits + kWaves - 1) / kWaves) * kThreads;
     const __amdgpu_buffer_rsrc_t prs = raw_rsrc(a.pos + (size_t)b * a.cap, n * 4);
+    auto k_rsrc = [&](int g) {
+        return raw_rsrc(static_cast<const T*>(a.k) + ((size_t)lb * a.hkv + g) * a.cap * D, n * L::kRowBytes);
+    };
 
-    if (threadIdx.x == 0) next_unit = 0;
+    if (threadIdx.x < kMaxMerge) next_unit[threadIdx.x] = 0;
+    int g = gblk * merge;
+    __amdgpu_buffer_rsrc_t krs = k_rsrc(g);
     chunk_t qv[GP][CPL];
-    ln.load_q(a, (size_t)l * a.batch + b, g, qv);
+    ln.load_q(a, (size_t)lb, g, qv);
     __syncthreads();
-    auto claim = [&]() -> int {
+    auto claim = [&](int gi) -> int {
         int u = 0;
-        if (ln.lane == 0) u = atomicAdd(&next_unit, 1);
+        if (ln.lane == 0) u = atomicAdd(&next_unit[gi], 1);
         return __builtin_amdgcn_readfirstlane(u);
     };
 
@@ -61,92 +76,110 @@ __attribute__((amdgpu_waves_per_eu(Geometry<T, D, GP>::kMinWavesLds))) void scor
     // every path (claims past the end read zeros), so the wait before a reduction covers only its own buffer.
     chunk_t kbuf[kNbuf][RPG][CPL];
     int pbuf[kNbuf], ubuf[kNbuf];
+    auto prime = [&](int gi) {
 #pragma unroll
-    for (int j = 0; j < kNbuf - 1; ++j) {
-        ubuf[j] = claim();
-        ln.load_unit(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
-    }
-    float m = kFloor;
-    bool more = true;
-    while (more) {
+        for (int j = 0; j < kNbuf - 1; ++j) {
+            ubuf[j] = claim(gi);
+            ln.load_unit(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
+        }
+    };
+    prime(0);
+    for (int gi = 0; gi < merge; ++gi, ++g) {
+        float m = kFloor;
+        bool more = true;
+        while (more) {
 #pragma unroll
-        for (int j = 0; j < kNbuf; ++j) {
-            const int slot = (j + kNbuf - 1) % kNbuf;
-            ubuf[slot] = claim();
-            ln.load_unit(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
-            if (more && ubuf[j] < nunits) {
-                const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.unit_row(ubuf[j]), n);
-                m = fmaxf(m, z);
-                zs[ubuf[j] * kWave + ln.lane] = z;
-            } else {
-                more = false;  // claims only grow: every later unit of this wave is past the end too
+            for (int j = 0; j < kNbuf; ++j) {
+                const int slot = (j + kNbuf - 1) % kNbuf;
+                ubuf[slot] = claim(gi);
+                ln.load_unit(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
+                if (more && ubuf[j] < nunits) {
+                    const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.unit_row(ubuf[j]), n);
+                    m = fmaxf(m, z);
+                    zs[ubuf[j] * kWave + ln.lane] = z;
+                } else {
+                    more = false;  // claims only grow: every later unit of this wave is past the end too
+                }
             }
         }
-    }
-
-    // epilogue: per-head softmax statistics, then normalised group sums.  Thread (wave w, lane) visits units
-    // w, w + kWaves, ...; a lane's head is the same in every unit.
-    float* zl = zs + ln.wave * kWave + ln.lane;
-    constexpr int kStep = kWaves * kWave;  // LDS words between a thread's consecutive units
-    const int mine = nunits > ln.wave ? (nunits - ln.wave + kWaves - 1) / kWaves : 0;
-#pragma unroll
-    for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
-    if (ln.lane < GP) red_m[ln.wave][ln.lane] = m;
-    __syncthreads();
-    m = red_m[0][ln.hh];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][ln.hh]);
-    auto expo = [&](float z) { return z == -INFINITY ? 0.0f : __expf(z - m); };
-    float ssum = 0.0f;
-    int i = 0;
-    for (; i + kEpi <= mine; i += kEpi) {
-        float e[kEpi];
-#pragma unroll
-        for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
-#pragma unroll
-        for (int v = 0; v < kEpi; ++v) {
-            e[v] = expo(e[v]);
-            ssum += e[v];
-            zl[(i + v) * kStep] = e[v];
+        if (gi + 1 < merge) {  // the next slab's first loads overlap this slab's epilogue
+            krs = k_rsrc(g + 1);
+            prime(gi + 1);
         }
+
+        // epilogue: per-head softmax statistics, then normalised group sums.  Thread (wave w, lane) visits
+        // units w, w + kWaves, ...; a lane's head is the same in every unit.
+        float* zl = zs + ln.wave * kWave + ln.lane;
+        constexpr int kStep = kWaves * kWave;  // LDS words between a thread's consecutive units
+        const int mine = nunits > ln.wave ? (nunits - ln.wave + kWaves - 1) / kWaves : 0;
+#pragma unroll
+        for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+        if (ln.lane < GP) red_m[ln.wave][ln.lane] = m;
+        __syncthreads();
+        m = red_m[0][ln.hh];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][ln.hh]);
+        auto expo = [&](float z) { return z == -INFINITY ? 0.0f : __expf(z - m); };
+        float ssum = 0.0f;
+        int i = 0;
+        for (; i + kEpi <= mine; i += kEpi) {
+            float e[kEpi];
+#pragma unroll
+            for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
+#pragma unroll
+            for (int v = 0; v < kEpi; ++v) {
+                e[v] = expo(e[v]);
+                ssum += e[v];
+                zl[(i + v) * kStep] = e[v];
+            }
+        }
+        for (; i < mine; ++i) {
+            const float e = expo(zl[i * kStep]);
+            ssum += e;
+            zl[i * kStep] = e;
+        }
+#pragma unroll
+        for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
+        if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;
+        __syncthreads();
+        float tot = red_s[0][ln.hh];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) tot += red_s[w][ln.hh];
+        const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
+        auto prob = [&](float e) { return e * inv; };
+        // group sum of the normalised probabilities of each row.  One slab: staged by one lane per row in the
+        // first RPW words of the row's unit block (only this wave reads that block, and it has already read
+        // the words) for the coalesced store below.  Several: added to the row's merged sum.
+        static_assert(RPW % 4 == 0, "the coalesced store moves 4 rows at a time");
+        auto emit = [&](int unit, float sum) {
+            if (ln.hh == 0) {
+                const int row = ln.kk * L::NG + ln.grp;
+                if (merge == 1) {
+                    zs[unit * kWave + row] = sum;
+                } else {
+                    float* acc = racc + unit * RPW + row;
+                    *acc = gi == 0 ? sum : *acc + sum;
+                }
+            }
+        };
+        i = 0;
+        for (; i + kEpi <= mine; i += kEpi) {
+            float e[kEpi];
+#pragma unroll
+            for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
+#pragma unroll
+            for (int v = 0; v < kEpi; ++v) emit(ln.wave + (i + v) * kWaves, group_allsum<GP>(prob(e[v])));
+        }
+        for (; i < mine; ++i) emit(ln.wave + i * kWaves, group_allsum<GP>(prob(zl[i * kStep])));
+        __syncthreads();  // also: every read of this slab's logits is done before the next slab's K pass
+        if (gi + 1 < merge) ln.load_q(a, (size_t)lb, g + 1, qv);
     }
-    for (; i < mine; ++i) {
-        const float e = expo(zl[i * kStep]);
-        ssum += e;
-        zl[i * kStep] = e;
-    }
-#pragma unroll
-    for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
-    if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;
-    __syncthreads();
-    float tot = red_s[0][ln.hh];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) tot += red_s[w][ln.hh];
-    const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
-    auto prob = [&](float e) { return e * inv; };
-    float* rrow = a.r + slab * a.n_stride;
-    // group sum of the normalised probabilities of each row, staged by one lane per row in the first RPW words
-    // of the row's unit block (only this wave reads that block, and it has already read the words) for the
-    // coalesced store below
-    static_assert(RPW % 4 == 0, "the coalesced store moves 4 rows at a time");
-    auto emit = [&](int unit, float sum) {
-        if (ln.hh == 0) zs[unit * kWave + ln.kk * L::NG + ln.grp] = sum;
-    };
-    i = 0;
-    for (; i + kEpi <= mine; i += kEpi) {
-        float e[kEpi];
-#pragma unroll
-        for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
-#pragma unroll
-        for (int v = 0; v < kEpi; ++v) emit(ln.wave + (i + v) * kWaves, group_allsum<GP>(prob(e[v])));
-    }
-    for (; i < mine; ++i) emit(ln.wave + i * kWaves, group_allsum<GP>(prob(zl[i * kStep])));
-    __syncthreads();
     // rows [4j, 4j + 4) lie in one unit (RPW is a multiple of 4); rows up to the padded stride are scratch
-    const __amdgpu_buffer_rsrc_t rrs = raw_rsrc(rrow, a.n_stride * 4);
+    const __amdgpu_buffer_rsrc_t rrs = raw_rsrc(a.r + ((size_t)lb * blocks + gblk) * a.n_stride, a.n_stride * 4);
     for (int j = threadIdx.x; j * 4 < n; j += kThreads) {
         const int row = j * 4;
-        store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]));
+        const float* src = merge == 1 ? &zs[(row / RPW) * kWave + row % RPW] : &racc[row];
+        store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(src));
     }
 }
 
@@ -191,17 +224,17 @@ __global__ __launch_bounds__(kFinishThreads) void split_finish_kernel(ScoreArgs 
 
 template <typename T, int D, int GP>
 hipError_t launch_lds(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
-    auto kern = score_lds_kernel<T, D, GP>;
+    auto kern = a.merge > 1 ? score_lds_kernel<T, D, GP, true> : score_lds_kernel<T, D, GP, false>;
     if (plan.lds_bytes > 64 * 1024) {
-        static bool raised = false;  // idempotent attribute; a benign race between threads
-        if (!raised) {
+        static bool raised[2] = {false, false};  // idempotent attribute; a benign race between threads
+        if (!raised[a.merge > 1]) {
             hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax);
             if (e != hipSuccess) return e;
-            raised = true;
+            raised[a.merge > 1] = true;
         }
     }
-    hipLaunchKernelGGL(kern, dim3(a.layers * a.batch * a.hkv), dim3(kThreads), plan.lds_bytes, s, a);
+    hipLaunchKernelGGL(kern, dim3(a.layers * a.batch * (a.hkv / a.merge)), dim3(kThreads), plan.lds_bytes, s, a);
     return hipGetLastError();
 }
 
@@ -213,6 +246,42 @@ hipError_t launch_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
         if (!plan.split) return launch_lds<T, D, GP>(plan, a, s);
         return hipErrorInvalidValue;  // long slabs are scored in chunks (launch_score_chunks)
     }
+}
+
+// Workgroups of the merged variant one CU holds by its registers (0 when the query fails); cached per
+// instance (a benign race: every thread computes the same value).
+template <typename T, int D, int GP>
+int merged_occupancy() {
+    if constexpr (Geometry<T, D, 1>::kLpr < GP) {
+        return 0;
+    } else {
+        static int occ = -1;
+        if (occ < 0) {
+            int v = 0;
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, score_lds_kernel<T, D, GP, true>, kThreads, 0) !=
+                hipSuccess)
+                v = 0;
+            occ = v;
+        }
+        return occ;
+    }
+}
+
+template <typename T, int D>
+int merged_occupancy_d(int gp) {
+    switch (gp) {
+        case 1: return merged_occupancy<T, D, 1>();
+        case 2: return merged_occupancy<T, D, 2>();
+        case 4: return merged_occupancy<T, D, 4>();
+        case 8: return merged_occupancy<T, D, 8>();
+        case 16: return merged_occupancy<T, D, 16>();
+        default: return 0;
+    }
+}
+
+int merged_occupancy(int dtype, int head_dim, int gp) {
+    if (dtype == 0) return head_dim == 64 ? merged_occupancy_d<float, 64>(gp) : merged_occupancy_d<float, 128>(gp);
+    return head_dim == 64 ? merged_occupancy_d<bf16_t, 64>(gp) : merged_occupancy_d<bf16_t, 128>(gp);
 }
 
 template <typename T, int D>
@@ -246,17 +315,47 @@ bool score_plan(int dtype, int head_dim, int group, int n, ScorePlan* plan) {
     const size_t lds = (size_t)nit * kThreads * sizeof(float);
     if (lds <= kFastLdsMax) {
         plan->split = false;
+        plan->merge = 1;
         plan->chunk_rows = nit * rpi;
         plan->nchunk = 1;
         plan->lds_bytes = lds;
     } else {  // scored in chunks, planned by attend_plan
         plan->split = true;
+        plan->merge = 1;
         plan->chunk_rows = 0;
         plan->nchunk = 0;
         plan->lds_bytes = 0;
     }
     plan->grid = 0;
     return true;
+}
+
+int score_merge(ScorePlan* plan, int dtype, int head_dim, int hkv, int lb_count, int forced) {
+    plan->merge = 1;
+    if (plan->split || hkv < 2) return 1;
+    const size_t racc = (size_t)plan->chunk_rows * sizeof(float);  // the merged sums
+    if (plan->lds_bytes + racc > kFastLdsMax) return 1;
+    int best = 1;
+    if (forced > 0) {
+        best = forced;
+    } else {
+        // Writing the group sums while the grid still streams K costs far more than their bytes, so KV heads
+        // of one (layer, sequence) share a workgroup and add their sums in LDS when that still fills the chip:
+        // the largest merge (a divisor of hkv) whose grid gives every CU as many workgroups as it holds (by LDS
+        // and by registers).
+        const int reg_per_cu = merged_occupancy(dtype, head_dim, plan->group_pad);
+        int dev = 0, cus = 0;
+        if (reg_per_cu < 1 || hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+            return 1;
+        size_t per_cu = kLdsPerCu / (plan->lds_bytes + racc);
+        if (per_cu > (size_t)reg_per_cu) per_cu = reg_per_cu;
+        for (int m = 2; m <= kMaxMerge && m <= hkv; ++m)
+            if (hkv % m == 0 && (size_t)lb_count * (hkv / m) >= per_cu * (size_t)cus) best = m;
+    }
+    plan->merge = best;
+    if (best > 1) plan->lds_bytes += racc;
+    return best;
 }
 
 hipError_t launch_score(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {

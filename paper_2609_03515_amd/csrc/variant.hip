@@ -84,7 +84,7 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
     }
 }
 
-// One workgroup per (layer, sequence): s(i) = (1/H) sum_g r_g(i); with S = sum_i s(i) the entropy of
+// One workgroup per (layer, sequence): s(i) = (1/H) sum of the r rows of the (layer, sequence); with S = sum_i s(i) the entropy of
 // p = s / S is ln S - (1/S) sum_i s(i) ln s(i); divided by ln n (factor 1 when n = 1 or S = 0).  Each thread
 // reads 4 consecutive tokens of every KV head per pass (rows are padded to a multiple of 64; the padding is
 // masked), so a 32k-token slab takes 8 passes.
@@ -93,11 +93,16 @@ constexpr int kEThreads = 1024;
 __global__ __launch_bounds__(kEThreads) void entropy_kernel(VariantArgs a) {
     __shared__ float ps[kEThreads / kWave], pe[kEThreads / kWave];
     const size_t lb = blockIdx.x;
-    const float* rb = a.r + lb * a.hkv * a.n_stride;
+    const float* rb = a.r + lb * a.r_groups * a.n_stride;
     float S = 0.0f, E = 0.0f;
     for (int i = threadIdx.x * 4; i < a.n; i += kEThreads * 4) {
         f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
-        for (int g = 0; g < a.hkv; ++g) s += *reinterpret_cast<const f32x4*>(rb + (size_t)g * a.n_stride + i);
+        for (int g = 0; g < a.r_groups; g += a.rblock) {  // blocks of rows as the fold adds them
+            f32x4 t = *reinterpret_cast<const f32x4*>(rb + (size_t)g * a.n_stride + i);
+            for (int j = 1; j < a.rblock; ++j)
+                t += *reinterpret_cast<const f32x4*>(rb + (size_t)(g + j) * a.n_stride + i);
+            s += t;
+        }
         s *= a.inv_hq;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {

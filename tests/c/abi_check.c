@@ -50,6 +50,10 @@ int main(void) {
     CHECK(kv_evict_step(&s, &p, 2, 3277, 40000, fake, fake, fake, fake, fake, (float*)fake, (int32_t*)fake, &n_out,
                         NULL, NULL, NULL, NULL, NULL, 0, NULL) == KV_ERR_INVALID_ARG);
     p.alpha = 0.9f;
+    p.score_merge = 3; /* not a divisor of the 8 KV heads */
+    CHECK(kv_evict_step(&s, &p, 2, 3277, 40000, fake, fake, fake, fake, fake, (float*)fake, (int32_t*)fake, &n_out,
+                        NULL, NULL, NULL, NULL, NULL, 0, NULL) == KV_ERR_INVALID_ARG);
+    p.score_merge = 0;
     CHECK(kv_attend_score(&s, 30, 3, 3278, fake, fake, fake, (const int32_t*)fake, 40000, 0.5f, 64, 1, fake, NULL, 0,
                           NULL) == KV_ERR_INVALID_ARG); /* layers 30..32 past the last */
     CHECK(kv_rank_trace_state_bytes(8, 40000, &st) == KV_OK && st == 8 * (4 + 2 * 1250) * 4);

@@ -124,6 +124,20 @@ def _step(s, p, t=1, n_in=10, n_out=True, **kw):
     return rc, out.value
 
 
+def test_score_merge_query(lib):
+    s = shape()   # 2 KV heads
+    assert B.kv_score_merge(s, 50, B.make_params(0.9, 20, score_merge=2)) == 2
+    assert B.kv_score_merge(s, 50, B.make_params(0.9, 20, score_merge=1)) == 1
+    assert B.kv_score_merge(s, 50, B.make_params(0.9, 20, vnorm=True)) == 1
+    out = ctypes.c_int32(-7)
+    L = lib_()
+    for p, n in ((B.make_params(0.9, 20, score_merge=4), 50), (B.make_params(0.9, 20, vnorm=True, score_merge=2), 50),
+                 (B.make_params(0.9, 20), 0), (B.make_params(0.9, 20), 101)):
+        assert L.kv_score_merge(ctypes.byref(s), n, ctypes.byref(p), ctypes.byref(out)) == B.KV_ERR_INVALID_ARG
+    assert L.kv_score_merge(ctypes.byref(s), 50, ctypes.byref(B.make_params(0.9, 20)), None) == B.KV_ERR_INVALID_ARG
+    assert out.value == -7
+
+
 def test_step_validation(lib):
     s = shape()
     good = B.make_params(0.9, 20)
@@ -145,6 +159,12 @@ def test_step_validation(lib):
     assert bad_variant.score_variant == B.KV_SCORE_VNORM | B.KV_SCORE_ENTROPY
     bad_variant.score_variant = 8
     assert _step(s, bad_variant)[0] == B.KV_ERR_INVALID_ARG
+    for merge in (-1, 9):
+        assert _step(s, B.make_params(0.9, 20, score_merge=merge))[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, B.make_params(0.9, 20, score_merge=3))[0] == B.KV_ERR_INVALID_ARG   # not a divisor of n_kv
+    assert _step(s, B.make_params(0.9, 20, vnorm=True, score_merge=2))[0] == B.KV_ERR_INVALID_ARG
+    assert _step(s, B.make_params(0.9, 20, vnorm=True, score_merge=1))[0] == B.KV_ERR_WORKSPACE
+    assert _step(s, B.make_params(0.9, 20, score_merge=2))[0] == B.KV_ERR_WORKSPACE
     assert _step(s, good, v_new=None)[0] == B.KV_ERR_INVALID_ARG
     assert _step(s, good, k=FAKE + 2)[0] == B.KV_ERR_UNSUPPORTED
     rc, out = _step(s, good)
@@ -206,6 +226,8 @@ def test_finish_validation(lib):
     assert call(n=101) == B.KV_ERR_INVALID_ARG
     assert call(n_out=False) == B.KV_ERR_INVALID_ARG
     assert call(k=FAKE + 8) == B.KV_ERR_UNSUPPORTED
+    assert call(p=B.make_params(0.9, 20, score_merge=3)) == B.KV_ERR_INVALID_ARG
+    assert call(p=B.make_params(0.9, 20, vnorm=True, score_merge=4)) == B.KV_ERR_INVALID_ARG
     assert call() == B.KV_ERR_WORKSPACE and out.value == -7
 
 

@@ -32,7 +32,7 @@ def attend_layers(shape, cfg, n, q, k, v, pos, cur_pos, emit, ws, per_layer):
     return o
 
 
-def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False, emit_norms=False):
+def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False, emit_norms=False, merge=0):
     w = Workload(cfg)
     cap = max(cfg.prefill_len, cfg.budget) + 1
     st = w.prefill(capacity=cap)
@@ -41,7 +41,7 @@ def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False, emit_n
     shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
     params = B.make_params(cfg.alpha, cfg.budget, cfg.refresh_period, cfg.score_free, cfg.nonrefresh_init,
                            cfg.recency_bias, cfg.recency_window, vnorm=vnorm, entropy=entropy,
-                           norms_emitted=emit_norms)
+                           norms_emitted=emit_norms, score_merge=merge)
     op = oracle_params(cfg, vnorm=vnorm, entropy=entropy)
     ws = B.workspace(shape, cap)
     n = st["n"]
@@ -108,6 +108,14 @@ def test_fused_step_scorer_variants(name, emit_norms):
         run_fused_lockstep(cfg, 2, per_layer=False, vnorm=True, entropy=False, emit_norms=True)
 
 
+@pytest.mark.parametrize("name,merge", [("llama8b_reduced", 4), ("llama8b_split_step1", 8), ("qwen_reduced", 2)])
+def test_fused_step_merged_fold(name, merge):
+    """The finish folds the attention's per-KV-head scores in the blocks a merging scorer would add (one and
+    several chunks per slab)."""
+    cfg, steps = CASES[name]
+    run_fused_lockstep(cfg, steps, per_layer=True, entropy=True, merge=merge)
+
+
 # ---- one call on random inputs over the supported geometries -------------------------------------------
 GEOMS = [  # (dtype, head_dim, n_q, n_kv, n)
     ("bf16", 128, 32, 8, 1), ("bf16", 128, 32, 8, 15), ("bf16", 128, 32, 8, 256), ("bf16", 128, 32, 8, 257),
@@ -161,16 +169,21 @@ def test_attend_geometries(dtype, d, hq, hkv, n):
     assert_close(s_out.cpu().numpy(), s_ref, "scores from the attention")
 
 
-def test_fused_scores_equal_separate_pass_bitwise():
+@pytest.mark.parametrize("merge,entropy", [(0, False), (1, False), (2, False), (4, False), (8, False), (4, True)],
+                         ids=["auto", "merge1", "merge2", "merge4", "merge8", "merge4_entropy"])
+def test_fused_scores_equal_separate_pass_bitwise(merge, entropy):
     """With one chunk per slab the attention computes its scores with the scorer's arithmetic in the same
-    order, so the fused step and kv_evict_step leave bit-identical utilities and caches."""
+    order, so the fused step and kv_evict_step leave bit-identical utilities and caches; also when the scorer
+    adds the group sums of several KV heads in one workgroup (the finish adds the attention's per-KV-head rows
+    in the same blocks), and with entropy weighting (computed from those sums)."""
     cfg = LLAMA8B.scaled(batch=8, layers=16, prefill_len=500, budget=400)
     w = Workload(cfg)
     cap = cfg.prefill_len + 1
     st = to_device(w.prefill(capacity=cap))
     st2 = {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in st.items()}
     shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
-    params = B.make_params(cfg.alpha, cfg.budget, 1, False, "mean", cfg.recency_bias, cfg.recency_window)
+    params = B.make_params(cfg.alpha, cfg.budget, 1, False, "mean", cfg.recency_bias, cfg.recency_window,
+                           entropy=entropy, score_merge=merge)
     ws = B.workspace(shape, cap)
     n = st["n"]
     si = to_device(w.step_inputs(1))

@@ -18,7 +18,7 @@ pytestmark = pytest.mark.gpu
 B = pytest.importorskip("paper_2609_03515_amd.binding")
 
 
-def run_lockstep(cfg, steps, seed=None, rule="ema", vnorm=False, entropy=False):
+def run_lockstep(cfg, steps, seed=None, rule="ema", vnorm=False, entropy=False, merge=0):
     w = Workload(cfg, seed=seed)
     cap = max(cfg.prefill_len, cfg.budget) + 1          # room for the cache to grow up to B + 1
     st = w.prefill(capacity=cap)
@@ -26,7 +26,8 @@ def run_lockstep(cfg, steps, seed=None, rule="ema", vnorm=False, entropy=False):
     dev = to_device(st)
     shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
     params = B.make_params(cfg.alpha, cfg.budget, cfg.refresh_period, cfg.score_free, cfg.nonrefresh_init,
-                           cfg.recency_bias, cfg.recency_window, rule, vnorm=vnorm, entropy=entropy)
+                           cfg.recency_bias, cfg.recency_window, rule, vnorm=vnorm, entropy=entropy,
+                           score_merge=merge)
     op = oracle_params(cfg, rule=rule, vnorm=vnorm, entropy=entropy)
     ws = B.workspace(shape, cap)
     n = st["n"]
@@ -149,3 +150,22 @@ def test_nonrefresh_newcomer_kept_on_position_tie(init):
     np.testing.assert_array_equal(dev["pos"][:, :n_out].cpu().numpy(), oc.pos[:, :n_out])
     np.testing.assert_array_equal(raw_numpy(dev["k"])[:, :, :, :n_out], oc.k[:, :, :, :n_out])
     np.testing.assert_array_equal(raw_numpy(dev["v"])[:, :, :, :n_out], oc.v[:, :, :, :n_out])
+
+
+MERGE_CASES = {
+    "llama8b_reduced": (LLAMA8B.scaled(batch=2, layers=3, prefill_len=1200, budget=120), 4),
+    "llama8b_split_step1": (LLAMA8B.scaled(batch=1, layers=2, prefill_len=6000, budget=600), 3),
+    "qwen_reduced": (QWEN.scaled(batch=2, layers=2, prefill_len=1000, budget=250), 3),
+    "tiny": (TINY, 5),
+}
+
+
+@pytest.mark.parametrize("name,merge,entropy", [
+    ("llama8b_reduced", 2, False), ("llama8b_reduced", 4, True), ("llama8b_reduced", 8, False),
+    ("llama8b_split_step1", 8, False), ("qwen_reduced", 2, False), ("qwen_reduced", 4, True),
+    ("tiny", 2, False)])
+def test_merged_scoring_lockstep(name, merge, entropy):
+    """Scoring workgroups that cover several KV heads of one (layer, sequence) and add their group sums in
+    LDS before writing them (the first step of the split case scores in chunks, one row per KV head)."""
+    cfg, steps = MERGE_CASES[name]
+    run_lockstep(cfg, steps, entropy=entropy, merge=merge)
