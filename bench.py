@@ -30,22 +30,20 @@ METRIC = "evict-steps/sec + achieved HBM GB/s (% peak), 8B shape, 32k ctx, 10% b
 def step_bytes(cfg, n, merge=1):
     """Algorithmic HBM bytes of one refresh step scoring n tokens (n = B + 1 in the steady state).
 
-    score : K rows read once (layers*batch*kv*n*d*2), queries, positions, group-sum scratch r written (4 B per
-            token per (layer, sequence, block of `merge` KV heads whose sums the scorer adds in one workgroup));
-    fold  : r read, u read + written;
-    append: new K/V rows read + written; select: u and pos read; compact: at most one K and one V row per
-            (layer, sequence, KV head) read + written, u/pos entries.
+    score : K rows read once (layers*batch*kv*n*d*2: the n - 1 cached rows and the newcomer's row), queries,
+            positions, group-sum scratch r written (4 B per token per (layer, sequence, block of `merge` KV heads
+            whose sums the scorer adds in one workgroup));
+    fold  : r read, u read + written, positions read (the eviction order's tie-break);
+    place : the newcomer's K/V rows read once and written once into the slot it takes (the append and the
+            compaction's one-row move of a steady step), its utility and position.
     """
     e = 2 if cfg.dtype == "bf16" else 4
     L, b, hq, hkv, d = cfg.layers, cfg.batch, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     rows = hkv // merge
     score = L * b * hkv * n * d * e + L * b * hq * d * e + b * n * 4 + L * b * rows * n * 4
-    fold = L * b * rows * n * 4 + 2 * b * n * 4
-    append = 2 * 2 * L * b * hkv * d * e
-    select = 2 * b * n * 4
-    compact = 2 * 2 * L * b * hkv * d * e + 4 * b * 4
-    return {"score": score, "fold": fold, "append": append, "select": select, "compact": compact,
-            "total": score + fold + append + select + compact}
+    fold = L * b * rows * n * 4 + 3 * b * n * 4
+    place = 2 * 2 * L * b * hkv * d * e + 2 * b * 8
+    return {"score": score, "fold": fold, "place": place, "total": score + fold + place}
 
 
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "score_llama8b_32k_steady_traffic.txt")

@@ -15,7 +15,7 @@ struct Layout {
     int max_pairs;
     ScorePlan plan;
     size_t r_off, z_off, part_off, opart_off, npart_off, vn_off, vinv_off, eta_off, pdst_off, psrc_off, np_off;
-    size_t raw_off, rmask_off, emask_off, kmask_off, tdst_off, tsrc_off, tnp_off, total;
+    size_t raw_off, rmask_off, emask_off, kmask_off, tdst_off, tsrc_off, tnp_off, cand_off, total;
 };
 
 int esize(const kv_shape& s) { return s.dtype == KV_F32 ? 4 : 2; }
@@ -100,6 +100,9 @@ Layout layout_for(const kv_shape& s, int n) {
     off = align256(off + (size_t)s.batch * L.max_pairs * sizeof(int32_t));
     L.tnp_off = off;
     off = align256(off + (size_t)s.batch * sizeof(int32_t));
+    // the fold's per-workgroup eviction candidates of a single-eviction refresh step
+    L.cand_off = off;
+    off = align256(off + (size_t)s.batch * fold_groups(n) * sizeof(EvictCand));
     L.total = off;
     return L;
 }
@@ -159,9 +162,11 @@ ScorePlan scorer_plan(const kv_shape& s, const Layout& L, int variant, int merge
 }
 
 // Scoring (Eq. 1) of rows [0, n) of every layer into the workspace r: [layers][batch][n_kv / merge] rows.
+// k_new (one workgroup per slab only): row n - 1 is the step's newcomer, read from k_new instead of the cache,
+// with position cur_pos.
 kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, const void* k, const int32_t* pos,
                     int cur_pos, float recency_bias, int recency_window, const ScorePlan& splan, void* ws,
-                    hipStream_t st) {
+                    hipStream_t st, const void* k_new = nullptr) {
     ScoreArgs a = score_args(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws);
     ScorePlan plan = splan;
     if (plan.split) {
@@ -181,6 +186,8 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
     a.chunk_rows = plan.chunk_rows;
     a.nchunk = plan.nchunk;
     a.merge = plan.merge;
+    a.k_new = k_new;
+    a.new_pos = cur_pos;
     plan.grid = s.layers * s.batch * (s.n_kv_heads / plan.merge);
     return hip_status(launch_score(s.dtype, s.head_dim, plan, a, st));
 }
@@ -211,11 +218,20 @@ kv_status run_variants(const kv_shape& s, const Layout& L, int n, const void* v,
 }
 
 // Layer fold of the workspace r into u (Eq. 2-4 by `rule`): r_groups rows per (layer, sequence), added in
-// blocks of rblock.
+// blocks of rblock.  Options for single-eviction steps: candidates (each fold workgroup's first token to
+// leave, for launch_place) and new_pos >= 0 (token n - 1 is the newcomer, not yet in u / pos).
+struct FoldExtra {
+    int32_t* pos = nullptr;
+    int new_pos = -1;
+    bool candidates = false;
+};
 kv_status run_fold(const kv_shape& s, const Layout& L, int n, float* u, float* s_out, int rule, float alpha,
                    int variant, int r_groups, int rblock, bool raw_out, void* ws, hipStream_t st,
-                   const kv_trace* tr) {
+                   const kv_trace* tr, const FoldExtra& ex = FoldExtra{}) {
     FoldArgs f{};
+    f.pos = ex.pos;
+    f.new_pos = ex.new_pos;
+    f.cand = ex.candidates ? at<EvictCand>(ws, L.cand_off) : nullptr;
     f.raw = raw_out ? at<float>(ws, L.raw_off) : nullptr;
     f.raw_scale = (float)(1.0 / ((double)s.layers * s.n_q_heads));
     f.r = at<float>(ws, L.r_off);
@@ -413,6 +429,39 @@ kv_status run_select_compact(const kv_shape& s, const Layout& L, int n, int budg
     return rc;
 }
 
+// Placement of the newcomer of a single-eviction refresh step (n <= budget + 1) after a fold with
+// candidates: its K/V rows come from k_new / v_new, or from row n - 1 of the cache when those are null.
+kv_status run_place(const kv_shape& s, const Layout& L, int n, int budget, const void* k_new, const void* v_new,
+                    void* k, void* v, float* u, int32_t* pos, uint8_t* keep_out, void* ws, hipStream_t st) {
+    PlaceArgs a{};
+    a.k = k;
+    a.v = v;
+    a.u = u;
+    a.pos = pos;
+    if (k_new) {
+        a.src_k = k_new;
+        a.src_v = v_new;
+        a.src_slab_rows = 1;
+        a.src_row0 = 0;
+    } else {
+        a.src_k = k;
+        a.src_v = v;
+        a.src_slab_rows = (size_t)s.capacity;
+        a.src_row0 = (size_t)(n - 1);
+    }
+    a.cand = at<EvictCand>(ws, L.cand_off);
+    a.ncand = fold_groups(n);
+    a.keep_out = keep_out;
+    a.batch = s.batch;
+    a.layers = s.layers;
+    a.hkv = s.n_kv_heads;
+    a.cap = s.capacity;
+    a.row_bytes = s.head_dim * esize(s);
+    a.n = n;
+    a.budget = budget;
+    return hip_status(launch_place(a, st));
+}
+
 }  // namespace
 }  // namespace ikv
 
@@ -530,6 +579,37 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
         *n_out = n < p.budget ? n : p.budget;
         return KV_OK;
     }
+    if (refresh && n_in <= p.budget && !rank_trace && !(p.score_variant & KV_SCORE_VNORM)) {
+        const ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
+        if (!plan.split) {
+            // A steady refresh step (one eviction, or none while under budget) in three kernels: the scorer
+            // takes the newcomer from k_new as row n - 1, the fold gives it the refresh prior and reports each
+            // workgroup's first token to leave, and the placement writes the newcomer's rows once, into the
+            // slot it takes (the append's and the compaction's row copies in one).
+            const int r_groups = s.n_kv_heads / plan.merge;
+            record(trace, 0, true, st);
+            record(trace, 0, false, st);
+            record(trace, 1, true, st);
+            rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, plan, ws, st, k_new);
+            if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st);
+            record(trace, 1, false, st);
+            FoldExtra ex;
+            ex.pos = pos;
+            ex.new_pos = new_pos;
+            ex.candidates = n > p.budget;
+            if (rc == KV_OK)
+                rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, r_groups, 1, false, ws, st, trace,
+                              ex);
+            record(trace, 3, true, st);
+            if (rc == KV_OK) rc = run_place(s, L, n, p.budget, k_new, v_new, k, v, u, pos, keep_out, ws, st);
+            record(trace, 3, false, st);
+            record(trace, 4, true, st);
+            record(trace, 4, false, st);
+            if (rc != KV_OK) return rc;
+            *n_out = n < p.budget ? n : p.budget;
+            return KV_OK;
+        }
+    }
     if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, st, trace)) != KV_OK) return rc;
     if (refresh) {
         const ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
@@ -621,6 +701,9 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const bool refresh = is_refresh(p, t);
+    // a refresh step with at most one eviction: the fold reports candidates and one placement kernel takes the
+    // eviction and moves the newcomer (row n - 1, appended by kv_append) into its slot
+    const bool single = refresh && n <= p.budget + 1 && !rank_trace;
     if (refresh) {
         // value norms already written by the step's attention calls: only the entropy factors remain
         const int computed = (p.score_variant & KV_SCORE_NORMS_EMITTED) ? (p.score_variant & ~KV_SCORE_VNORM)
@@ -631,9 +714,19 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
         if ((rc = run_variants(s, L, n, v, computed & (KV_SCORE_VNORM | KV_SCORE_ENTROPY), s.n_kv_heads, rblock,
                                ws, st)) != KV_OK)
             return rc;
+        FoldExtra ex;
+        ex.pos = pos;
+        ex.candidates = single && n > p.budget;
         rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, s.n_kv_heads, rblock,
-                      rank_trace != nullptr, ws, st, nullptr);
+                      rank_trace != nullptr, ws, st, nullptr, ex);
         if (rc != KV_OK) return rc;
+    }
+    if (single) {
+        if (n > p.budget || keep_out)
+            rc = run_place(s, L, n, p.budget, nullptr, nullptr, k, v, u, pos, keep_out, ws, st);
+        if (rc != KV_OK) return rc;
+        *n_out = n < p.budget ? n : p.budget;
+        return KV_OK;
     }
     rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, nullptr);
     if (rc != KV_OK) return rc;

@@ -97,13 +97,7 @@ __global__ __launch_bounds__(kThreads) void append_kernel(AppendArgs a) {
 constexpr int kNrThreads = 1024;
 constexpr int kNrWaves = kNrThreads / kWave;
 
-struct Cand {  // eviction candidate: order key of u, position, slot
-    uint32_t key;
-    int pos, idx;
-};
-__device__ __forceinline__ bool evicts_before(const Cand& a, const Cand& b) {  // a leaves before b
-    return b.idx < 0 || (a.idx >= 0 && (a.key < b.key || (a.key == b.key && a.pos > b.pos)));
-}
+using Cand = EvictCand;
 
 __global__ __launch_bounds__(kNrThreads) void nonrefresh_kernel(AppendArgs a, uint8_t* keep_out, int budget,
                                                                 int* slot_out, int copy_rows) {
@@ -129,8 +123,7 @@ __global__ __launch_bounds__(kNrThreads) void nonrefresh_kernel(AppendArgs a, ui
     for (int o = kWave / 2; o >= 1; o >>= 1) {
         const float w = __shfl_xor(v, o, kWave);
         v = use_min ? fminf(v, w) : v + w;
-        const Cand x{(uint32_t)__shfl_xor((int)c.key, o, kWave), __shfl_xor(c.pos, o, kWave),
-                     __shfl_xor(c.idx, o, kWave)};
+        const Cand x = shfl_xor_cand(c, o);
         if (evicts_before(x, c)) c = x;
     }
     if (lane == 0) {
@@ -217,7 +210,69 @@ __global__ __launch_bounds__(kThreads) void newcomer_rows_kernel(AppendArgs a, c
     reinterpret_cast<u32x4*>(dst)[ch] = reinterpret_cast<const u32x4*>(src)[ch];
 }
 
+// Placement of a refresh step's newcomer after the fold (steady steps: exactly one eviction, or none while
+// the cache is under budget).  Workgroup (l, b): the sequence's single eviction from the fold's candidates
+// (every workgroup of the sequence reduces them the same way), then the newcomer's K and V rows of layer l
+// into its slot; workgroup (0, b) also moves its utility and position, and every workgroup writes its share
+// of the decision.  Reads (candidates, the newcomer's rows at row n - 1 or in k_new / v_new) never overlap
+// writes (rows and entries of the slot < n - 1).
+constexpr int kPlaceThreads = 256;
+
+__global__ __launch_bounds__(kPlaceThreads) void place_kernel(PlaceArgs a) {
+    __shared__ Cand best[kPlaceThreads / kWave];
+    const int l = blockIdx.x, b = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int n = a.n;
+    int evicted = -1;
+    if (n > a.budget) {
+        const Cand* cb = a.cand + (size_t)b * a.ncand;
+        Cand c{0xffffffffu, -1, -1};
+        for (int i = tid; i < a.ncand; i += kPlaceThreads)
+            if (evicts_before(cb[i], c)) c = cb[i];
+#pragma unroll
+        for (int o = kWave / 2; o >= 1; o >>= 1) {
+            const Cand x = shfl_xor_cand(c, o);
+            if (evicts_before(x, c)) c = x;
+        }
+        if (lane == 0) best[wave] = c;
+        __syncthreads();
+        c = best[0];
+        for (int w = 1; w < kPlaceThreads / kWave; ++w)
+            if (evicts_before(best[w], c)) c = best[w];
+        evicted = c.idx;
+    }
+    const int slot = evicted == n - 1 ? -1 : (evicted >= 0 ? evicted : n - 1);
+    if (a.keep_out) {
+        const int per = (n + a.layers - 1) / a.layers;
+        const int i1 = min(n, (l + 1) * per);
+        for (int i = l * per + tid; i < i1; i += kPlaceThreads) a.keep_out[(size_t)b * a.cap + i] = i != evicted;
+    }
+    if (slot < 0) return;
+    if (l == 0 && tid == 0 && slot != n - 1) {
+        a.u[(size_t)b * a.cap + slot] = a.u[(size_t)b * a.cap + n - 1];
+        a.pos[(size_t)b * a.cap + slot] = a.pos[(size_t)b * a.cap + n - 1];
+    }
+    // the source is the cache's own row n - 1 when src_row0 == n - 1 and src is the cache: nothing to move
+    const int lpr = a.row_bytes / 16;
+    const int total = 2 * a.hkv * lpr;  // (tensor, KV head, chunk)
+    for (int c = tid; c < total; c += kPlaceThreads) {
+        const int ch = c % lpr;
+        const int g = (c / lpr) % a.hkv;
+        const int tensor = c / (lpr * a.hkv);
+        const size_t slab = ((size_t)l * a.batch + b) * a.hkv + g;
+        const char* src = static_cast<const char*>(tensor ? a.src_v : a.src_k) +
+                          (slab * a.src_slab_rows + a.src_row0) * a.row_bytes;
+        char* dst = static_cast<char*>(tensor ? a.v : a.k) + (slab * a.cap + slot) * a.row_bytes;
+        if (src != dst) reinterpret_cast<u32x4*>(dst)[ch] = reinterpret_cast<const u32x4*>(src)[ch];
+    }
+}
+
 }  // namespace
+
+hipError_t launch_place(const PlaceArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(place_kernel, dim3(a.layers, a.batch), dim3(kPlaceThreads), 0, s, a);
+    return hipGetLastError();
+}
 
 // Where the newcomer's rows are copied depends on the prior policy.  Under the minimum prior the newcomer
 // ties the lowest utility and, holding the newest position, is normally evicted at once: the decision kernel

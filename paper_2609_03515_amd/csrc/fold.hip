@@ -6,7 +6,9 @@
 // be reduced in parallel.  A workgroup covers 32 tokens of one sequence: each thread reads four consecutive
 // tokens (16-byte loads) of the group sums r of one layer slice (one row per KV head, or per block of KV heads
 // the scorer already added), weights them, and the
-// partial sums of the 32 layer slices are added in a fixed order, so the result is deterministic.
+// partial sums of the 32 layer slices are added in a fixed order, so the result is deterministic.  On request
+// the workgroup also reports the first of its tokens to leave under the single-eviction order (u ascending,
+// position descending), from which the placement kernel takes a steady step's one eviction.
 #include "kernels.h"
 #include "kv_common.h"
 
@@ -72,26 +74,41 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
         partial_raw[slice][quad * 4 + j] = racc[j];
     }
     __syncthreads();
-    if (threadIdx.x < kQuads * 4) {
-        const int tok = blockIdx.x * (kQuads * 4) + threadIdx.x;
-        if (tok < a.n) {
-            float tot = 0.0f;
-            for (int sl = 0; sl < kSlices; ++sl) tot += partial[sl][threadIdx.x];
-            float* up = a.u + (size_t)b * a.cap + tok;
-            *up = fmaf(a.prior_w, *up, tot);
-            if (a.raw) {
-                float rt = 0.0f;
-                for (int sl = 0; sl < kSlices; ++sl) rt += partial_raw[sl][threadIdx.x];
-                a.raw[(size_t)b * a.cap + tok] = rt * a.raw_scale;
-            }
+    if (threadIdx.x >= kWave) return;
+    // wave 0: one token per lane (lanes >= 32 hold none) and the workgroup's eviction candidate
+    EvictCand c{0xffffffffu, -1, -1};
+    const int tok = blockIdx.x * (kQuads * 4) + threadIdx.x;
+    if (threadIdx.x < kQuads * 4 && tok < a.n) {
+        float tot = 0.0f;
+        for (int sl = 0; sl < kSlices; ++sl) tot += partial[sl][threadIdx.x];
+        float* up = a.u + (size_t)b * a.cap + tok;
+        int32_t* pp = a.pos + (size_t)b * a.cap + tok;
+        const bool newcomer = a.new_pos >= 0 && tok == a.n - 1;  // refresh prior 0, position not yet stored
+        const float un = fmaf(a.prior_w, newcomer ? 0.0f : *up, tot);
+        *up = un;
+        if (newcomer) *pp = a.new_pos;
+        if (a.cand) c = EvictCand{float_key(un), newcomer ? a.new_pos : *pp, tok};
+        if (a.raw) {
+            float rt = 0.0f;
+            for (int sl = 0; sl < kSlices; ++sl) rt += partial_raw[sl][threadIdx.x];
+            a.raw[(size_t)b * a.cap + tok] = rt * a.raw_scale;
         }
     }
+    if (!a.cand) return;
+#pragma unroll
+    for (int o = kQuads * 2; o >= 1; o >>= 1) {
+        const EvictCand x = shfl_xor_cand(c, o);
+        if (evicts_before(x, c)) c = x;
+    }
+    if (threadIdx.x == 0) a.cand[(size_t)b * gridDim.x + blockIdx.x] = c;
 }
 
 }  // namespace
 
+int fold_groups(int n) { return (n + kQuads * 4 - 1) / (kQuads * 4); }
+
 hipError_t launch_fold(const FoldArgs& a, hipStream_t s) {
-    dim3 grid((a.n + kQuads * 4 - 1) / (kQuads * 4), a.batch);
+    dim3 grid(fold_groups(a.n), a.batch);
     hipLaunchKernelGGL(fold_kernel, grid, dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }

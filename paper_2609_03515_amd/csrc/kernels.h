@@ -40,6 +40,11 @@ struct ScoreArgs {
     float* npart;   // [layers][batch][n_kv][nchunk]
     int emit_norms;
     int merge;      // scorer: KV heads per workgroup whose group sums are added (r: [layers][batch][n_kv / merge])
+    // scorer (one workgroup per slab): when non-null, row n - 1 of every slab is the step's newcomer, read from
+    // here ([layers][batch][n_kv][d]) instead of the cache (that row of K and of pos is not read), with
+    // position new_pos
+    const void* k_new;
+    int new_pos;
 };
 
 struct ScorePlan {
@@ -87,6 +92,13 @@ hipError_t launch_attend(int dtype, int head_dim, const ScorePlan& plan, const S
 // (max, sum) for launch_split_finish; plan from attend_plan.
 hipError_t launch_score_chunks(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s);
 
+// Eviction candidate of a range of tokens: the token that leaves first under (u ascending, position
+// descending), as the order-preserving key of its utility, its position and its slot (-1: none).
+struct EvictCand {
+    uint32_t key;
+    int pos, idx;
+};
+
 // Layer fold (Eq. 2-4): u <- prior_w * u + sum_l w_l s_l with s_l = (1/H) sum_g r_{l,g}.
 struct FoldArgs {
     const float* r;
@@ -103,9 +115,16 @@ struct FoldArgs {
     int r_groups, rblock;
     float inv_hq;
     float prior_w;
+    // new_pos >= 0: token n - 1 is the step's newcomer, not yet in u / pos: its previous utility is taken as
+    // 0 (the refresh prior) and pos[n - 1] = new_pos is written with its folded utility
+    int new_pos;
+    int32_t* pos;     // positions (read for the candidates, written for the newcomer)
+    EvictCand* cand;  // nullable: [batch][fold_groups(n)] eviction candidate of each workgroup's tokens
     float w[kMaxLayers];
 };
 hipError_t launch_fold(const FoldArgs& a, hipStream_t s);
+// Workgroups of the fold per sequence (each covers a fixed range of tokens and writes one candidate).
+int fold_groups(int n);
 
 // Scorer perturbations (Sec. 5.1): value-row norms with their per-slab mean, and the normalised entropy of
 // each layer's pooled attention, computed from the group sums r.
@@ -180,5 +199,26 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s);
 // eviction and the newcomer's slot (one workgroup per sequence; slot[batch] in device memory), then its rows
 // copied into that slot by a kernel over every (layer, KV head) row.
 hipError_t launch_nonrefresh(const AppendArgs& a, uint8_t* keep_out, int budget, int* slot, hipStream_t s);
+
+// A refresh step on a cache of n - 1 <= budget tokens after the fold: the newcomer (slot n - 1, already folded
+// into u[n - 1] / pos[n - 1]) takes the slot of the single evicted token, the least of the fold's candidates
+// (n = budget + 1), or slot n - 1 when nothing is evicted; it is dropped when it is itself the least.  Its K/V
+// rows are read from src (row src_row0 of slab s at src + (s * src_slab_rows + src_row0) * row_bytes: the
+// step's k_new / v_new, or row n - 1 of the cache) and written into that slot, with its utility and position.
+// One workgroup per (layer, sequence).
+struct PlaceArgs {
+    void* k;
+    void* v;
+    float* u;
+    int32_t* pos;
+    const void* src_k;
+    const void* src_v;
+    size_t src_slab_rows, src_row0;
+    const EvictCand* cand;  // [batch][ncand]
+    uint8_t* keep_out;      // nullable: the decision over the n slots
+    int ncand;
+    int batch, layers, hkv, cap, row_bytes, n, budget;
+};
+hipError_t launch_place(const PlaceArgs& a, hipStream_t s);
 
 }  // namespace ikv

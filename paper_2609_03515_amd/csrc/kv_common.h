@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kernels.h"
+
 namespace ikv {
 
 constexpr int kWave = 64;
@@ -81,6 +83,15 @@ __device__ __forceinline__ MaxSum ms_combine(MaxSum a, MaxSum b) {
 __device__ __forceinline__ uint32_t float_key(float x) {
     const uint32_t b = __float_as_uint(x);
     return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// Eviction order of single-eviction steps: a leaves before b when its utility key is lower, or equal with a
+// higher position (ties keep the lower position); a candidate with idx < 0 is none.
+__device__ __forceinline__ bool evicts_before(const EvictCand& a, const EvictCand& b) {
+    return b.idx < 0 || (a.idx >= 0 && (a.key < b.key || (a.key == b.key && a.pos > b.pos)));
+}
+__device__ __forceinline__ EvictCand shfl_xor_cand(const EvictCand& c, int o) {
+    return EvictCand{(uint32_t)__shfl_xor((int)c.key, o, 64), __shfl_xor(c.pos, o, 64), __shfl_xor(c.idx, o, 64)};
 }
 
 __device__ __forceinline__ float wave_max(float x) {

@@ -55,16 +55,24 @@ void score_lds_kernel(ScoreArgs a) {
     const int nunits = (n + RPW - 1) / RPW;
     // merged group sums after the logits (sized by the plan: the logits' units rounded up to whole iterations)
     float* racc = zs + (size_t)((nunits + kWaves - 1) / kWaves) * kThreads;
-    const __amdgpu_buffer_rsrc_t prs = raw_rsrc(a.pos + (size_t)b * a.cap, n * 4);
+    // with the newcomer given apart, rows [0, n - 1) come from the cache and row n - 1 is substituted into the
+    // buffers of its unit before its logits are taken (the same arithmetic as a cached row)
+    const bool has_new = a.k_new != nullptr;
+    const int cached = n - (has_new ? 1 : 0);
+    const int unit_new = has_new ? (n - 1) / RPW : -1;
+    const __amdgpu_buffer_rsrc_t prs = raw_rsrc(a.pos + (size_t)b * a.cap, cached * 4);
     auto k_rsrc = [&](int g) {
-        return raw_rsrc(static_cast<const T*>(a.k) + ((size_t)lb * a.hkv + g) * a.cap * D, n * L::kRowBytes);
+        return raw_rsrc(static_cast<const T*>(a.k) + ((size_t)lb * a.hkv + g) * a.cap * D, cached * L::kRowBytes);
     };
+    auto new_row = [&](int g) { return static_cast<const T*>(a.k_new) + ((size_t)lb * a.hkv + g) * D; };
 
     if (threadIdx.x < kMaxMerge) next_unit[threadIdx.x] = 0;
     int g = gblk * merge;
     __amdgpu_buffer_rsrc_t krs = k_rsrc(g);
     chunk_t qv[GP][CPL];
+    chunk_t kn[CPL];
     ln.load_q(a, (size_t)lb, g, qv);
+    if (has_new) ln.load_row(new_row(g), kn);
     __syncthreads();
     auto claim = [&](int gi) -> int {
         int u = 0;
@@ -94,6 +102,7 @@ void score_lds_kernel(ScoreArgs a) {
                 ubuf[slot] = claim(gi);
                 ln.load_unit(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
                 if (more && ubuf[j] < nunits) {
+                    if (ubuf[j] == unit_new) ln.put_row(kbuf[j], pbuf[j], kn, a.new_pos, unit_new, n - 1);
                     const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.unit_row(ubuf[j]), n);
                     m = fmaxf(m, z);
                     zs[ubuf[j] * kWave + ln.lane] = z;
@@ -172,7 +181,10 @@ void score_lds_kernel(ScoreArgs a) {
         }
         for (; i < mine; ++i) emit(ln.wave + i * kWaves, group_allsum<GP>(prob(zl[i * kStep])));
         __syncthreads();  // also: every read of this slab's logits is done before the next slab's K pass
-        if (gi + 1 < merge) ln.load_q(a, (size_t)lb, g + 1, qv);
+        if (gi + 1 < merge) {
+            ln.load_q(a, (size_t)lb, g + 1, qv);
+            if (has_new) ln.load_row(new_row(g + 1), kn);
+        }
     }
     // rows [4j, 4j + 4) lie in one unit (RPW is a multiple of 4); rows up to the padded stride are scratch
     const __amdgpu_buffer_rsrc_t rrs = raw_rsrc(a.r + ((size_t)lb * blocks + gblk) * a.n_stride, a.n_stride * 4);

@@ -155,6 +155,24 @@ struct Lane {
         pdst = (int)__builtin_amdgcn_raw_buffer_load_b32(prs, unit_row(u) * 4, 0, 0);
     }
 
+    // This lane's chunks of one row (the row's 16-byte chunks p + c * LPR), e.g. the step's newcomer.
+    __device__ void load_row(const T* row, chunk_t (&dst)[CPL]) const {
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) dst[c] = *reinterpret_cast<const chunk_t*>(row + (p + c * LPR) * EPC);
+    }
+    // Replaces row `row` of unit u in this lane's buffers by `src` (the lanes that hold chunks of it) and its
+    // position by posv (the lanes that own it after the reduce-scatter).
+    __device__ void put_row(chunk_t (&dst)[RPG][CPL], int& pdst, const chunk_t (&src)[CPL], int posv, int u,
+                            int row) const {
+#pragma unroll
+        for (int k = 0; k < RPG; ++k) {
+            const bool here = u * RPW + k * NG + grp == row;
+#pragma unroll
+            for (int c = 0; c < CPL; ++c) dst[k][c] = here ? src[c] : dst[k][c];
+        }
+        if (unit_row(u) == row) pdst = posv;
+    }
+
     // Logit of the (row, head) this lane owns for one iteration; -inf when masked (a padded head, or a row
     // past the end of the range).
     __device__ float logit(const ScoreArgs& a, const chunk_t (&kb)[RPG][CPL], const chunk_t (&qv)[GP][CPL],
