@@ -156,8 +156,8 @@ ScoreArgs score_args(const kv_shape& s, const Layout& L, int n, const void* q, c
 // apart (it weights them per head).
 ScorePlan scorer_plan(const kv_shape& s, const Layout& L, int variant, int merge) {
     ScorePlan plan = L.plan;
-    if (!(variant & KV_SCORE_VNORM))
-        score_merge(&plan, s.dtype, s.head_dim, s.n_kv_heads, s.layers * s.batch, merge);
+    score_merge(&plan, s.dtype, s.head_dim, s.n_kv_heads, s.layers * s.batch,
+                (variant & KV_SCORE_VNORM) ? 1 : merge);
     return plan;
 }
 
@@ -188,7 +188,6 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
     a.merge = plan.merge;
     a.k_new = k_new;
     a.new_pos = cur_pos;
-    plan.grid = s.layers * s.batch * (s.n_kv_heads / plan.merge);
     return hip_status(launch_score(s.dtype, s.head_dim, plan, a, st));
 }
 

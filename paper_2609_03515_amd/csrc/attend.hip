@@ -392,7 +392,7 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
 
 template <typename T, int D, int GP>
 hipError_t launch_attend_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
-    if constexpr (Geometry<T, D, 1>::kLpr < GP) {
+    if constexpr (Geometry<T, D, 1>::kChunks < GP) {
         return hipErrorInvalidValue;
     } else {
         auto kern = attend_kernel<T, D, GP, true>;
@@ -418,7 +418,7 @@ hipError_t launch_attend_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream
 
 template <typename T, int D, int GP>
 hipError_t launch_chunks_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
-    if constexpr (Geometry<T, D, 1>::kLpr < GP) {
+    if constexpr (Geometry<T, D, 1>::kChunks < GP) {
         return hipErrorInvalidValue;
     } else {
         auto kern = attend_kernel<T, D, GP, false>;

@@ -14,27 +14,30 @@
 // r(row) = sum over the group's heads of exp(z - max) / sum.  Slabs too long for one workgroup's LDS (long
 // first steps) are scored in chunks by the attention kernel's K pass (attend.hip), which writes logits and
 // per-chunk (max, sum); the finish kernel below combines them.
+#include <algorithm>
+
 #include "stream_lane.h"
 
 namespace ikv {
 namespace {
 
-// A workgroup scores `merge` consecutive KV heads (slabs) of one (layer, sequence) in turn.  Each slab is cut
-// into units of RPW rows; waves claim units from an LDS counter when they issue the units' loads, so a wave
-// whose loads come back late simply processes fewer units instead of holding the whole workgroup at the
-// barrier (with a static split the last wave finished ~40% after the first).  Logits are stored per unit;
-// after a barrier the epilogue walks the units in a fixed pattern.  With merge > 1 the slabs' group sums are
-// added in LDS (in KV-head order) and written once: one row of r per `merge` KV heads.
-// The merged variant's LDS also holds the sums, so it runs fewer workgroups per CU: it asks for at most the
-// waves of two workgroups per SIMD, which leaves it the registers of the slab loop.
-template <typename T, int D, int GP, bool kMerge>
+// Work items: `merge` consecutive KV heads (slabs) of one (layer, sequence), scored in turn, their group sums
+// added in LDS (in KV-head order) and written once: one row of r per item.  A workgroup takes items
+// blockIdx.x, blockIdx.x + gridDim.x, ... (one item when the grid covers them); the next slab's first loads
+// are issued before each slab's epilogue.  Each slab is cut into units of RPW rows; waves claim units from an LDS counter when they issue
+// the units' loads, so a wave whose loads come back late simply processes fewer units instead of holding the
+// whole workgroup at the barrier (with a static split the last wave finished ~40% after the first).  Logits
+// are stored per unit; after a barrier the epilogue walks the units in a fixed pattern.
+// The multi-slab variant's LDS also holds the item's sums, so it runs fewer workgroups per CU: it asks for at
+// most the waves of two workgroups per SIMD, which leaves it the registers of the slab loop.
+template <typename T, int D, int GP, bool kMulti>
 constexpr int score_waves_per_eu() {
     constexpr int w = Geometry<T, D, GP>::kMinWavesLds;
-    return kMerge && w > 2 * kWaves / 4 ? 2 * kWaves / 4 : w;
+    return kMulti && w > 2 * kWaves / 4 ? 2 * kWaves / 4 : w;
 }
 
-template <typename T, int D, int GP, bool kMerge>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(score_waves_per_eu<T, D, GP, kMerge>())))
+template <typename T, int D, int GP, bool kMulti>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(score_waves_per_eu<T, D, GP, kMulti>())))
 void score_lds_kernel(ScoreArgs a) {
     using L = Lane<T, D, GP>;
     using chunk_t = typename L::chunk_t;
@@ -43,40 +46,46 @@ void score_lds_kernel(ScoreArgs a) {
 
     extern __shared__ float zs[];
     __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
-    __shared__ int next_unit[kMaxMerge];  // one claim counter per slab
+    __shared__ int next_unit[2];  // claim counters of the slab being streamed and of the next one
 
     const L ln;
-    const int merge = kMerge ? a.merge : 1;
-    const int blocks = a.hkv / merge;
-    const int lb = blockIdx.x / blocks;  // l * batch + b
-    const int gblk = blockIdx.x % blocks;
-    const int b = lb % a.batch;
+    const int merge = kMulti ? a.merge : 1;
+    const int blocks = a.hkv / merge;  // items per (layer, sequence)
+    const int items = a.layers * a.batch * blocks;
+    const int nslab = kMulti ? (items - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x * merge : 1;
+    // global slab index (lb * hkv + g) of this workgroup's si-th slab; items are lb * blocks + block
+    auto slab_at = [&](int si) { return ((int)blockIdx.x + si / merge * (int)gridDim.x) * merge + si % merge; };
     const int n = a.n;
     const int nunits = (n + RPW - 1) / RPW;
-    // merged group sums after the logits (sized by the plan: the logits' units rounded up to whole iterations)
+    // item sums after the logits (sized by the plan: the logits' units rounded up to whole iterations)
     float* racc = zs + (size_t)((nunits + kWaves - 1) / kWaves) * kThreads;
     // with the newcomer given apart, rows [0, n - 1) come from the cache and row n - 1 is substituted into the
     // buffers of its unit before its logits are taken (the same arithmetic as a cached row)
     const bool has_new = a.k_new != nullptr;
     const int cached = n - (has_new ? 1 : 0);
     const int unit_new = has_new ? (n - 1) / RPW : -1;
-    const __amdgpu_buffer_rsrc_t prs = raw_rsrc(a.pos + (size_t)b * a.cap, cached * 4);
-    auto k_rsrc = [&](int g) {
-        return raw_rsrc(static_cast<const T*>(a.k) + ((size_t)lb * a.hkv + g) * a.cap * D, cached * L::kRowBytes);
+    auto p_rsrc = [&](int sidx) {
+        return raw_rsrc(a.pos + (size_t)(sidx / a.hkv % a.batch) * a.cap, cached * 4);
     };
-    auto new_row = [&](int g) { return static_cast<const T*>(a.k_new) + ((size_t)lb * a.hkv + g) * D; };
+    auto k_rsrc = [&](int sidx) {
+        return raw_rsrc(static_cast<const T*>(a.k) + (size_t)sidx * a.cap * D, cached * L::kRowBytes);
+    };
+    auto new_row = [&](int sidx) { return static_cast<const T*>(a.k_new) + (size_t)sidx * D; };
+    auto load_slab_consts = [&](int sidx, chunk_t (&qv)[GP][CPL], chunk_t (&kn)[CPL]) {
+        ln.load_q(a, (size_t)(sidx / a.hkv), sidx % a.hkv, qv);
+        if (has_new) ln.load_row(new_row(sidx), kn);
+    };
 
-    if (threadIdx.x < kMaxMerge) next_unit[threadIdx.x] = 0;
-    int g = gblk * merge;
-    __amdgpu_buffer_rsrc_t krs = k_rsrc(g);
+    if (threadIdx.x < 2) next_unit[threadIdx.x] = 0;
+    int sidx = slab_at(0);
+    __amdgpu_buffer_rsrc_t krs = k_rsrc(sidx), prs = p_rsrc(sidx);
     chunk_t qv[GP][CPL];
     chunk_t kn[CPL];
-    ln.load_q(a, (size_t)lb, g, qv);
-    if (has_new) ln.load_row(new_row(g), kn);
+    load_slab_consts(sidx, qv, kn);
     __syncthreads();
-    auto claim = [&](int gi) -> int {
+    auto claim = [&](int si) -> int {
         int u = 0;
-        if (ln.lane == 0) u = atomicAdd(&next_unit[gi], 1);
+        if (ln.lane == 0) u = atomicAdd(&next_unit[si & 1], 1);
         return __builtin_amdgcn_readfirstlane(u);
     };
 
@@ -84,22 +93,23 @@ void score_lds_kernel(ScoreArgs a) {
     // every path (claims past the end read zeros), so the wait before a reduction covers only its own buffer.
     chunk_t kbuf[kNbuf][RPG][CPL];
     int pbuf[kNbuf], ubuf[kNbuf];
-    auto prime = [&](int gi) {
+    auto prime = [&](int si) {
 #pragma unroll
         for (int j = 0; j < kNbuf - 1; ++j) {
-            ubuf[j] = claim(gi);
+            ubuf[j] = claim(si);
             ln.load_unit(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
         }
     };
     prime(0);
-    for (int gi = 0; gi < merge; ++gi, ++g) {
+    for (int si = 0; si < nslab; ++si) {
+        const int gi = si % merge;  // position of the slab in its item
         float m = kFloor;
         bool more = true;
         while (more) {
 #pragma unroll
             for (int j = 0; j < kNbuf; ++j) {
                 const int slot = (j + kNbuf - 1) % kNbuf;
-                ubuf[slot] = claim(gi);
+                ubuf[slot] = claim(si);
                 ln.load_unit(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
                 if (more && ubuf[j] < nunits) {
                     if (ubuf[j] == unit_new) ln.put_row(kbuf[j], pbuf[j], kn, a.new_pos, unit_new, n - 1);
@@ -111,9 +121,12 @@ void score_lds_kernel(ScoreArgs a) {
                 }
             }
         }
-        if (gi + 1 < merge) {  // the next slab's first loads overlap this slab's epilogue
-            krs = k_rsrc(g + 1);
-            prime(gi + 1);
+        const int item = slab_at(si) / merge;
+        if (si + 1 < nslab) {  // the next slab's first loads overlap this slab's epilogue
+            sidx = slab_at(si + 1);
+            krs = k_rsrc(sidx);
+            prs = p_rsrc(sidx);
+            prime(si + 1);
         }
 
         // epilogue: per-head softmax statistics, then normalised group sums.  Thread (wave w, lane) visits
@@ -125,6 +138,9 @@ void score_lds_kernel(ScoreArgs a) {
         for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
         if (ln.lane < GP) red_m[ln.wave][ln.lane] = m;
         __syncthreads();
+        // every wave has left this slab's claims: its counter is free for the slab after next (primed only
+        // after the barrier that ends this epilogue)
+        if (threadIdx.x == 0) next_unit[si & 1] = 0;
         m = red_m[0][ln.hh];
 #pragma unroll
         for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][ln.hh]);
@@ -156,14 +172,14 @@ void score_lds_kernel(ScoreArgs a) {
         for (int w = 1; w < kWaves; ++w) tot += red_s[w][ln.hh];
         const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
         auto prob = [&](float e) { return e * inv; };
-        // group sum of the normalised probabilities of each row.  One slab: staged by one lane per row in the
-        // first RPW words of the row's unit block (only this wave reads that block, and it has already read
-        // the words) for the coalesced store below.  Several: added to the row's merged sum.
+        // group sum of the normalised probabilities of each row.  One slab per workgroup: staged by one lane per
+        // row in the first RPW words of the row's unit block (only this wave reads that block, and it has
+        // already read the words) for the coalesced store below.  Several: added to the row's item sum.
         static_assert(RPW % 4 == 0, "the coalesced store moves 4 rows at a time");
         auto emit = [&](int unit, float sum) {
             if (ln.hh == 0) {
                 const int row = ln.kk * L::NG + ln.grp;
-                if (merge == 1) {
+                if (!kMulti) {
                     zs[unit * kWave + row] = sum;
                 } else {
                     float* acc = racc + unit * RPW + row;
@@ -181,17 +197,18 @@ void score_lds_kernel(ScoreArgs a) {
         }
         for (; i < mine; ++i) emit(ln.wave + i * kWaves, group_allsum<GP>(prob(zl[i * kStep])));
         __syncthreads();  // also: every read of this slab's logits is done before the next slab's K pass
-        if (gi + 1 < merge) {
-            ln.load_q(a, (size_t)lb, g + 1, qv);
-            if (has_new) ln.load_row(new_row(g + 1), kn);
+        if (gi == merge - 1) {
+            // the item is complete: its row of r.  Rows [4j, 4j + 4) lie in one unit (RPW is a multiple of 4);
+            // rows up to the padded stride are scratch.  The next item's sums are written only after the next
+            // epilogue's first barrier, when every thread has issued these stores.
+            const __amdgpu_buffer_rsrc_t rrs = raw_rsrc(a.r + (size_t)item * a.n_stride, a.n_stride * 4);
+            for (int j = threadIdx.x; j * 4 < n; j += kThreads) {
+                const int row = j * 4;
+                const float* src = !kMulti ? &zs[(row / RPW) * kWave + row % RPW] : &racc[row];
+                store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(src));
+            }
         }
-    }
-    // rows [4j, 4j + 4) lie in one unit (RPW is a multiple of 4); rows up to the padded stride are scratch
-    const __amdgpu_buffer_rsrc_t rrs = raw_rsrc(a.r + ((size_t)lb * blocks + gblk) * a.n_stride, a.n_stride * 4);
-    for (int j = threadIdx.x; j * 4 < n; j += kThreads) {
-        const int row = j * 4;
-        const float* src = merge == 1 ? &zs[(row / RPW) * kWave + row % RPW] : &racc[row];
-        store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(src));
+        if (si + 1 < nslab) load_slab_consts(sidx, qv, kn);
     }
 }
 
@@ -236,23 +253,26 @@ __global__ __launch_bounds__(kFinishThreads) void split_finish_kernel(ScoreArgs 
 
 template <typename T, int D, int GP>
 hipError_t launch_lds(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
-    auto kern = a.merge > 1 ? score_lds_kernel<T, D, GP, true> : score_lds_kernel<T, D, GP, false>;
+    const int items = a.layers * a.batch * (a.hkv / a.merge);
+    const bool multi = a.merge > 1 || (plan.grid > 0 && plan.grid < items);
+    auto kern = multi ? score_lds_kernel<T, D, GP, true> : score_lds_kernel<T, D, GP, false>;
     if (plan.lds_bytes > 64 * 1024) {
         static bool raised[2] = {false, false};  // idempotent attribute; a benign race between threads
-        if (!raised[a.merge > 1]) {
+        if (!raised[multi]) {
             hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax);
             if (e != hipSuccess) return e;
-            raised[a.merge > 1] = true;
+            raised[multi] = true;
         }
     }
-    hipLaunchKernelGGL(kern, dim3(a.layers * a.batch * (a.hkv / a.merge)), dim3(kThreads), plan.lds_bytes, s, a);
+    const int grid = plan.grid > 0 && plan.grid < items ? plan.grid : items;
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), plan.lds_bytes, s, a);
     return hipGetLastError();
 }
 
 template <typename T, int D, int GP>
 hipError_t launch_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
-    if constexpr (Geometry<T, D, 1>::kLpr < GP) {
+    if constexpr (Geometry<T, D, 1>::kChunks < GP) {
         return hipErrorInvalidValue;
     } else {
         if (!plan.split) return launch_lds<T, D, GP>(plan, a, s);
@@ -260,17 +280,17 @@ hipError_t launch_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
     }
 }
 
-// Workgroups of the merged variant one CU holds by its registers (0 when the query fails); cached per
-// instance (a benign race: every thread computes the same value).
-template <typename T, int D, int GP>
-int merged_occupancy() {
-    if constexpr (Geometry<T, D, 1>::kLpr < GP) {
+// Workgroups of the single-slab (kMulti false) or multi-slab variant one CU holds by its registers (0 when
+// the query fails); cached per instance (a benign race: every thread computes the same value).
+template <typename T, int D, int GP, bool kMulti>
+int kernel_occupancy() {
+    if constexpr (Geometry<T, D, 1>::kChunks < GP) {
         return 0;
     } else {
         static int occ = -1;
         if (occ < 0) {
             int v = 0;
-            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, score_lds_kernel<T, D, GP, true>, kThreads, 0) !=
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, score_lds_kernel<T, D, GP, kMulti>, kThreads, 0) !=
                 hipSuccess)
                 v = 0;
             occ = v;
@@ -280,20 +300,20 @@ int merged_occupancy() {
 }
 
 template <typename T, int D>
-int merged_occupancy_d(int gp) {
+int occupancy_d(int gp, bool multi) {
     switch (gp) {
-        case 1: return merged_occupancy<T, D, 1>();
-        case 2: return merged_occupancy<T, D, 2>();
-        case 4: return merged_occupancy<T, D, 4>();
-        case 8: return merged_occupancy<T, D, 8>();
-        case 16: return merged_occupancy<T, D, 16>();
+        case 1: return multi ? kernel_occupancy<T, D, 1, true>() : kernel_occupancy<T, D, 1, false>();
+        case 2: return multi ? kernel_occupancy<T, D, 2, true>() : kernel_occupancy<T, D, 2, false>();
+        case 4: return multi ? kernel_occupancy<T, D, 4, true>() : kernel_occupancy<T, D, 4, false>();
+        case 8: return multi ? kernel_occupancy<T, D, 8, true>() : kernel_occupancy<T, D, 8, false>();
+        case 16: return multi ? kernel_occupancy<T, D, 16, true>() : kernel_occupancy<T, D, 16, false>();
         default: return 0;
     }
 }
 
-int merged_occupancy(int dtype, int head_dim, int gp) {
-    if (dtype == 0) return head_dim == 64 ? merged_occupancy_d<float, 64>(gp) : merged_occupancy_d<float, 128>(gp);
-    return head_dim == 64 ? merged_occupancy_d<bf16_t, 64>(gp) : merged_occupancy_d<bf16_t, 128>(gp);
+int kernel_occupancy(int dtype, int head_dim, int gp, bool multi) {
+    if (dtype == 0) return head_dim == 64 ? occupancy_d<float, 64>(gp, multi) : occupancy_d<float, 128>(gp, multi);
+    return head_dim == 64 ? occupancy_d<bf16_t, 64>(gp, multi) : occupancy_d<bf16_t, 128>(gp, multi);
 }
 
 template <typename T, int D>
@@ -342,31 +362,51 @@ bool score_plan(int dtype, int head_dim, int group, int n, ScorePlan* plan) {
     return true;
 }
 
+// Schedule of the LDS-resident scorer: how many consecutive KV heads of one (layer, sequence) one workgroup
+// scores in turn (merge m, a divisor of hkv up to kMaxMerge; `forced` > 0: that one), one item of m slabs per
+// workgroup.  The hardware hands items to CUs as slots free up, so the busiest CU streams
+// ceil(items / CUs) x m slabs: the cost to minimise.  Ties go to (1) two or more workgroups per CU (one hides
+// less latency) and (2) the larger merge: the group sums written while K still streams cost far more than
+// their bytes, and a multi-slab workgroup issues the next slab's first loads before each epilogue.  Measured at
+// the 8B steady step (2,048 slabs, all costs 8): m = 4 285.5 us, m = 2 291.7, m = 8 (one workgroup per CU)
+// 295.0, m = 1 302.8; at the Qwen-shaped step (3,584 slabs): m = 2 (cost 14) 327 us, m = 1 (14) 347, m = 4
+// (16) 347.
 int score_merge(ScorePlan* plan, int dtype, int head_dim, int hkv, int lb_count, int forced) {
     plan->merge = 1;
-    if (plan->split || hkv < 2) return 1;
-    const size_t racc = (size_t)plan->chunk_rows * sizeof(float);  // the merged sums
-    if (plan->lds_bytes + racc > kFastLdsMax) return 1;
+    plan->grid = 0;
+    if (plan->split) return 1;
+    const size_t racc = (size_t)plan->chunk_rows * sizeof(float);  // an item's sums
+    const size_t lds1 = plan->lds_bytes, ldsm = lds1 + racc;
     int best = 1;
     if (forced > 0) {
         best = forced;
     } else {
-        // Writing the group sums while the grid still streams K costs far more than their bytes, so KV heads
-        // of one (layer, sequence) share a workgroup and add their sums in LDS when that still fills the chip:
-        // the largest merge (a divisor of hkv) whose grid gives every CU as many workgroups as it holds (by LDS
-        // and by registers).
-        const int reg_per_cu = merged_occupancy(dtype, head_dim, plan->group_pad);
         int dev = 0, cus = 0;
-        if (reg_per_cu < 1 || hipGetDevice(&dev) != hipSuccess ||
+        const int occ1 = kernel_occupancy(dtype, head_dim, plan->group_pad, false);
+        const int occm = ldsm <= kFastLdsMax ? kernel_occupancy(dtype, head_dim, plan->group_pad, true) : 0;
+        if (occ1 < 1 || hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
             return 1;
-        size_t per_cu = kLdsPerCu / (plan->lds_bytes + racc);
-        if (per_cu > (size_t)reg_per_cu) per_cu = reg_per_cu;
-        for (int m = 2; m <= kMaxMerge && m <= hkv; ++m)
-            if (hkv % m == 0 && (size_t)lb_count * (hkv / m) >= per_cu * (size_t)cus) best = m;
+        long best_cost = -1;
+        bool best_conc = false;
+        for (int m = 1; m <= kMaxMerge && m <= hkv; ++m) {
+            if (hkv % m || (m > 1 && occm < 1)) continue;
+            const long items = (long)lb_count * (hkv / m);
+            const long per_cu = m == 1 ? std::min<long>((long)(kLdsPerCu / lds1), occ1)
+                                       : std::min<long>((long)(kLdsPerCu / ldsm), occm);
+            const long on_cu = (items + cus - 1) / cus;  // items of the busiest CU
+            const long cost = on_cu * m;
+            const bool conc = std::min(per_cu, on_cu) >= 2;
+            if (best_cost < 0 || cost < best_cost || (cost == best_cost && conc >= best_conc)) {
+                best_cost = cost;
+                best_conc = conc;
+                best = m;
+            }
+        }
     }
+    if (best > 1 && ldsm > kFastLdsMax) best = 1;  // the item sums do not fit beside the logits
     plan->merge = best;
-    if (best > 1) plan->lds_bytes += racc;
+    if (best > 1) plan->lds_bytes = ldsm;
     return best;
 }
 
