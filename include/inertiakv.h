@@ -107,7 +107,9 @@ typedef struct {
 
 /* Optional timing hooks: when an entry is non-NULL, kv_evict_step records that hipEvent_t on its stream
  * immediately before (begin) / after (end) the kernels of the phase.  Phases: 0 append, 1 score, 2 fold,
- * 3 select, 4 compact. */
+ * 3 select, 4 compact.  On a refresh step over a cache of at most B tokens (without VNorm or a rank trace) the
+ * newcomer is scored from k_new and written once, into the slot it takes: phase 3 then times the selection
+ * with that placement, and phases 0 and 4 record their events back to back. */
 #define KV_PHASES 5
 typedef struct {
     void* begin[KV_PHASES];
