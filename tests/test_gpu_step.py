@@ -74,6 +74,9 @@ CASES = {
     # Lazy steps that first only append (cache under budget), then evict one token each
     "lazy_under_budget": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=40, budget=44, nonrefresh_init="mean"), 9),
     "lazy_under_budget_min": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=40, budget=44), 9),
+    # an empty cache: the first refresh steps score only the newcomer (no cached row is read), then evict
+    "empty_start": (TINY.scaled(prefill_len=0, budget=3), 8),
+    "lazy_empty_start": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=0, budget=4, nonrefresh_init="mean"), 10),
 }
 
 
@@ -169,3 +172,34 @@ def test_merged_scoring_lockstep(name, merge, entropy):
     LDS before writing them (the first step of the split case scores in chunks, one row per KV head)."""
     cfg, steps = MERGE_CASES[name]
     run_lockstep(cfg, steps, entropy=entropy, merge=merge)
+
+
+@pytest.mark.parametrize("cfg", [LLAMA8B.scaled(batch=2, layers=3, prefill_len=300, budget=60),
+                                 QWEN.scaled(batch=3, layers=2, prefill_len=200, budget=50)],
+                         ids=["llama8b_reduced", "qwen_reduced"])
+def test_steps_without_keep_out_leave_identical_caches(cfg):
+    """kv_evict_step with and without keep_out (the benchmark's call) leaves bit-identical caches, utilities and
+    positions: the decision writes are the only difference between the two launches."""
+    w = Workload(cfg)
+    cap = cfg.prefill_len + 1
+    st = to_device(w.prefill(capacity=cap))
+    other = {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in st.items()}
+    shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
+    params = B.make_params(cfg.alpha, cfg.budget, 1, False, "mean", cfg.recency_bias, cfg.recency_window)
+    ws = B.workspace(shape, cap)
+    n1 = n2 = st["n"]
+    for t in range(1, 7):
+        sig = to_device(w.step_inputs(t))
+        keep = torch.zeros(cfg.batch, cap, dtype=torch.uint8, device="cuda")
+        n1 = B.kv_evict_step(shape, params, t, n1, sig["new_pos"], sig["q"], sig["k_new"], sig["v_new"], st["k"],
+                             st["v"], st["u"], st["pos"], ws, keep_out=keep)
+        n2 = B.kv_evict_step(shape, params, t, n2, sig["new_pos"], sig["q"], sig["k_new"], sig["v_new"],
+                             other["k"], other["v"], other["u"], other["pos"], ws)
+        torch.cuda.synchronize()
+        assert n1 == n2 == min(cfg.budget, (cfg.prefill_len if t == 1 else cfg.budget) + 1)
+        assert int(keep[:, : (cfg.prefill_len if t == 1 else cfg.budget) + 1].sum()) == cfg.batch * n1
+        for name in ("u", "pos"):
+            assert torch.equal(st[name][:, :n1], other[name][:, :n1]), (t, name)
+        for name in ("k", "v"):
+            assert torch.equal(st[name][:, :, :, :n1], other[name][:, :, :, :n1]), (t, name)
+        print(f"{cfg.name} t={t}: identical with and without keep_out", flush=True)
