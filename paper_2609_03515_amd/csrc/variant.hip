@@ -14,10 +14,11 @@ namespace {
 constexpr int kVThreads = 512;
 
 // One workgroup per (layer, sequence, KV head) slab: a value row is read as 16-byte chunks by an aligned
-// group of LPR lanes, kRows rows per lane and pass; the next pass's loads are issued before the current pass
-// is reduced (raw buffer loads over the slab's live rows: reads past the end return zero and are not
-// stored).  The sum of squares is reduced over the lane group with DPP, the group's first lane stores the
-// norm, and the norms are summed in a fixed order for the mean.
+// group of LPR lanes; a wave covers kRows x (64 / LPR) consecutive rows per pass, and the next pass's loads are
+// issued before the current pass is reduced (raw buffer loads over the slab's live rows: reads past the end
+// return zero and are not stored).  The sum of squares is reduced over the lane group with DPP; the wave's
+// norms are gathered in its own LDS row and written as 16-byte stores (one per four rows instead of one 4-byte
+// store per row, while V streams), and summed in a fixed order for the mean.
 constexpr int kRows = 4;
 
 template <typename T, int D>
@@ -25,15 +26,23 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
     using E = Elem<T>;
     using chunk_t = typename E::chunk_t;
     constexpr int EPC = E::kPerChunk, CH = D / EPC, LPR = CH >= 16 ? 16 : CH, CPL = CH / LPR;
-    constexpr int RPI = kVThreads / LPR;  // rows per pass and row slot
+    constexpr int GPW = kWave / LPR;             // row groups per wave
+    constexpr int RPW = GPW * kRows;              // consecutive rows per wave and pass
+    constexpr int kWavesV = kVThreads / kWave;
+    constexpr int kPass = kWavesV * RPW;          // rows per pass
     constexpr int kRowBytes = D * (int)sizeof(T);
-    __shared__ float part[kVThreads / kWave];
+    static_assert(RPW % 4 == 0, "16-byte norm stores");
+    __shared__ float part[kWavesV];
+    __shared__ float stage[kWavesV][RPW];
     const size_t slab = blockIdx.x;
     const __amdgpu_buffer_rsrc_t vrs =
         raw_rsrc(static_cast<const T*>(a.v) + slab * a.cap * D, a.n * kRowBytes);
-    const int p = threadIdx.x % LPR;
-    const int rsub = threadIdx.x / LPR;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int p = lane % LPR;
+    const int grp = lane / LPR;
     const __amdgpu_buffer_rsrc_t out = raw_rsrc(a.vnorm + slab * a.n_stride, a.n_stride * 4);
+    // row of (pass base, k) for this lane: the wave's block, then k-major, row groups innermost
+    auto row_of = [&](int base, int k) { return base + wave * RPW + k * GPW + grp; };
     auto load = [&](int base, chunk_t (&c)[kRows][CPL]) {
 #pragma unroll
         for (int k = 0; k < kRows; ++k)
@@ -41,7 +50,7 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
             for (int cc = 0; cc < CPL; ++cc)
                 c[k][cc] = __builtin_bit_cast(
                     chunk_t, __builtin_amdgcn_raw_buffer_load_b128(
-                                 vrs, (base + k * RPI + rsub) * kRowBytes + (p + cc * LPR) * 16, 0, kNonTemporal));
+                                 vrs, row_of(base, k) * kRowBytes + (p + cc * LPR) * 16, 0, kNonTemporal));
     };
     float sum = 0.0f;
     auto reduce = [&](int base, const chunk_t (&c)[kRows][CPL]) {
@@ -56,15 +65,20 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
                 for (int x = 0; x < EPC; ++x) ss = fmaf(f[x], f[x], ss);
             }
             ss = group_allsum<LPR>(ss);  // DPP inside the row's aligned lane group
-            const int row = base + k * RPI + rsub;
-            if (row < a.n && p == 0) {
-                const float nrm = sqrtf(ss);
-                store_stream(out, row * 4, nrm);  // written while V streams: streaming-result policy
+            const int row = row_of(base, k);
+            if (p == 0) {
+                const float nrm = row < a.n ? sqrtf(ss) : 0.0f;
+                stage[wave][k * GPW + grp] = nrm;
                 sum += nrm;
             }
         }
+        // the wave's RPW consecutive norms, 4 per lane (a group starting below n ends inside the padded stride,
+        // a multiple of 64); the wave's own LDS row, so only the wave's order matters
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        const int first = base + wave * RPW;
+        if (lane * 4 < RPW && first + lane * 4 < a.n)
+            store_stream(out, (first + lane * 4) * 4, *reinterpret_cast<const f32x4*>(&stage[wave][lane * 4]));
     };
-    constexpr int kPass = RPI * kRows;
     chunk_t c0[kRows][CPL], c1[kRows][CPL];
     load(0, c0);
     for (int base = 0; base < a.n; base += 2 * kPass) {  // uniform trip count: every lane joins the DPP sums
@@ -75,11 +89,11 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
     }
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) sum += __shfl_xor(sum, o, kWave);
-    if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = sum;
+    if (lane == 0) part[wave] = sum;
     __syncthreads();
     if (threadIdx.x == 0) {
         float tot = 0.0f;
-        for (int w = 0; w < kVThreads / kWave; ++w) tot += part[w];
+        for (int w = 0; w < kWavesV; ++w) tot += part[w];
         a.vnorm_inv_mean[slab] = tot > 0.0f ? (float)a.n / tot : 0.0f;
     }
 }
