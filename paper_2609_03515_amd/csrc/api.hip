@@ -18,6 +18,10 @@ namespace {
 #define IKV_SPLIT_LOGIT_MIB 160
 #endif
 constexpr size_t kSplitLogitBytes = (size_t)IKV_SPLIT_LOGIT_MIB << 20;
+#ifndef IKV_COOP_SPLIT
+#define IKV_COOP_SPLIT 1
+#endif
+constexpr bool kCoopSplit = IKV_COOP_SPLIT != 0;
 
 struct Layout {
     int n_stride;
@@ -179,9 +183,29 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
     ScoreArgs a = score_args(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws);
     ScorePlan plan = splan;
     if (plan.split) {
-        // long slabs: LDS-resident chunks of the attention kernel's K pass, then the finish kernel, for groups
-        // of layers whose logits fit kSplitLogitBytes (read back while they may still be cached)
         const int group = s.n_q_heads / s.n_kv_heads;
+        // long slabs: chunks that exchange their softmax statistics and write the group sums directly, on a
+        // grid the device holds at once
+        ScorePlan xp;
+        if (kCoopSplit &&
+            attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &xp, kScoreChunkLds) &&
+            xp.split && xp.nchunk * xp.group_pad <= kCoopMaxWords) {
+            const long slabs = (long)s.layers * s.batch * s.n_kv_heads;
+            long grid = coop_workgroups(s.dtype, s.head_dim, xp) / xp.nchunk * xp.nchunk;
+            if (grid > slabs * xp.nchunk) grid = slabs * xp.nchunk;
+            if (grid >= xp.nchunk &&
+                (size_t)s.layers * s.batch * s.n_q_heads * xp.nchunk * sizeof(uint64_t) <= L.opart_off - L.part_off) {
+                a.v = k;
+                a.chunk_rows = xp.chunk_rows;
+                a.nchunk = xp.nchunk;
+                a.emit = 1;
+                return hip_status(launch_score_coop(s.dtype, s.head_dim, xp, a, at<uint64_t>(ws, L.part_off),
+                                                    (int)grid, st));
+            }
+        }
+        // otherwise LDS-resident chunks of the attention kernel's K pass that write logits, then the finish
+        // kernel, for groups of layers whose logits fit kSplitLogitBytes (read back while they may still be
+        // cached)
         const size_t layer_logits = (size_t)s.batch * s.n_q_heads * L.n_stride * sizeof(float);
         const size_t fit = kSplitLogitBytes / layer_logits;
         const int lg = fit < 1 ? 1 : (fit > (size_t)s.layers ? s.layers : (int)fit);

@@ -91,6 +91,14 @@ hipError_t launch_attend(int dtype, int head_dim, const ScorePlan& plan, const S
 // Scoring of long slabs in LDS-resident chunks (the attention kernel without its V pass): logits and per-chunk
 // (max, sum) for launch_split_finish; plan from attend_plan.
 hipError_t launch_score_chunks(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s);
+// Scoring of long slabs in chunks that exchange their softmax statistics instead of writing logits: plan
+// (chunk_rows, nchunk, lds_bytes) from attend_plan with at most kCoopMaxWords / group_pad chunks; grid = a
+// multiple of nchunk no larger than coop_workgroups() (the workgroups the device holds at once).  xchg: zeroed
+// here, then one 64-bit word per (layer, sequence, query head, chunk).
+constexpr int kCoopMaxWords = 4 * 64;
+int coop_workgroups(int dtype, int head_dim, const ScorePlan& plan);
+hipError_t launch_score_coop(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg,
+                             int grid, hipStream_t s);
 
 // Eviction candidate of a range of tokens: the token that leaves first under (u ascending, position
 // descending), as the order-preserving key of its utility, its position and its slot (-1: none).

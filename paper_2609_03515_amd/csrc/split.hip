@@ -1,0 +1,337 @@
+// Scoring of slabs too long for one workgroup's LDS (first decode steps: a 32k- or 128k-token prefill), Eq. 1
+// over chunks of a slab whose logits stay in LDS.
+//
+// Each chunk needs the softmax statistics of the whole slab: per query head, the maximum M and the sum S of
+// exp(z - M) over every chunk.  The chunks of a slab therefore exchange their own (max, sum) pairs: each pair is
+// one 64-bit word (max bits high, sum bits low) written with a single device-scope atomic store, so a reader
+// that sees the word sees both halves, and a chunk's sum is at least 1 (its maximum contributes exp(0)), so a
+// zero word means "not written yet".  No other data crosses workgroups, so no fence is needed.  A workgroup then
+// scales its chunk's exponentials by exp(m - M) / S and writes the chunk's group sums r directly: no logits
+// round trip through memory.
+//
+// The grid is persistent and no larger than the workgroups the chip holds at once: workgroup w always takes
+// chunk w % C of slabs w / C, w / C + P, ... (P = grid / C slabs per round), so the C chunks of a slab are
+// consecutive workgroups that are dispatched together and only ever wait for one another.  Every wait is
+// bounded (kSpinLimit sleeps); the exchange words are zeroed by a fill kernel before each launch.
+#include <algorithm>
+
+#include "stream_lane.h"
+
+namespace ikv {
+namespace {
+
+constexpr int kSpinLimit = 1 << 22;  // 64-clock sleeps: about 0.1 s, far beyond any chunk's streaming time
+constexpr int kMaxWords = 4;         // exchange words per lane: chunks x padded group <= 256
+
+__device__ __forceinline__ uint64_t pack_ms(float m, float s) {
+    return ((uint64_t)__float_as_uint(m) << 32) | (uint64_t)__float_as_uint(s);
+}
+
+template <typename T, int D, int GP>
+constexpr int coop_waves_per_eu() {
+    return Geometry<T, D, GP>::kMinWavesLds;
+}
+
+template <typename T, int D, int GP>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(coop_waves_per_eu<T, D, GP>())))
+void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round) {
+    using L = Lane<T, D, GP>;
+    using chunk_t = typename L::chunk_t;
+    constexpr int RPG = L::RPG, CPL = L::CPL, RPW = L::RPW;
+    constexpr int kNbuf = Geometry<T, D, GP>::kNbufLds;
+
+    extern __shared__ float zs[];
+    __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
+    __shared__ float fh[GP];
+    __shared__ int next_unit[2];
+
+    const L ln;
+    const int n = a.n, C = a.nchunk;
+    const int slabs = a.layers * a.batch * a.hkv;
+    const int cw = blockIdx.x % C;  // this workgroup's chunk of every slab it scores
+    const int row0 = cw * a.chunk_rows;
+    const int rows = min(a.chunk_rows, n - row0);
+    const int nunits = (rows + RPW - 1) / RPW;
+    auto k_rsrc = [&](int slab) {
+        return raw_rsrc(static_cast<const T*>(a.k) + ((size_t)slab * a.cap + row0) * D, rows * L::kRowBytes);
+    };
+    auto p_rsrc = [&](int slab) {
+        return raw_rsrc(a.pos + (size_t)(slab / a.hkv % a.batch) * a.cap + row0, rows * 4);
+    };
+
+    int slab = (int)blockIdx.x / C;
+    if (slab >= slabs) return;
+    if (threadIdx.x < 2) next_unit[threadIdx.x] = 0;
+    __amdgpu_buffer_rsrc_t krs = k_rsrc(slab), prs = p_rsrc(slab);
+    chunk_t qv[GP][CPL];
+    ln.load_q(a, (size_t)(slab / a.hkv), slab % a.hkv, qv);
+    __syncthreads();
+    auto claim = [&](int si) -> int {
+        int u = 0;
+        if (ln.lane == 0) u = atomicAdd(&next_unit[si & 1], 1);
+        return __builtin_amdgcn_readfirstlane(u);
+    };
+    chunk_t kbuf[kNbuf][RPG][CPL];
+    int pbuf[kNbuf], ubuf[kNbuf];
+    auto prime = [&](int si) {
+#pragma unroll
+        for (int j = 0; j < kNbuf - 1; ++j) {
+            ubuf[j] = claim(si);
+            ln.load_unit(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
+        }
+    };
+    prime(0);
+    for (int si = 0;; ++si) {
+        const int cur = slab;
+        float m = kFloor;
+        bool more = true;
+        while (more) {
+#pragma unroll
+            for (int j = 0; j < kNbuf; ++j) {
+                const int slot = (j + kNbuf - 1) % kNbuf;
+                ubuf[slot] = claim(si);
+                ln.load_unit(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
+                if (more && ubuf[j] < nunits) {
+                    const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.unit_row(ubuf[j]), rows);
+                    m = fmaxf(m, z);
+                    zs[ubuf[j] * kWave + ln.lane] = z;
+                } else {
+                    more = false;
+                }
+            }
+        }
+        slab += slabs_per_round;
+        const bool next = slab < slabs;
+        if (next) {  // the next slab's first loads overlap this chunk's epilogue and exchange
+            krs = k_rsrc(slab);
+            prs = p_rsrc(slab);
+            prime(si + 1);
+        }
+
+        // the chunk's per-head maximum and sum of exponentials (exponentials kept in LDS)
+        float* zl = zs + ln.wave * kWave + ln.lane;
+        constexpr int kStep = kWaves * kWave;
+        const int mine = nunits > ln.wave ? (nunits - ln.wave + kWaves - 1) / kWaves : 0;
+#pragma unroll
+        for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+        if (ln.lane < GP) red_m[ln.wave][ln.lane] = m;
+        __syncthreads();
+        if (threadIdx.x == 0) next_unit[si & 1] = 0;  // every wave has left this chunk's claims
+        m = red_m[0][ln.hh];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][ln.hh]);
+        auto expo = [&](float z) { return z == -INFINITY ? 0.0f : __expf(z - m); };
+        float ssum = 0.0f;
+        int i = 0;
+        for (; i + kEpi <= mine; i += kEpi) {
+            float e[kEpi];
+#pragma unroll
+            for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
+#pragma unroll
+            for (int v = 0; v < kEpi; ++v) {
+                e[v] = expo(e[v]);
+                ssum += e[v];
+                zl[(i + v) * kStep] = e[v];
+            }
+        }
+        for (; i < mine; ++i) {
+            const float e = expo(zl[i * kStep]);
+            ssum += e;
+            zl[i * kStep] = e;
+        }
+#pragma unroll
+        for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
+        if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;
+        __syncthreads();
+
+        // exchange (wave 0): publish this chunk's pairs, then gather every chunk's pairs (lane l holds words
+        // l, l + 64, ... of the [chunk][padded head] grid, so a lane's head is l % GP) and combine them per head
+        // in a fixed order (a lane's words, then butterflies over the lanes of the same head)
+        uint64_t* xs = xchg + (size_t)cur * C * a.group;  // [chunk][head]
+        if (ln.wave == 0) {
+            const int h = ln.lane % GP;
+            float mh = -INFINITY;  // this chunk's statistics of head h
+            if (h < a.group) {
+                float sh = 0.0f;
+                mh = red_m[0][h];
+                sh = red_s[0][h];
+                for (int w = 1; w < kWaves; ++w) {
+                    mh = fmaxf(mh, red_m[w][h]);
+                    sh += red_s[w][h];
+                }
+                if (ln.lane < GP)
+                    __hip_atomic_store(xs + (size_t)cw * a.group + h, pack_ms(mh, sh), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            }
+            float cm[kMaxWords], cs[kMaxWords];
+            bool done[kMaxWords];
+#pragma unroll
+            for (int k = 0; k < kMaxWords; ++k) {
+                const int c = (ln.lane + k * kWave) / GP;
+                cm[k] = -INFINITY;
+                cs[k] = 0.0f;
+                done[k] = !(c < C && h < a.group);
+            }
+            for (int spin = 0; spin < kSpinLimit; ++spin) {
+                bool all = true;
+#pragma unroll
+                for (int k = 0; k < kMaxWords; ++k) {
+                    if (done[k]) continue;
+                    const int c = (ln.lane + k * kWave) / GP;
+                    const uint64_t v = __hip_atomic_load(xs + (size_t)c * a.group + h, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT);
+                    if ((uint32_t)v != 0u) {
+                        cm[k] = __uint_as_float((uint32_t)(v >> 32));
+                        cs[k] = __uint_as_float((uint32_t)v);
+                        done[k] = true;
+                    } else {
+                        all = false;
+                    }
+                }
+                if (all) break;
+                __builtin_amdgcn_s_sleep(1);
+            }
+            float M = cm[0];
+#pragma unroll
+            for (int k = 1; k < kMaxWords; ++k) M = fmaxf(M, cm[k]);
+#pragma unroll
+            for (int o = GP; o < kWave; o <<= 1) M = fmaxf(M, __shfl_xor(M, o, kWave));
+            float S = 0.0f;
+#pragma unroll
+            for (int k = 0; k < kMaxWords; ++k)
+                if (cs[k] > 0.0f) S += cs[k] * __expf(cm[k] - M);
+#pragma unroll
+            for (int o = GP; o < kWave; o <<= 1) S += __shfl_xor(S, o, kWave);
+            if (ln.lane < GP) fh[h] = (h < a.group && S > 0.0f) ? __expf(mh - M) / S : 0.0f;
+        }
+        __syncthreads();
+
+        // group sums of the normalised probabilities, staged in the first RPW words of each unit's block
+        const float f = fh[ln.hh];
+        auto emit = [&](int unit, float sum) {
+            if (ln.hh == 0) zs[unit * kWave + ln.kk * L::NG + ln.grp] = sum;
+        };
+        i = 0;
+        for (; i + kEpi <= mine; i += kEpi) {
+            float e[kEpi];
+#pragma unroll
+            for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
+#pragma unroll
+            for (int v = 0; v < kEpi; ++v) emit(ln.wave + (i + v) * kWaves, group_allsum<GP>(e[v] * f));
+        }
+        for (; i < mine; ++i) emit(ln.wave + i * kWaves, group_allsum<GP>(zl[i * kStep] * f));
+        __syncthreads();
+        // rows [4j, 4j + 4) of the chunk lie in one unit; rows up to the padded stride are scratch
+        const __amdgpu_buffer_rsrc_t rrs =
+            raw_rsrc(a.r + (size_t)cur * a.n_stride + row0, (a.n_stride - row0) * 4);
+        for (int j = threadIdx.x; j * 4 < rows; j += kThreads) {
+            const int row = j * 4;
+            store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]));
+        }
+        if (!next) break;
+        __syncthreads();  // every thread has read its staged sums before the next chunk's logits land
+        ln.load_q(a, (size_t)(slab / a.hkv), slab % a.hkv, qv);
+    }
+}
+
+// Zeroes the exchange words before a launch (a kernel, not a memset, so that the step can be captured).
+__global__ __launch_bounds__(256) void zero_words_kernel(uint64_t* w, size_t count) {
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (size_t)gridDim.x * 256) w[i] = 0;
+}
+
+template <typename T, int D, int GP>
+hipError_t launch_coop_gp(const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg, int grid, hipStream_t s) {
+    if constexpr (Geometry<T, D, 1>::kChunks < GP) {
+        return hipErrorInvalidValue;
+    } else {
+        auto kern = score_coop_kernel<T, D, GP>;
+        if (plan.lds_bytes > 64 * 1024) {
+            static bool raised = false;  // idempotent attribute; a benign race between threads
+            if (!raised) {
+                hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax);
+                if (e != hipSuccess) return e;
+                raised = true;
+            }
+        }
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), plan.lds_bytes, s, a, xchg, grid / a.nchunk);
+        return hipGetLastError();
+    }
+}
+
+template <typename T, int D, int GP>
+int coop_occupancy(size_t lds) {
+    if constexpr (Geometry<T, D, 1>::kChunks < GP) {
+        return 0;
+    } else {
+        int v = 0;
+        if (lds > 64 * 1024 &&
+            hipFuncSetAttribute(reinterpret_cast<const void*>(score_coop_kernel<T, D, GP>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax) != hipSuccess)
+            return 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, score_coop_kernel<T, D, GP>, kThreads, lds) !=
+            hipSuccess)
+            return 0;
+        return v;
+    }
+}
+
+template <typename T, int D>
+hipError_t launch_coop_d(const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg, int grid, hipStream_t s) {
+    switch (plan.group_pad) {
+        case 1: return launch_coop_gp<T, D, 1>(plan, a, xchg, grid, s);
+        case 2: return launch_coop_gp<T, D, 2>(plan, a, xchg, grid, s);
+        case 4: return launch_coop_gp<T, D, 4>(plan, a, xchg, grid, s);
+        case 8: return launch_coop_gp<T, D, 8>(plan, a, xchg, grid, s);
+        case 16: return launch_coop_gp<T, D, 16>(plan, a, xchg, grid, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <typename T, int D>
+int coop_occupancy_d(int gp, size_t lds) {
+    switch (gp) {
+        case 1: return coop_occupancy<T, D, 1>(lds);
+        case 2: return coop_occupancy<T, D, 2>(lds);
+        case 4: return coop_occupancy<T, D, 4>(lds);
+        case 8: return coop_occupancy<T, D, 8>(lds);
+        case 16: return coop_occupancy<T, D, 16>(lds);
+        default: return 0;
+    }
+}
+
+}  // namespace
+
+int coop_workgroups(int dtype, int head_dim, const ScorePlan& plan) {
+    int occ = 0;
+    if (dtype == 0)
+        occ = head_dim == 64 ? coop_occupancy_d<float, 64>(plan.group_pad, plan.lds_bytes)
+                             : coop_occupancy_d<float, 128>(plan.group_pad, plan.lds_bytes);
+    else
+        occ = head_dim == 64 ? coop_occupancy_d<bf16_t, 64>(plan.group_pad, plan.lds_bytes)
+                             : coop_occupancy_d<bf16_t, 128>(plan.group_pad, plan.lds_bytes);
+    int dev = 0, cus = 0;
+    if (occ < 1 || hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        return 0;
+    return occ * cus;
+}
+
+hipError_t launch_score_coop(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg,
+                             int grid, hipStream_t s) {
+    const size_t words = (size_t)a.layers * a.batch * a.hq * a.nchunk;
+    const unsigned zb = (unsigned)std::min<size_t>((words + 255) / 256, 2048);
+    hipLaunchKernelGGL(zero_words_kernel, dim3(zb), dim3(256), 0, s, xchg, words);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (dtype == 0) {
+        if (head_dim == 64) return launch_coop_d<float, 64>(plan, a, xchg, grid, s);
+        if (head_dim == 128) return launch_coop_d<float, 128>(plan, a, xchg, grid, s);
+    } else {
+        if (head_dim == 64) return launch_coop_d<bf16_t, 64>(plan, a, xchg, grid, s);
+        if (head_dim == 128) return launch_coop_d<bf16_t, 128>(plan, a, xchg, grid, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace ikv

@@ -35,6 +35,8 @@ SCORE_CASES = [
     ("bf16", 128, 14, 2, 3000, 1, 2, False),  # group 7 split path
     ("f32", 64, 2, 1, 10500, 1, 1, False),    # f32 split path
     ("bf16", 128, 4, 1, 1, 1, 1, False),      # a single cached token
+    ("bf16", 128, 8, 2, 40000, 1, 1, True),   # split path: 13 chunks exchanging their statistics
+    ("bf16", 128, 32, 2, 14000, 1, 1, False),  # group 16, 17 chunks: too many to exchange, logits + finish
 ]
 
 
