@@ -27,9 +27,6 @@ constexpr int kMaxSegs = 2048;  // plan segments (a multiple of 64)
 #endif
 constexpr int kBatch = IKV_SEL_BATCH;  // loads issued together by the histogram sweeps
 constexpr int kPlanBatch = 16;  // 64-slot groups whose decisions a wave loads together in the plan sweeps
-#ifndef IKV_SEL_RUNS
-#define IKV_SEL_RUNS 1
-#endif
 
 struct SelShared {
     unsigned hist[256];
@@ -76,10 +73,6 @@ __device__ void find_digit(SelShared& sh, unsigned krem, bool descending) {
 struct RunCounter {
     unsigned bin = 0xffffffffu, count = 0;
     __device__ void add(unsigned* hist, unsigned d) {
-#if !IKV_SEL_RUNS
-        atomicAdd(&hist[d], 1u);
-        return;
-#endif
         if (d != bin) {
             if (count) atomicAdd(&hist[bin], count);
             bin = d;
