@@ -116,6 +116,8 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     // K/V loads of two units in flight, one when a lane's share of a unit is already large (a single head
     // per KV head: 16 rows per lane), which would otherwise spill
     constexpr int kNbuf = IKV_ATTN_NBUF > 0 ? IKV_ATTN_NBUF : (RPG * CPL > 8 ? 1 : 2);
+    using KP = KUnit<T, D, GP>;
+    constexpr int kNbufK = use_mfma<T, D, GP>() ? 2 : kNbuf;  // K units in flight (16 rows each on MFMA)
 
     extern __shared__ float zs[];
     __shared__ float red_m[kWaves][GP], red_s[kWaves][GP], red_n[kWaves];
@@ -123,6 +125,7 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     __shared__ int next_unit[2];
 
     const L ln;
+    const KP kp;
     const int chunk = blockIdx.x % a.nchunk;
     const int s = blockIdx.x / a.nchunk;  // slab: (l * batch + b) * hkv + g, l relative to the call
     const int g = s % a.hkv;
@@ -130,7 +133,8 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     const int b = lb % a.batch;
     const int row0 = chunk * a.chunk_rows;
     const int nrows = min(a.n - row0, a.chunk_rows);  // >= 1: the plan leaves no empty chunk
-    const int nunits = (nrows + RPW - 1) / RPW;
+    const int nunits = (nrows + RPW - 1) / RPW;          // LDS blocks of logits (and V units)
+    const int nku = (nrows + KP::kRows - 1) / KP::kRows;  // claimed units of the K pass
     const size_t base = ((size_t)s * a.cap + row0) * D;
     const __amdgpu_buffer_rsrc_t krs = raw_rsrc(static_cast<const T*>(a.k) + base, nrows * L::kRowBytes);
     const __amdgpu_buffer_rsrc_t vrs = raw_rsrc(static_cast<const T*>(a.v) + base, nrows * L::kRowBytes);
@@ -140,8 +144,8 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
         next_unit[0] = 0;
         next_unit[1] = 0;
     }
-    chunk_t qv[GP][CPL];
-    ln.load_q(a, (size_t)lb, g, qv);
+    typename KP::q_t qv;
+    kp.load_q(a, (size_t)lb, g, qv);
     __syncthreads();
     auto claim = [&](int which) -> int {
         int u = 0;
@@ -150,26 +154,24 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     };
 
     // 1. K pass (loads of claims past the end read zeros and are not reduced)
-    float m = kFloor;
+    typename KP::max_t mk = kp.max_init();
     {
-        chunk_t kbuf[kNbuf][RPG][CPL];
-        int pbuf[kNbuf], ubuf[kNbuf];
+        typename KP::buf_t kbuf[kNbufK];
+        int pbuf[kNbufK], ubuf[kNbufK];
 #pragma unroll
-        for (int j = 0; j < kNbuf - 1; ++j) {
+        for (int j = 0; j < kNbufK - 1; ++j) {
             ubuf[j] = claim(0);
-            ln.load_unit(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
+            kp.load(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
         }
         bool more = true;
         while (more) {
 #pragma unroll
-            for (int j = 0; j < kNbuf; ++j) {
-                const int slot = (j + kNbuf - 1) % kNbuf;
+            for (int j = 0; j < kNbufK; ++j) {
+                const int slot = (j + kNbufK - 1) % kNbufK;
                 ubuf[slot] = claim(0);
-                ln.load_unit(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
-                if (more && ubuf[j] < nunits) {
-                    const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.unit_row(ubuf[j]), nrows);
-                    m = fmaxf(m, z);
-                    zs[ubuf[j] * kWave + ln.lane] = z;
+                kp.load(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
+                if (more && ubuf[j] < nku) {
+                    kp.logits(a, kbuf[j], qv, pbuf[j], ubuf[j], nrows, zs, mk);
                 } else {
                     more = false;
                 }
@@ -191,11 +193,9 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
 
     // 2. per-head max, exponentials in place, per-head sums; several chunks: the logits go to HBM for the
     //    score's finish kernel
-#pragma unroll
-    for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
-    if (ln.lane < GP) red_m[ln.wave][ln.lane] = m;
+    kp.publish_max(mk, red_m[ln.wave]);
     __syncthreads();
-    m = red_m[0][ln.hh];
+    float m = red_m[0][ln.hh];
 #pragma unroll
     for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][ln.hh]);
 

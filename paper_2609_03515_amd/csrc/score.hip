@@ -1,10 +1,11 @@
 // Last-query attention scoring (Eq. 1 with GQA-shared KV heads) for gfx950.
 //
 // The work is a matrix-vector product per (layer, sequence, KV head) slab: every cached key row meets the G
-// query heads of its group.  It is bound by the HBM stream of K (2G flop per 2-byte element), so it runs on
-// the vector ALUs with packed bf16 dot products, not on MFMA.
+// query heads of its group.  It is bound by the HBM stream of K (2G flop per 2-byte element).  Small groups
+// run on the vector ALUs with packed bf16 dot products; padded groups of 8 and 16 over bf16 keys take the
+// logits from the matrix cores instead (KUnit in stream_lane.h), whose result lands in the same LDS layout.
 //
-// Lane layout: a K row of d elements is LPR 16-byte chunks, one per lane of an aligned LPR-lane group (16 for
+// Lane layout (vector form): a K row of d elements is LPR 16-byte chunks, one per lane of an aligned LPR-lane group (16 for
 // d = 128 bf16 / d = 64 f32, 8 for d = 64 bf16); a wave load instruction therefore covers 64/LPR consecutive
 // rows, 1 KiB contiguous.  Each lane handles RPG = LPR / GP rows per iteration (GP = group size rounded up to
 // a power of two), producing RPG * GP = LPR partial dot products; a DPP reduce-scatter over the group leaves
@@ -40,8 +41,8 @@ template <typename T, int D, int GP, bool kMulti>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(score_waves_per_eu<T, D, GP, kMulti>())))
 void score_lds_kernel(ScoreArgs a) {
     using L = Lane<T, D, GP>;
-    using chunk_t = typename L::chunk_t;
-    constexpr int RPG = L::RPG, CPL = L::CPL, RPW = L::RPW;
+    using KP = KUnit<T, D, GP>;
+    constexpr int RPW = L::RPW;
     constexpr int kNbuf = Geometry<T, D, GP>::kNbufLds;
 
     extern __shared__ float zs[];
@@ -49,6 +50,7 @@ void score_lds_kernel(ScoreArgs a) {
     __shared__ int next_unit[2];  // claim counters of the slab being streamed and of the next one
 
     const L ln;
+    const KP kp;
     const int merge = kMulti ? a.merge : 1;
     const int blocks = a.hkv / merge;  // items per (layer, sequence)
     const int items = a.layers * a.batch * blocks;
@@ -56,14 +58,15 @@ void score_lds_kernel(ScoreArgs a) {
     // global slab index (lb * hkv + g) of this workgroup's si-th slab; items are lb * blocks + block
     auto slab_at = [&](int si) { return ((int)blockIdx.x + si / merge * (int)gridDim.x) * merge + si % merge; };
     const int n = a.n;
-    const int nunits = (n + RPW - 1) / RPW;
+    const int nunits = (n + RPW - 1) / RPW;      // LDS blocks of logits
+    const int nku = (n + KP::kRows - 1) / KP::kRows;  // claimed units of the K pass
     // item sums after the logits (sized by the plan: the logits' units rounded up to whole iterations)
     float* racc = zs + (size_t)((nunits + kWaves - 1) / kWaves) * kThreads;
     // with the newcomer given apart, rows [0, n - 1) come from the cache and row n - 1 is substituted into the
     // buffers of its unit before its logits are taken (the same arithmetic as a cached row)
     const bool has_new = a.k_new != nullptr;
     const int cached = n - (has_new ? 1 : 0);
-    const int unit_new = has_new ? (n - 1) / RPW : -1;
+    const int unit_new = has_new ? (n - 1) / KP::kRows : -1;
     auto p_rsrc = [&](int sidx) {
         return raw_rsrc(a.pos + (size_t)(sidx / a.hkv % a.batch) * a.cap, cached * 4);
     };
@@ -71,16 +74,16 @@ void score_lds_kernel(ScoreArgs a) {
         return raw_rsrc(static_cast<const T*>(a.k) + (size_t)sidx * a.cap * D, cached * L::kRowBytes);
     };
     auto new_row = [&](int sidx) { return static_cast<const T*>(a.k_new) + (size_t)sidx * D; };
-    auto load_slab_consts = [&](int sidx, chunk_t (&qv)[GP][CPL], chunk_t (&kn)[CPL]) {
-        ln.load_q(a, (size_t)(sidx / a.hkv), sidx % a.hkv, qv);
-        if (has_new) ln.load_row(new_row(sidx), kn);
+    auto load_slab_consts = [&](int sidx, typename KP::q_t& qv, typename KP::row_t& kn) {
+        kp.load_q(a, (size_t)(sidx / a.hkv), sidx % a.hkv, qv);
+        if (has_new) kp.load_row(new_row(sidx), kn);
     };
 
     if (threadIdx.x < 2) next_unit[threadIdx.x] = 0;
     int sidx = slab_at(0);
     __amdgpu_buffer_rsrc_t krs = k_rsrc(sidx), prs = p_rsrc(sidx);
-    chunk_t qv[GP][CPL];
-    chunk_t kn[CPL];
+    typename KP::q_t qv;
+    typename KP::row_t kn;
     load_slab_consts(sidx, qv, kn);
     __syncthreads();
     auto claim = [&](int si) -> int {
@@ -91,31 +94,29 @@ void score_lds_kernel(ScoreArgs a) {
 
     // stream: claim a unit, issue its loads kNbuf-1 units ahead of the one being reduced.  Loads are issued on
     // every path (claims past the end read zeros), so the wait before a reduction covers only its own buffer.
-    chunk_t kbuf[kNbuf][RPG][CPL];
+    typename KP::buf_t kbuf[kNbuf];
     int pbuf[kNbuf], ubuf[kNbuf];
     auto prime = [&](int si) {
 #pragma unroll
         for (int j = 0; j < kNbuf - 1; ++j) {
             ubuf[j] = claim(si);
-            ln.load_unit(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
+            kp.load(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
         }
     };
     prime(0);
     for (int si = 0; si < nslab; ++si) {
         const int gi = si % merge;  // position of the slab in its item
-        float m = kFloor;
+        typename KP::max_t mk = kp.max_init();
         bool more = true;
         while (more) {
 #pragma unroll
             for (int j = 0; j < kNbuf; ++j) {
                 const int slot = (j + kNbuf - 1) % kNbuf;
                 ubuf[slot] = claim(si);
-                ln.load_unit(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
-                if (more && ubuf[j] < nunits) {
-                    if (ubuf[j] == unit_new) ln.put_row(kbuf[j], pbuf[j], kn, a.new_pos, unit_new, n - 1);
-                    const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.unit_row(ubuf[j]), n);
-                    m = fmaxf(m, z);
-                    zs[ubuf[j] * kWave + ln.lane] = z;
+                kp.load(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
+                if (more && ubuf[j] < nku) {
+                    if (ubuf[j] == unit_new) kp.put_row(kbuf[j], pbuf[j], kn, a.new_pos, unit_new, n - 1);
+                    kp.logits(a, kbuf[j], qv, pbuf[j], ubuf[j], n, zs, mk);
                 } else {
                     more = false;  // claims only grow: every later unit of this wave is past the end too
                 }
@@ -134,14 +135,12 @@ void score_lds_kernel(ScoreArgs a) {
         float* zl = zs + ln.wave * kWave + ln.lane;
         constexpr int kStep = kWaves * kWave;  // LDS words between a thread's consecutive units
         const int mine = nunits > ln.wave ? (nunits - ln.wave + kWaves - 1) / kWaves : 0;
-#pragma unroll
-        for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
-        if (ln.lane < GP) red_m[ln.wave][ln.lane] = m;
+        kp.publish_max(mk, red_m[ln.wave]);
         __syncthreads();
         // every wave has left this slab's claims: its counter is free for the slab after next (primed only
         // after the barrier that ends this epilogue)
         if (threadIdx.x == 0) next_unit[si & 1] = 0;
-        m = red_m[0][ln.hh];
+        float m = red_m[0][ln.hh];
 #pragma unroll
         for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][ln.hh]);
         auto expo = [&](float z) { return z == -INFINITY ? 0.0f : __expf(z - m); };

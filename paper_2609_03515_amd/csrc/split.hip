@@ -36,8 +36,8 @@ template <typename T, int D, int GP>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(coop_waves_per_eu<T, D, GP>())))
 void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round) {
     using L = Lane<T, D, GP>;
-    using chunk_t = typename L::chunk_t;
-    constexpr int RPG = L::RPG, CPL = L::CPL, RPW = L::RPW;
+    using KP = KUnit<T, D, GP>;
+    constexpr int RPW = L::RPW;
     constexpr int kNbuf = Geometry<T, D, GP>::kNbufLds;
 
     extern __shared__ float zs[];
@@ -46,12 +46,14 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round) {
     __shared__ int next_unit[2];
 
     const L ln;
+    const KP kp;
     const int n = a.n, C = a.nchunk;
     const int slabs = a.layers * a.batch * a.hkv;
     const int cw = blockIdx.x % C;  // this workgroup's chunk of every slab it scores
     const int row0 = cw * a.chunk_rows;
     const int rows = min(a.chunk_rows, n - row0);
-    const int nunits = (rows + RPW - 1) / RPW;
+    const int nunits = (rows + RPW - 1) / RPW;          // LDS blocks of logits
+    const int nku = (rows + KP::kRows - 1) / KP::kRows;  // claimed units of the K pass
     auto k_rsrc = [&](int slab) {
         return raw_rsrc(static_cast<const T*>(a.k) + ((size_t)slab * a.cap + row0) * D, rows * L::kRowBytes);
     };
@@ -63,38 +65,36 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round) {
     if (slab >= slabs) return;
     if (threadIdx.x < 2) next_unit[threadIdx.x] = 0;
     __amdgpu_buffer_rsrc_t krs = k_rsrc(slab), prs = p_rsrc(slab);
-    chunk_t qv[GP][CPL];
-    ln.load_q(a, (size_t)(slab / a.hkv), slab % a.hkv, qv);
+    typename KP::q_t qv;
+    kp.load_q(a, (size_t)(slab / a.hkv), slab % a.hkv, qv);
     __syncthreads();
     auto claim = [&](int si) -> int {
         int u = 0;
         if (ln.lane == 0) u = atomicAdd(&next_unit[si & 1], 1);
         return __builtin_amdgcn_readfirstlane(u);
     };
-    chunk_t kbuf[kNbuf][RPG][CPL];
+    typename KP::buf_t kbuf[kNbuf];
     int pbuf[kNbuf], ubuf[kNbuf];
     auto prime = [&](int si) {
 #pragma unroll
         for (int j = 0; j < kNbuf - 1; ++j) {
             ubuf[j] = claim(si);
-            ln.load_unit(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
+            kp.load(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
         }
     };
     prime(0);
     for (int si = 0;; ++si) {
         const int cur = slab;
-        float m = kFloor;
+        typename KP::max_t mk = kp.max_init();
         bool more = true;
         while (more) {
 #pragma unroll
             for (int j = 0; j < kNbuf; ++j) {
                 const int slot = (j + kNbuf - 1) % kNbuf;
                 ubuf[slot] = claim(si);
-                ln.load_unit(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
-                if (more && ubuf[j] < nunits) {
-                    const float z = ln.logit(a, kbuf[j], qv, pbuf[j], ln.unit_row(ubuf[j]), rows);
-                    m = fmaxf(m, z);
-                    zs[ubuf[j] * kWave + ln.lane] = z;
+                kp.load(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
+                if (more && ubuf[j] < nku) {
+                    kp.logits(a, kbuf[j], qv, pbuf[j], ubuf[j], rows, zs, mk);
                 } else {
                     more = false;
                 }
@@ -112,12 +112,10 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round) {
         float* zl = zs + ln.wave * kWave + ln.lane;
         constexpr int kStep = kWaves * kWave;
         const int mine = nunits > ln.wave ? (nunits - ln.wave + kWaves - 1) / kWaves : 0;
-#pragma unroll
-        for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
-        if (ln.lane < GP) red_m[ln.wave][ln.lane] = m;
+        kp.publish_max(mk, red_m[ln.wave]);
         __syncthreads();
         if (threadIdx.x == 0) next_unit[si & 1] = 0;  // every wave has left this chunk's claims
-        m = red_m[0][ln.hh];
+        float m = red_m[0][ln.hh];
 #pragma unroll
         for (int w = 1; w < kWaves; ++w) m = fmaxf(m, red_m[w][ln.hh]);
         auto expo = [&](float z) { return z == -INFINITY ? 0.0f : __expf(z - m); };
@@ -230,7 +228,7 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round) {
         }
         if (!next) break;
         __syncthreads();  // every thread has read its staged sums before the next chunk's logits land
-        ln.load_q(a, (size_t)(slab / a.hkv), slab % a.hkv, qv);
+        kp.load_q(a, (size_t)(slab / a.hkv), slab % a.hkv, qv);
     }
 }
 

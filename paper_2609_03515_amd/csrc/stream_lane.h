@@ -5,6 +5,8 @@
 // (row, head) logit.
 #pragma once
 
+#include <type_traits>
+
 #include "kernels.h"
 #include "kv_common.h"
 
@@ -199,6 +201,177 @@ struct Lane {
         const float dotv = reduce_scatter<LPR>(v, p);
         const float z = fmaf(dotv, a.scale, posv >= a.recent_from ? a.bias : 0.0f);
         return (row < row_end && hh < a.group) ? z : -INFINITY;
+    }
+};
+
+typedef __bf16 __attribute__((ext_vector_type(8))) bf16x8;
+
+// Logits of the K pass, one claimed unit of rows at a time, for the G heads that share a KV head.  Two forms
+// leave the same LDS layout (block u of 64 words holds the logits of rows [u RPW, (u + 1) RPW) in the word of
+// the lane that owns each (row, head) after the reduce-scatter), so the kernels' epilogues and V passes do not
+// depend on which one ran:
+//  * the vector-ALU lane machinery above (units of RPW rows, one logit per lane);
+//  * matrix cores, for bf16 keys with a padded group of 8 or 16: the group's query heads against 16 key rows
+//    are a 16 x 16 x d product (heads past G are zero rows), D / 32 v_mfma_f32_16x16x32_bf16 per unit.  With
+//    G = 7 the vector dot products cost two instructions per byte of K and left the Qwen-shaped scorer
+//    partly ALU-bound (removing them saved 24 of 323 us per launch); with G = 4 they are hidden behind the
+//    stream (the matrix-core form measured no faster there), so group 4 keeps the vector form.
+template <typename T, int D, int GP>
+constexpr bool use_mfma() {
+    return std::is_same<T, bf16_t>::value && (GP == 8 || GP == 16) &&
+           Geometry<T, D, 1>::kChunks >= GP;
+}
+
+template <typename T, int D, int GP, bool kMfma = use_mfma<T, D, GP>()>
+struct KUnit {
+    using L = Lane<T, D, GP>;
+    using chunk_t = typename L::chunk_t;
+    static constexpr int kRows = L::RPW;  // rows per claimed unit
+    typedef chunk_t q_t[GP][L::CPL];
+    typedef chunk_t buf_t[L::RPG][L::CPL];
+    typedef chunk_t row_t[L::CPL];
+    typedef float max_t;
+
+    L ln;
+
+    __device__ void load_q(const ScoreArgs& a, size_t lb, int g, q_t& qv) const { ln.load_q(a, lb, g, qv); }
+    __device__ void load(__amdgpu_buffer_rsrc_t krs, __amdgpu_buffer_rsrc_t prs, int u, buf_t& dst, int& pdst) const {
+        ln.load_unit(krs, prs, u, dst, pdst);
+    }
+    __device__ void load_row(const T* row, row_t& dst) const { ln.load_row(row, dst); }
+    __device__ void put_row(buf_t& dst, int& pdst, const row_t& src, int posv, int u, int row) const {
+        ln.put_row(dst, pdst, src, posv, u, row);
+    }
+    __device__ max_t max_init() const { return kFloor; }
+    // logits of unit u (rows past row_end masked to -inf) into LDS, and the running maximum
+    __device__ void logits(const ScoreArgs& a, const buf_t& kb, const q_t& qv, int posv, int u, int row_end,
+                           float* zs, max_t& m) const {
+        const float z = ln.logit(a, kb, qv, posv, ln.unit_row(u), row_end);
+        m = fmaxf(m, z);
+        zs[u * kWave + ln.lane] = z;
+    }
+    // the wave's per-head maxima into red[0, GP)
+    __device__ void publish_max(max_t m, float* red) const {
+#pragma unroll
+        for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+        if (ln.lane < GP) red[ln.lane] = m;
+    }
+};
+
+// Matrix-core form.  v_mfma_f32_16x16x32_bf16 operand layout (checked on the device): lane l supplies row
+// l % 16 of A (a query head) and column l % 16 of B (a key row), each as 8 elements (slice l / 16) of the
+// 32-element k block, and receives D[4 (l / 16) + i][l % 16] for i < 4: four heads of one row, which go to
+// LDS as one 16-byte store.  MFMA kb covers the elements [32 kb, 32 kb + 32) of every row.
+//
+// Loading those operands directly would have every load instruction read 64 bytes of 16 rows, half of each
+// 128-byte line, and the other half one instruction later: measured 14% slower than the vector form on the
+// Qwen shape.  So the loads stay whole-line: load (c, v) gives lane l = 16 kq + 8 w + r (r < 8, w < 2) the
+// 16 bytes 128 c + 64 w + 16 kq of row 8 v + r of the unit; the 8 lanes with equal r cover line c of that
+// row.  Lane l then needs, for MFMA 2 c + w, what it loaded itself at v = w, and for MFMA 2 c + (1 - w) what
+// lane l ^ 8 loaded at v = w: one DPP row_ror:8 move per dword, restricted by the bank mask to the lanes
+// that take it (banks 2, 3 are the lanes with w = 1).
+template <typename T, int D, int GP>
+struct KUnit<T, D, GP, true> {
+    using L = Lane<T, D, GP>;
+    typedef u32x4 chunk_t;
+    static constexpr int kLines = D * (int)sizeof(T) / 128;  // 128-byte lines per row
+    static constexpr int kRows = 16;
+    static_assert(L::RPW * GP == kWave && kRows % L::RPW == 0 && GP % 4 == 0, "whole LDS blocks, 4 heads per store");
+    typedef chunk_t q_t[2 * kLines];
+    typedef chunk_t buf_t[kLines][2];
+    typedef chunk_t row_t[kLines];
+    typedef f32x4 max_t;
+
+    int col, kq, w, r;  // D column (row of the unit) / A row (head); k slice; half-line and row of the loads
+
+    __device__ KUnit() {
+        const int lane = threadIdx.x & (kWave - 1);
+        col = lane % 16;
+        kq = lane / 16;
+        w = (lane / 8) % 2;
+        r = lane % 8;
+    }
+
+    __device__ void load_q(const ScoreArgs& a, size_t lb, int g, q_t& qv) const {
+        const T* qh = static_cast<const T*>(a.q) + (lb * a.hq + (size_t)g * a.group + col) * D + kq * 8;
+#pragma unroll
+        for (int kb = 0; kb < 2 * kLines; ++kb)
+            qv[kb] = col < a.group ? *reinterpret_cast<const chunk_t*>(qh + kb * 32) : chunk_t{};
+    }
+    static constexpr int kRowBytes = D * (int)sizeof(T);
+    __device__ void load(__amdgpu_buffer_rsrc_t krs, __amdgpu_buffer_rsrc_t prs, int u, buf_t& dst, int& pdst) const {
+        const int off = (u * kRows + r) * kRowBytes + w * 64 + kq * 16;
+#pragma unroll
+        for (int c = 0; c < kLines; ++c)
+#pragma unroll
+            for (int v = 0; v < 2; ++v)
+                dst[c][v] = __builtin_amdgcn_raw_buffer_load_b128(krs, off + v * 8 * kRowBytes + c * 128, 0,
+                                                                  IKV_NT_LOADS ? kNonTemporal : 0);
+        pdst = (int)__builtin_amdgcn_raw_buffer_load_b32(prs, (u * kRows + col) * 4, 0, 0);
+    }
+    // this lane's pieces of one row as the loads above would give them (the newcomer)
+    __device__ void load_row(const T* row, row_t& dst) const {
+#pragma unroll
+        for (int c = 0; c < kLines; ++c)
+            dst[c] = *reinterpret_cast<const chunk_t*>(row + c * 64 + w * 32 + kq * 8);
+    }
+    __device__ void put_row(buf_t& dst, int& pdst, const row_t& src, int posv, int u, int row) const {
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+            const bool here = u * kRows + 8 * v + r == row;
+#pragma unroll
+            for (int c = 0; c < kLines; ++c) dst[c][v] = here ? src[c] : dst[c][v];
+        }
+        pdst = u * kRows + col == row ? posv : pdst;
+    }
+    __device__ max_t max_init() const { return max_t{kFloor, kFloor, kFloor, kFloor}; }
+
+    // B operand of MFMA 2 c + h from the whole-line loads of line c
+    template <int BANKS>
+    __device__ static chunk_t take(const chunk_t& own, const chunk_t& other) {
+        chunk_t x;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            x[j] = (uint32_t)__builtin_amdgcn_update_dpp((int)own[j], (int)other[j], kRor8, 0xF, BANKS, false);
+        return x;
+    }
+    __device__ void logits(const ScoreArgs& a, const buf_t& kb, const q_t& qv, int posv, int u, int row_end,
+                           float* zs, max_t& m) const {
+        f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int c = 0; c < kLines; ++c) {
+            const chunk_t b0 = take<0xC>(kb[c][0], kb[c][1]);  // w = 1 lanes: lane l ^ 8's load of rows 8..15
+            const chunk_t b1 = take<0x3>(kb[c][1], kb[c][0]);  // w = 0 lanes: lane l ^ 8's load of rows 0..7
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qv[2 * c]),
+                                                          __builtin_bit_cast(bf16x8, b0), acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qv[2 * c + 1]),
+                                                          __builtin_bit_cast(bf16x8, b1), acc, 0, 0, 0);
+        }
+        const int row = u * kRows + col;
+        const int h0 = kq * 4;
+        const float bias = posv >= a.recent_from ? a.bias : 0.0f;
+        f32x4 z;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            z[i] = (row < row_end && h0 + i < a.group) ? fmaf(acc[i], a.scale, bias) : -INFINITY;
+            m[i] = fmaxf(m[i], z[i]);
+        }
+        // the word of (row, head) is the one the lane that owns it in the vector form writes: block row / RPW,
+        // lane (row_in_block % NG) * LPR + (row_in_block / NG) * GP + head.  Rows of the last block past row_end
+        // still get their -inf; nothing past that block is written.
+        const int rib = row % L::RPW;
+        const int word = row / L::RPW * kWave + rib % L::NG * L::LPR + rib / L::NG * GP + h0;
+        const int pad_end = (row_end + L::RPW - 1) / L::RPW * L::RPW;
+        if (h0 < GP && row < pad_end) *reinterpret_cast<f32x4*>(zs + word) = z;
+    }
+    __device__ void publish_max(max_t m, float* red) const {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int o = 1; o < 16; o <<= 1) m[i] = fmaxf(m[i], __shfl_xor(m[i], o, kWave));
+        if (col == 0 && kq * 4 < GP)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) red[kq * 4 + i] = m[i];
     }
 };
 
