@@ -31,7 +31,9 @@
  *    Query head h reads KV head h / (n_q_heads / n_kv_heads).  Every sequence holds the same n tokens.
  *  - Preconditions not checked on the device: keys, queries and utilities are finite; utilities are >= 0
  *    when produced by this library; positions are unique within a sequence.
- *  - The calls are stateless and may run concurrently on different streams with disjoint buffers.
+ *  - The calls keep no state between calls (apart from per-device caches of kernel attributes and occupancy,
+ *    filled on first use under atomics) and may run concurrently, from several host threads, on different
+ *    streams with disjoint buffers.
  */
 #ifndef INERTIAKV_H
 #define INERTIAKV_H

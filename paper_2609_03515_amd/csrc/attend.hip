@@ -397,13 +397,9 @@ hipError_t launch_attend_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream
     } else {
         auto kern = attend_kernel<T, D, GP, true>;
         if (plan.lds_bytes > 64 * 1024) {
-            static bool raised = false;  // idempotent attribute; a benign race between threads
-            if (!raised) {
-                hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax);
-                if (e != hipSuccess) return e;
-                raised = true;
-            }
+            static std::atomic<bool> raised[kMaxDevices];
+            const hipError_t e = raise_lds_limit(reinterpret_cast<const void*>(kern), raised);
+            if (e != hipSuccess) return e;
         }
         hipLaunchKernelGGL(kern, dim3(plan.grid), dim3(kThreads), plan.lds_bytes, s, a);
         if (plan.split) {
@@ -423,13 +419,9 @@ hipError_t launch_chunks_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream
     } else {
         auto kern = attend_kernel<T, D, GP, false>;
         if (plan.lds_bytes > 64 * 1024) {
-            static bool raised = false;  // idempotent attribute; a benign race between threads
-            if (!raised) {
-                hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax);
-                if (e != hipSuccess) return e;
-                raised = true;
-            }
+            static std::atomic<bool> raised[kMaxDevices];
+            const hipError_t e = raise_lds_limit(reinterpret_cast<const void*>(kern), raised);
+            if (e != hipSuccess) return e;
         }
         hipLaunchKernelGGL(kern, dim3(plan.grid), dim3(kThreads), plan.lds_bytes, s, a);
         return hipGetLastError();

@@ -256,13 +256,9 @@ hipError_t launch_lds(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) 
     const bool multi = a.merge > 1 || (plan.grid > 0 && plan.grid < items);
     auto kern = multi ? score_lds_kernel<T, D, GP, true> : score_lds_kernel<T, D, GP, false>;
     if (plan.lds_bytes > 64 * 1024) {
-        static bool raised[2] = {false, false};  // idempotent attribute; a benign race between threads
-        if (!raised[multi]) {
-            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax);
-            if (e != hipSuccess) return e;
-            raised[multi] = true;
-        }
+        static std::atomic<bool> raised[2][kMaxDevices];
+        const hipError_t e = raise_lds_limit(reinterpret_cast<const void*>(kern), raised[multi]);
+        if (e != hipSuccess) return e;
     }
     const int grid = plan.grid > 0 && plan.grid < items ? plan.grid : items;
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), plan.lds_bytes, s, a);
@@ -280,21 +276,25 @@ hipError_t launch_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
 }
 
 // Workgroups of the single-slab (kMulti false) or multi-slab variant one CU holds by its registers (0 when
-// the query fails); cached per instance (a benign race: every thread computes the same value).
+// the query fails); cached per instance and device (atomics: concurrent first calls store the same value).
 template <typename T, int D, int GP, bool kMulti>
 int kernel_occupancy() {
     if constexpr (Geometry<T, D, 1>::kChunks < GP) {
         return 0;
     } else {
-        static int occ = -1;
-        if (occ < 0) {
-            int v = 0;
-            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, score_lds_kernel<T, D, GP, kMulti>, kThreads, 0) !=
-                hipSuccess)
-                v = 0;
-            occ = v;
+        static std::atomic<int> cached[kMaxDevices];  // occupancy + 1; 0 = not queried yet
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = -1;
+        if (dev >= 0) {
+            const int c = cached[dev].load(std::memory_order_relaxed);
+            if (c > 0) return c - 1;
         }
-        return occ;
+        int v = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, score_lds_kernel<T, D, GP, kMulti>, kThreads, 0) !=
+            hipSuccess)
+            v = 0;
+        if (dev >= 0) cached[dev].store(v + 1, std::memory_order_relaxed);
+        return v;
     }
 }
 

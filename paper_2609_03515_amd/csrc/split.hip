@@ -244,13 +244,9 @@ hipError_t launch_coop_gp(const ScorePlan& plan, const ScoreArgs& a, uint64_t* x
     } else {
         auto kern = score_coop_kernel<T, D, GP>;
         if (plan.lds_bytes > 64 * 1024) {
-            static bool raised = false;  // idempotent attribute; a benign race between threads
-            if (!raised) {
-                hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax);
-                if (e != hipSuccess) return e;
-                raised = true;
-            }
+            static std::atomic<bool> raised[kMaxDevices];
+            const hipError_t e = raise_lds_limit(reinterpret_cast<const void*>(kern), raised);
+            if (e != hipSuccess) return e;
         }
         hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), plan.lds_bytes, s, a, xchg, grid / a.nchunk);
         return hipGetLastError();
@@ -263,9 +259,9 @@ int coop_occupancy(size_t lds) {
         return 0;
     } else {
         int v = 0;
+        static std::atomic<bool> raised[kMaxDevices];
         if (lds > 64 * 1024 &&
-            hipFuncSetAttribute(reinterpret_cast<const void*>(score_coop_kernel<T, D, GP>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax) != hipSuccess)
+            raise_lds_limit(reinterpret_cast<const void*>(score_coop_kernel<T, D, GP>), raised) != hipSuccess)
             return 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, score_coop_kernel<T, D, GP>, kThreads, lds) !=
             hipSuccess)

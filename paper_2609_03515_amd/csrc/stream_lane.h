@@ -5,6 +5,7 @@
 // (row, head) logit.
 #pragma once
 
+#include <atomic>
 #include <type_traits>
 
 #include "kernels.h"
@@ -38,6 +39,18 @@ constexpr int kRsrcConfig = 0x00020000;  // raw (unformatted, stride 0) buffer r
 // the 27 MB of group sums cost ~40 us of a 290 us launch with the default policy, ~24 us with this one
 // (non-temporal: ~30 us).
 constexpr int kStoreStream = 16;
+
+// Host side: raises a kernel's dynamic-LDS limit to kFastLdsMax once per device.  `done` is the kernel's own
+// flag array; concurrent first calls may both set the (idempotent) attribute, and the flags are atomics.
+constexpr int kMaxDevices = 64;
+inline hipError_t raise_lds_limit(const void* kern, std::atomic<bool> (&done)[kMaxDevices]) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = -1;
+    if (dev >= 0 && done[dev].load(std::memory_order_acquire)) return hipSuccess;
+    const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kFastLdsMax);
+    if (e == hipSuccess && dev >= 0) done[dev].store(true, std::memory_order_release);
+    return e;
+}
 
 // Raw buffer resource over `bytes` bytes at `base` (reads at offsets >= bytes return zero).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, int bytes) {
