@@ -123,6 +123,7 @@ GEOMS = [  # (dtype, head_dim, n_q, n_kv, n)
     ("bf16", 128, 16, 2, 300), ("bf16", 128, 16, 1, 520), ("bf16", 64, 8, 8, 333), ("bf16", 64, 16, 4, 1000),
     ("bf16", 64, 16, 2, 999), ("f32", 64, 4, 2, 513), ("f32", 128, 4, 4, 600), ("f32", 128, 8, 2, 1025),
     ("f32", 64, 16, 1, 200), ("bf16", 128, 32, 8, 5200),  # LDS limit: more than 5120 rows per chunk
+    ("bf16", 128, 10, 2, 701), ("bf16", 128, 24, 2, 611), ("bf16", 64, 12, 2, 803),  # groups 5, 12, 6
 ]
 
 
