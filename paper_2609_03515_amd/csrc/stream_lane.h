@@ -72,12 +72,12 @@ struct Geometry {
     static constexpr int kChunks = D / kEpc;
     // Lanes per K row: IKV_LPR (16: one 16-byte chunk each for d = 128 bf16, a wave load covers 1 KiB of
     // consecutive rows), at least the padded group (the reduce-scatter leaves one (row, head) per lane), at
-    // most the row's chunks.  A padded group of 8 over rows of at most 16 chunks takes 8 lanes instead: there
-    // the dot products cost two instructions per byte of K and dominate the issue slots, and 8 lanes (two
-    // chunks each, every load still on whole 128-byte lines) need a 3-step reduce-scatter of 8 values per
-    // lane instead of a 4-step one of 16 (the Qwen-shaped steady step: 347 -> 320 us with the scorer's
-    // schedule).  Group 4 gains nothing from it and the attention's V pass (two chunks of accumulators per
-    // lane) loses 5-13%.
+    // most the row's chunks.  A padded group of 8 over rows of at most 16 chunks takes 8 lanes instead (two
+    // chunks each, every load still on whole 128-byte lines): with vector dot products the 3-step
+    // reduce-scatter of 8 values took the Qwen-shaped steady step from 347 to 320 us, and with the matrix-core
+    // logits (which keep this layout) the step is still ~0.4% and step 1 ~3% faster than with 16 lanes.
+    // Group 4 gains nothing from it and the attention's V pass (two chunks of accumulators per lane) loses
+    // 5-13%.
     static constexpr int kLprWide = (GP > IKV_LPR ? GP : IKV_LPR) < kChunks ? (GP > IKV_LPR ? GP : IKV_LPR) : kChunks;
     static constexpr int kLpr = (GP == 8 && kChunks <= 16) ? 8 : kLprWide;
     static constexpr int kCpl = kChunks / kLpr;
