@@ -62,12 +62,30 @@ __global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
     __shared__ float cm[GP], ci[GP];
     const int s = blockIdx.x;  // slab: (l * batch + b) * hkv + g, l relative to the call
     const size_t head0 = (size_t)(s / a.hkv) * a.hq + (size_t)(s % a.hkv) * a.group;
+    // The loops over chunks load four chunks' values before using them (the loads are independent; the
+    // arithmetic keeps the sequential order, so the result does not depend on the unrolling).
+    constexpr int kU = 4;
     if (threadIdx.x < a.group) {
         const float2* pp = a.part + (head0 + threadIdx.x) * a.nchunk;
         float mx = -INFINITY;
-        for (int c = 0; c < a.nchunk; ++c) mx = fmaxf(mx, pp[c].x);
+        int c = 0;
+        for (; c + kU <= a.nchunk; c += kU) {
+            float2 p[kU];
+#pragma unroll
+            for (int j = 0; j < kU; ++j) p[j] = pp[c + j];
+#pragma unroll
+            for (int j = 0; j < kU; ++j) mx = fmaxf(mx, p[j].x);
+        }
+        for (; c < a.nchunk; ++c) mx = fmaxf(mx, pp[c].x);
         float tot = 0.0f;
-        for (int c = 0; c < a.nchunk; ++c) tot = fmaf(__expf(pp[c].x - mx), pp[c].y, tot);
+        for (c = 0; c + kU <= a.nchunk; c += kU) {
+            float2 p[kU];
+#pragma unroll
+            for (int j = 0; j < kU; ++j) p[j] = pp[c + j];
+#pragma unroll
+            for (int j = 0; j < kU; ++j) tot = fmaf(__expf(p[j].x - mx), p[j].y, tot);
+        }
+        for (; c < a.nchunk; ++c) tot = fmaf(__expf(pp[c].x - mx), pp[c].y, tot);
         cm[threadIdx.x] = mx;
         ci[threadIdx.x] = tot > 0.0f ? 1.0f / tot : 0.0f;
     }
@@ -83,7 +101,18 @@ __global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
         const float2* pp = a.part + (head0 + h) * a.nchunk;
         const float* op = a.opart + (head0 + h) * a.nchunk * D + idx % D;
         float acc = 0.0f;
-        for (int c = 0; c < a.nchunk; ++c) acc = fmaf(__expf(pp[c].x - cm[h]), op[(size_t)c * D], acc);
+        int c = 0;
+        for (; c + kU <= a.nchunk; c += kU) {
+            float m[kU], x[kU];
+#pragma unroll
+            for (int j = 0; j < kU; ++j) {
+                m[j] = pp[c + j].x;
+                x[j] = op[(size_t)(c + j) * D];
+            }
+#pragma unroll
+            for (int j = 0; j < kU; ++j) acc = fmaf(__expf(m[j] - cm[h]), x[j], acc);
+        }
+        for (; c < a.nchunk; ++c) acc = fmaf(__expf(pp[c].x - cm[h]), op[(size_t)c * D], acc);
         Elem<T>::store(ob + idx, acc * ci[h]);
     }
     if (a.emit) {
