@@ -241,6 +241,7 @@ def _hip_runtime():
     if _hip is None:
         _hip = ctypes.CDLL("libamdhip64.so")
         _hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        _hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
         _hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
         _hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
         _hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
@@ -248,10 +249,20 @@ def _hip_runtime():
     return _hip
 
 
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000  # hipEventDisableSystemFence
+
+
 class HipEvent:
-    def __init__(self):
+    """A HIP event.  timing_only: created with hipEventDisableSystemFence, so recording it does not write back
+    and invalidate the caches (a timestamp between kernels that leaves them undisturbed); read it only after
+    the stream has been synchronized."""
+
+    def __init__(self, timing_only: bool = False):
         self.handle = ctypes.c_void_p()
-        rc = _hip_runtime().hipEventCreate(ctypes.byref(self.handle))
+        if timing_only:
+            rc = _hip_runtime().hipEventCreateWithFlags(ctypes.byref(self.handle), HIP_EVENT_DISABLE_SYSTEM_FENCE)
+        else:
+            rc = _hip_runtime().hipEventCreate(ctypes.byref(self.handle))
         if rc != 0:
             raise RuntimeError(f"hipEventCreate failed ({rc})")
 

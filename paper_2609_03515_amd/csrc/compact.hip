@@ -223,6 +223,23 @@ __global__ __launch_bounds__(kPlaceThreads) void place_kernel(PlaceArgs a) {
     const int l = blockIdx.x, b = blockIdx.y;
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     const int n = a.n;
+    // this thread's 16-byte chunks of the newcomer's rows (tensor, KV head, chunk) are loaded first, so their
+    // latency overlaps the candidates' reduction
+    const int lpr = a.row_bytes / 16;
+    const int total = 2 * a.hkv * lpr;
+    constexpr int kPre = 2;
+    u32x4 pre[kPre];
+    auto src_of = [&](int c) {
+        const int ch = c % lpr;
+        const int g = (c / lpr) % a.hkv;
+        const int tensor = c / (lpr * a.hkv);
+        const size_t slab = ((size_t)l * a.batch + b) * a.hkv + g;
+        return reinterpret_cast<const u32x4*>(static_cast<const char*>(tensor ? a.src_v : a.src_k) +
+                                              (slab * a.src_slab_rows + a.src_row0) * a.row_bytes) + ch;
+    };
+#pragma unroll
+    for (int j = 0; j < kPre; ++j)
+        if (tid + j * kPlaceThreads < total) pre[j] = *src_of(tid + j * kPlaceThreads);
     int evicted = -1;
     if (n > a.budget) {
         const Cand* cb = a.cand + (size_t)b * a.ncand;
@@ -253,18 +270,19 @@ __global__ __launch_bounds__(kPlaceThreads) void place_kernel(PlaceArgs a) {
         a.pos[(size_t)b * a.cap + slot] = a.pos[(size_t)b * a.cap + n - 1];
     }
     // the source is the cache's own row n - 1 when src_row0 == n - 1 and src is the cache: nothing to move
-    const int lpr = a.row_bytes / 16;
-    const int total = 2 * a.hkv * lpr;  // (tensor, KV head, chunk)
-    for (int c = tid; c < total; c += kPlaceThreads) {
+    auto put = [&](int c, const u32x4& x) {
         const int ch = c % lpr;
         const int g = (c / lpr) % a.hkv;
         const int tensor = c / (lpr * a.hkv);
         const size_t slab = ((size_t)l * a.batch + b) * a.hkv + g;
-        const char* src = static_cast<const char*>(tensor ? a.src_v : a.src_k) +
-                          (slab * a.src_slab_rows + a.src_row0) * a.row_bytes;
-        char* dst = static_cast<char*>(tensor ? a.v : a.k) + (slab * a.cap + slot) * a.row_bytes;
-        if (src != dst) reinterpret_cast<u32x4*>(dst)[ch] = reinterpret_cast<const u32x4*>(src)[ch];
-    }
+        u32x4* dst = reinterpret_cast<u32x4*>(static_cast<char*>(tensor ? a.v : a.k) + (slab * a.cap + slot) * a.row_bytes) +
+                     ch;
+        if (src_of(c) != dst) *dst = x;
+    };
+#pragma unroll
+    for (int j = 0; j < kPre; ++j)
+        if (tid + j * kPlaceThreads < total) put(tid + j * kPlaceThreads, pre[j]);
+    for (int c = tid + kPre * kPlaceThreads; c < total; c += kPlaceThreads) put(c, *src_of(c));
 }
 
 }  // namespace

@@ -28,6 +28,16 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
     const int tok0 = blockIdx.x * (kQuads * 4) + quad * 4;  // r rows are padded to a multiple of 64
     f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
     f32x4 racc = {0.0f, 0.0f, 0.0f, 0.0f};  // rank trace: sum over layers of the plain group sums
+    // wave 0's token (lane < 32): its utility and position are read now, their latency overlapping the layers'
+    const int tok = blockIdx.x * (kQuads * 4) + threadIdx.x;
+    const bool own = threadIdx.x < kQuads * 4 && tok < a.n;
+    const bool newcomer = own && a.new_pos >= 0 && tok == a.n - 1;  // refresh prior 0, position not yet stored
+    float u_old = 0.0f;
+    int32_t p_old = 0;
+    if (own && !newcomer) {
+        u_old = a.u[(size_t)b * a.cap + tok];
+        if (a.cand) p_old = a.pos[(size_t)b * a.cap + tok];
+    }
     if (tok0 < a.n) {
         for (int l = slice; l < a.layers; l += kSlices) {
             const float* rl = a.r + ((size_t)(l * a.batch + b) * a.r_groups) * a.n_stride + tok0;
@@ -77,17 +87,13 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
     if (threadIdx.x >= kWave) return;
     // wave 0: one token per lane (lanes >= 32 hold none) and the workgroup's eviction candidate
     EvictCand c{0xffffffffu, -1, -1};
-    const int tok = blockIdx.x * (kQuads * 4) + threadIdx.x;
-    if (threadIdx.x < kQuads * 4 && tok < a.n) {
+    if (own) {
         float tot = 0.0f;
         for (int sl = 0; sl < kSlices; ++sl) tot += partial[sl][threadIdx.x];
-        float* up = a.u + (size_t)b * a.cap + tok;
-        int32_t* pp = a.pos + (size_t)b * a.cap + tok;
-        const bool newcomer = a.new_pos >= 0 && tok == a.n - 1;  // refresh prior 0, position not yet stored
-        const float un = fmaf(a.prior_w, newcomer ? 0.0f : *up, tot);
-        *up = un;
-        if (newcomer) *pp = a.new_pos;
-        if (a.cand) c = EvictCand{float_key(un), newcomer ? a.new_pos : *pp, tok};
+        const float un = fmaf(a.prior_w, u_old, tot);
+        a.u[(size_t)b * a.cap + tok] = un;
+        if (newcomer) a.pos[(size_t)b * a.cap + tok] = a.new_pos;
+        if (a.cand) c = EvictCand{float_key(un), newcomer ? a.new_pos : p_old, tok};
         if (a.raw) {
             float rt = 0.0f;
             for (int sl = 0; sl < kSlices; ++sl) rt += partial_raw[sl][threadIdx.x];
