@@ -10,34 +10,50 @@ namespace ikv {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxBlocks = 65536;
+
+// Grid (pair blocks, (layer, KV head, tensor), sequence): a workgroup moves kMoveUnroll passes of
+// kThreads / lpr rows of one slab of K or V, each row by lpr lanes of 16 bytes; a thread issues its
+// kMoveUnroll loads before its stores (the rows are disjoint), so several loads are in flight per lane.
+constexpr int kMoveUnroll = 4;
 
 __global__ __launch_bounds__(kThreads) void move_kernel(MoveArgs a) {
     const int lpr = a.row_bytes / 16;
-    const long long total = (long long)a.batch * a.layers * a.hkv * 2 * a.max_pairs * lpr;
-    const long long stride = (long long)gridDim.x * blockDim.x;
-    for (long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x; gid < total; gid += stride) {
-        const int c = (int)(gid % lpr);
-        long long task = gid / lpr;
-        const int j = (int)(task % a.max_pairs);
-        task /= a.max_pairs;
-        const int tensor = (int)(task & 1);
-        task >>= 1;
-        const int g = (int)(task % a.hkv);
-        task /= a.hkv;
-        const int l = (int)(task % a.layers);
-        const int b = (int)(task / a.layers);
-        if (j >= a.npairs[b]) continue;
-        const int dst = a.pair_dst[(size_t)b * a.pair_stride + j];
-        const int src = a.pair_src[(size_t)b * a.pair_stride + j];
-        char* base = static_cast<char*>(tensor ? a.v : a.k);
-        const size_t slab = ((size_t)(l * a.batch + b) * a.hkv + g) * a.cap;
-        const u32x4* from = reinterpret_cast<const u32x4*>(base + (slab + src) * a.row_bytes) + c;
-        u32x4* to = reinterpret_cast<u32x4*>(base + (slab + dst) * a.row_bytes) + c;
-        *to = *from;
-        if (l == 0 && g == 0 && tensor == 0 && c == 0) {
-            a.u[(size_t)b * a.cap + dst] = a.u[(size_t)b * a.cap + src];
-            a.pos[(size_t)b * a.cap + dst] = a.pos[(size_t)b * a.cap + src];
+    const int rows_per_pass = kThreads / lpr;
+    const int b = blockIdx.z;
+    const int tensor = (int)blockIdx.y & 1;
+    const int g = ((int)blockIdx.y >> 1) % a.hkv;
+    const int l = ((int)blockIdx.y >> 1) / a.hkv;
+    const int np = a.npairs[b];
+    const int j0 = (int)blockIdx.x * rows_per_pass * kMoveUnroll + (int)threadIdx.x / lpr;
+    if (j0 >= np) return;
+    const int c = (int)threadIdx.x % lpr;
+    char* base = static_cast<char*>(tensor ? a.v : a.k) + ((size_t)(l * a.batch + b) * a.hkv + g) * a.cap * a.row_bytes;
+    const int32_t* pd = a.pair_dst + (size_t)b * a.pair_stride;
+    const int32_t* ps = a.pair_src + (size_t)b * a.pair_stride;
+    u32x4 x[kMoveUnroll];
+    int dst[kMoveUnroll];
+#pragma unroll
+    for (int i = 0; i < kMoveUnroll; ++i) {
+        const int j = j0 + i * rows_per_pass;
+        dst[i] = -1;
+        if (j < np) {
+            const int src = ps[j];
+            dst[i] = pd[j];
+            x[i] = reinterpret_cast<const u32x4*>(base + (size_t)src * a.row_bytes)[c];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < kMoveUnroll; ++i)
+        if (dst[i] >= 0) reinterpret_cast<u32x4*>(base + (size_t)dst[i] * a.row_bytes)[c] = x[i];
+    if (blockIdx.y == 0 && c == 0) {  // layer 0, KV head 0, K: the rows' utilities and positions
+#pragma unroll
+        for (int i = 0; i < kMoveUnroll; ++i) {
+            const int j = j0 + i * rows_per_pass;
+            if (j < np) {
+                const int src = ps[j];
+                a.u[(size_t)b * a.cap + pd[j]] = a.u[(size_t)b * a.cap + src];
+                a.pos[(size_t)b * a.cap + pd[j]] = a.pos[(size_t)b * a.cap + src];
+            }
         }
     }
 }
@@ -310,11 +326,12 @@ hipError_t launch_nonrefresh(const AppendArgs& a, uint8_t* keep_out, int budget,
 }
 
 hipError_t launch_move(const MoveArgs& a, hipStream_t s) {
-    const long long threads = (long long)a.batch * a.layers * a.hkv * 2 * a.max_pairs * (a.row_bytes / 16);
-    if (threads <= 0) return hipSuccess;
-    long long blocks = (threads + kThreads - 1) / kThreads;
-    if (blocks > kMaxBlocks) blocks = kMaxBlocks;
-    hipLaunchKernelGGL(move_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
+    if (a.max_pairs <= 0) return hipSuccess;
+    const int rows_per_block = kThreads / (a.row_bytes / 16) * kMoveUnroll;
+    const long long bx = (a.max_pairs + rows_per_block - 1) / rows_per_block;
+    const long long by = 2LL * a.layers * a.hkv;
+    if (bx > 0x7fffffffLL || by > 65535 || a.batch > 65535) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(move_kernel, dim3((unsigned)bx, (unsigned)by, (unsigned)a.batch), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
