@@ -14,7 +14,10 @@ constexpr int kThreads = 256;
 // Grid (pair blocks, (layer, KV head, tensor), sequence): a workgroup moves kMoveUnroll passes of
 // kThreads / lpr rows of one slab of K or V, each row by lpr lanes of 16 bytes; a thread issues its
 // kMoveUnroll loads before its stores (the rows are disjoint), so several loads are in flight per lane.
-constexpr int kMoveUnroll = 4;
+// Rows are read and written once: non-temporal loads and stores.  Step 1 at the 8B shape, same process: 4.20
+// ms with cached accesses and 4 rows per thread, 4.13 ms non-temporal; then 1 / 2 / 3 / 4 / 6 rows per thread:
+// 4.14 / 4.05 / 4.08 / 4.13 / 4.35 ms (8: 5.36 ms).
+constexpr int kMoveUnroll = 2;
 
 __global__ __launch_bounds__(kThreads) void move_kernel(MoveArgs a) {
     const int lpr = a.row_bytes / 16;
@@ -39,12 +42,12 @@ __global__ __launch_bounds__(kThreads) void move_kernel(MoveArgs a) {
         if (j < np) {
             const int src = ps[j];
             dst[i] = pd[j];
-            x[i] = reinterpret_cast<const u32x4*>(base + (size_t)src * a.row_bytes)[c];
+            x[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(base + (size_t)src * a.row_bytes) + c);
         }
     }
 #pragma unroll
     for (int i = 0; i < kMoveUnroll; ++i)
-        if (dst[i] >= 0) reinterpret_cast<u32x4*>(base + (size_t)dst[i] * a.row_bytes)[c] = x[i];
+        if (dst[i] >= 0) __builtin_nontemporal_store(x[i], reinterpret_cast<u32x4*>(base + (size_t)dst[i] * a.row_bytes) + c);
     if (blockIdx.y == 0 && c == 0) {  // layer 0, KV head 0, K: the rows' utilities and positions
 #pragma unroll
         for (int i = 0; i < kMoveUnroll; ++i) {
