@@ -28,7 +28,7 @@ struct Layout {
     int max_pairs;
     ScorePlan plan;
     size_t r_off, z_off, part_off, opart_off, npart_off, vn_off, vinv_off, eta_off, pdst_off, psrc_off, np_off;
-    size_t raw_off, rmask_off, emask_off, kmask_off, tdst_off, tsrc_off, tnp_off, cand_off, total;
+    size_t raw_off, rmask_off, emask_off, kmask_off, tdst_off, tsrc_off, tnp_off, cand_off, wide_off, total;
 };
 
 int esize(const kv_shape& s) { return s.dtype == KV_F32 ? 4 : 2; }
@@ -116,6 +116,9 @@ Layout layout_for(const kv_shape& s, int n) {
     // the fold's per-workgroup eviction candidates of a single-eviction refresh step
     L.cand_off = off;
     off = align256(off + (size_t)s.batch * fold_groups(n) * sizeof(EvictCand));
+    // the multi-workgroup selection's histograms, counts and state (long sequences in a small batch)
+    L.wide_off = off;
+    off = align256(off + select_wide_words(s.batch) * sizeof(uint32_t));
     L.total = off;
     return L;
 }
@@ -334,6 +337,7 @@ SelectArgs select_args(const kv_shape& s, const Layout& L, int n, int budget, co
     a.n = n;
     a.budget = budget;
     a.max_pairs = L.max_pairs;
+    a.wide = select_wide_words(s.batch) ? at<uint32_t>(ws, L.wide_off) : nullptr;
     return a;
 }
 

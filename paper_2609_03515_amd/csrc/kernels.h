@@ -173,8 +173,11 @@ struct SelectArgs {
     int32_t* pair_src;
     int32_t* npairs;         // [batch]
     int batch, cap, n, budget, max_pairs;
+    uint32_t* wide;          // scratch of the multi-workgroup selection (select_wide_words words)
 };
 hipError_t launch_select(const SelectArgs& a, bool plan_only, hipStream_t s);
+// Scratch words of the multi-workgroup selection for a batch (0: that path is never taken for it).
+size_t select_wide_words(int batch);
 
 // Row moves of the compaction plan for K, V, u and pos.
 struct MoveArgs {

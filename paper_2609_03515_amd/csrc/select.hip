@@ -354,10 +354,283 @@ __global__ __launch_bounds__(kThreads) void select_kernel(SelectArgs a, int plan
     }
 }
 
+// ---- Multi-workgroup selection: long sequences in a small batch ------------------------------------------
+// One workgroup per sequence leaves most of the chip idle when the batch is small and the sequences long (the
+// selection of a 128k-token first step at batch 2 took ~0.3 ms).  In the threshold case (n > B + 1) the same
+// radix select then runs as a short sequence of launches over P slices of every sequence:
+//   4 x (per-slice 256-bin histograms of the digit under the prefix found so far; one workgroup per sequence
+//   adds the slices' bins and picks the digit),
+//   one launch for ties at tau (the position select of the single-workgroup kernel; it returns at once unless
+//   more tokens tie at tau than are kept),
+//   per-slice hole and tail counts (and the decision, when asked for), then the pairs: every slice writes its
+//   holes and tails at the ranks that follow the slices before it.
+// The decisions and pairs are those of the single-workgroup kernel.  Scratch: P x 256 bins and P x 2 counts
+// per sequence, and a few state words (prefix, mask, remaining rank, tie count, position bound).
+__device__ __forceinline__ unsigned wave_sum_u(unsigned x) {
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) x += __shfl_xor(x, o, kWave);
+    return x;
+}
+
+constexpr int kWideThreads = 256;
+constexpr int kWideMaxParts = 128;
+constexpr int kWideMinRows = 16384;  // shorter sequences keep the single-workgroup kernel
+constexpr int kWideSlice = 1024;     // fewest slots per slice
+constexpr int kStateWords = 8;
+
+int wide_parts_max(int batch) {
+    const int p = 512 / batch;
+    return p < 4 ? 0 : (p > kWideMaxParts ? kWideMaxParts : p);
+}
+
+int wide_parts(int batch, int n) {
+    if (n < kWideMinRows) return 0;
+    int p = wide_parts_max(batch);
+    if (p > n / kWideSlice) p = n / kWideSlice;
+    return p < 4 ? 0 : p;
+}
+
+struct Wide {
+    unsigned* hist;  // [batch][P][256]
+    unsigned* cnt;   // [batch][P][2]
+    unsigned* st;    // [batch][kStateWords]: prefix, mask, remaining rank, ties at tau, position bound
+    int P, slice;
+    __device__ int lo(int p) const { return p * slice; }
+};
+
+Wide wide_of(const SelectArgs& a, int P) {
+    Wide w;
+    const size_t pm = (size_t)wide_parts_max(a.batch);
+    w.hist = a.wide;
+    w.cnt = a.wide + (size_t)a.batch * pm * 256;
+    w.st = w.cnt + (size_t)a.batch * pm * 2;
+    w.P = P;
+    w.slice = ((a.n + P - 1) / P + kWave - 1) / kWave * kWave;
+    return w;
+}
+
+__global__ __launch_bounds__(kWideThreads) void wide_hist_kernel(SelectArgs a, Wide w, int shift) {
+    __shared__ unsigned hist[256];
+    const int p = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const unsigned* st = w.st + (size_t)b * kStateWords;
+    const uint32_t prefix = shift == 24 ? 0u : st[0], pmask = shift == 24 ? 0u : st[1];
+    const float* ub = a.u + (size_t)b * a.cap;
+    const int lo = w.lo(p), hi = min(a.n, lo + w.slice);
+    hist[tid] = 0;
+    __syncthreads();
+    RunCounter rc;
+    for (int i0 = lo + tid; i0 < hi; i0 += kWideThreads * kBatch) {
+        uint32_t key[kBatch];
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+            const int i = i0 + j * kWideThreads;
+            key[j] = i < hi ? float_key(ub[i]) : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j)
+            if (i0 + j * kWideThreads < hi && (key[j] & pmask) == prefix) rc.add(hist, (key[j] >> shift) & 255u);
+    }
+    rc.flush(hist);
+    __syncthreads();
+    w.hist[((size_t)b * w.P + p) * 256 + tid] = hist[tid];
+}
+
+__global__ __launch_bounds__(kWideThreads) void wide_digit_kernel(SelectArgs a, Wide w, int shift) {
+    __shared__ SelShared sh;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    unsigned* st = w.st + (size_t)b * kStateWords;
+    // the slices' bins, eight loads in flight per thread
+    const unsigned* hb = w.hist + (size_t)b * w.P * 256 + tid;
+    unsigned c = 0;
+    int p = 0;
+    for (; p + 8 <= w.P; p += 8) {
+        unsigned x[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = hb[(size_t)(p + j) * 256];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) c += x[j];
+    }
+    for (; p < w.P; ++p) c += hb[(size_t)p * 256];
+    sh.hist[tid] = c;
+    const unsigned krem = shift == 24 ? (unsigned)a.budget : st[2];
+    __syncthreads();
+    find_digit(sh, krem, true);
+    __syncthreads();
+    if (tid == 0) {
+        st[0] = (shift == 24 ? 0u : st[0]) | (sh.bcast[0] << shift);
+        st[1] = (shift == 24 ? 0u : st[1]) | (255u << shift);
+        st[2] = krem - sh.bcast[1];
+        st[3] = sh.bcast[2];
+    }
+}
+
+// Ties at tau: the krem lowest positions among them are kept (position radix select, one workgroup).
+__global__ __launch_bounds__(kThreads) void wide_ties_kernel(SelectArgs a, Wide w) {
+    __shared__ SelShared sh;
+    const int b = blockIdx.x, tid = threadIdx.x;
+    unsigned* st = w.st + (size_t)b * kStateWords;
+    const uint32_t tau = st[0];
+    unsigned krem = st[2];
+    if (krem >= st[3]) {
+        if (tid == 0) st[4] = 0x7fffffffu;
+        return;
+    }
+    const float* ub = a.u + (size_t)b * a.cap;
+    const int32_t* pb = a.pos + (size_t)b * a.cap;
+    uint32_t pp = 0, pm = 0;
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        if (tid < 256) sh.hist[tid] = 0;
+        __syncthreads();
+        RunCounter rc;
+        for (int i = tid; i < a.n; i += kThreads) {
+            if (float_key(ub[i]) != tau) continue;
+            const uint32_t ps = (uint32_t)pb[i];
+            if ((ps & pm) == pp) rc.add(sh.hist, (ps >> shift) & 255u);
+        }
+        rc.flush(sh.hist);
+        __syncthreads();
+        find_digit(sh, krem, false);
+        __syncthreads();
+        pp |= sh.bcast[0] << shift;
+        pm |= 255u << shift;
+        krem -= sh.bcast[1];
+        __syncthreads();
+    }
+    if (tid == 0) st[4] = pp;
+}
+
+__device__ __forceinline__ bool wide_keep(const SelectArgs& a, const Wide& w, int b, int i) {
+    const unsigned* st = w.st + (size_t)b * kStateWords;
+    const uint32_t key = float_key(a.u[(size_t)b * a.cap + i]);
+    return key > st[0] || (key == st[0] && a.pos[(size_t)b * a.cap + i] <= (int)st[4]);
+}
+
+// Per slice: holes (dropped slots < k) and tails (kept slots >= k), and the decision when asked for.
+__global__ __launch_bounds__(kWideThreads) void wide_count_kernel(SelectArgs a, Wide w) {
+    __shared__ unsigned part[kWideThreads / kWave][2];
+    const int p = blockIdx.x, b = blockIdx.y, tid = threadIdx.x;
+    const int k = min(a.budget, a.n);
+    const int lo = w.lo(p), hi = min(a.n, lo + w.slice);
+    unsigned ch = 0, ct = 0;
+    for (int i = lo + tid; i < hi; i += kWideThreads) {
+        const bool kp = wide_keep(a, w, b, i);
+        if (a.keep_out) a.keep_out[(size_t)b * a.cap + i] = kp ? 1 : 0;
+        ch += i < k && !kp;
+        ct += i >= k && kp;
+    }
+    ch = wave_sum_u(ch);
+    ct = wave_sum_u(ct);
+    if (tid % kWave == 0) {
+        part[tid / kWave][0] = ch;
+        part[tid / kWave][1] = ct;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        unsigned h = 0, t = 0;
+        for (int j = 0; j < kWideThreads / kWave; ++j) {
+            h += part[j][0];
+            t += part[j][1];
+        }
+        w.cnt[((size_t)b * w.P + p) * 2] = h;
+        w.cnt[((size_t)b * w.P + p) * 2 + 1] = t;
+    }
+}
+
+// Pairs: wave j of a slice takes its j-th quarter (whole 64-slot groups) and writes its holes and tails at the
+// ranks after the earlier slices and quarters; the last slice records the pair count.
+__global__ __launch_bounds__(kWideThreads) void wide_plan_kernel(SelectArgs a, Wide w) {
+    constexpr int kW = kWideThreads / kWave;
+    __shared__ unsigned base[2], wc[kW][2];
+    const int p = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int k = min(a.budget, a.n);
+    const int lo = w.lo(p), hi = min(a.n, lo + w.slice);
+    if (wave == 0) {  // holes and tails of the slices before this one (P <= 128: two per lane)
+        unsigned h = 0, t = 0;
+        for (int q = lane; q < p; q += kWave) {
+            h += w.cnt[((size_t)b * w.P + q) * 2];
+            t += w.cnt[((size_t)b * w.P + q) * 2 + 1];
+        }
+        h = wave_sum_u(h);
+        t = wave_sum_u(t);
+        if (lane == 0) {
+            base[0] = h;
+            base[1] = t;
+        }
+    }
+    const int groups = hi > lo ? (hi - lo + kWave - 1) / kWave : 0;
+    const int per = (groups + kW - 1) / kW;
+    const int g0 = wave * per, g1 = min(groups, g0 + per);
+    unsigned ch = 0, ct = 0;
+    for (int g = g0; g < g1; ++g) {
+        const int i = lo + g * kWave + lane;
+        const bool in = i < hi;
+        const bool kp = in && wide_keep(a, w, b, i);
+        ch += __popcll(__ballot(in && i < k && !kp));
+        ct += __popcll(__ballot(in && i >= k && kp));
+    }
+    if (lane == 0) {
+        wc[wave][0] = ch;
+        wc[wave][1] = ct;
+    }
+    __syncthreads();
+    unsigned oh = base[0], ot = base[1];
+    for (int j = 0; j < wave; ++j) {
+        oh += wc[j][0];
+        ot += wc[j][1];
+    }
+    int32_t* pdst = a.pair_dst + (size_t)b * a.max_pairs;
+    int32_t* psrc = a.pair_src + (size_t)b * a.max_pairs;
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+    for (int g = g0; g < g1; ++g) {
+        const int i = lo + g * kWave + lane;
+        const bool in = i < hi;
+        const bool kp = in && wide_keep(a, w, b, i);
+        const bool hole = in && i < k && !kp;
+        const bool tail = in && i >= k && kp;
+        const uint64_t mh = __ballot(hole), mt = __ballot(tail);
+        if (hole) {
+            const unsigned r = oh + __popcll(mh & below);
+            if (r < (unsigned)a.max_pairs) pdst[r] = i;
+        }
+        if (tail) {
+            const unsigned r = ot + __popcll(mt & below);
+            if (r < (unsigned)a.max_pairs) psrc[r] = i;
+        }
+        oh += __popcll(mh);
+        ot += __popcll(mt);
+    }
+    if (p == w.P - 1 && tid == 0) {
+        unsigned h = base[0], t = base[1];
+        for (int j = 0; j < kW; ++j) {
+            h += wc[j][0];
+            t += wc[j][1];
+        }
+        a.npairs[b] = (int)min(min(h, t), (unsigned)a.max_pairs);
+    }
+}
+
 }  // namespace
 
+size_t select_wide_words(int batch) {
+    const size_t pm = (size_t)wide_parts_max(batch);
+    return pm ? (size_t)batch * (pm * 258 + kStateWords) : 0;
+}
+
 hipError_t launch_select(const SelectArgs& a, bool plan_only, hipStream_t s) {
-    hipLaunchKernelGGL(select_kernel, dim3(a.batch), dim3(kThreads), 0, s, a, plan_only ? 1 : 0);
+    const int P = a.wide ? wide_parts(a.batch, a.n) : 0;
+    if (plan_only || a.n <= a.budget + 1 || P == 0) {
+        hipLaunchKernelGGL(select_kernel, dim3(a.batch), dim3(kThreads), 0, s, a, plan_only ? 1 : 0);
+        return hipGetLastError();
+    }
+    const Wide w = wide_of(a, P);
+    const dim3 sliced(P, a.batch);
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        hipLaunchKernelGGL(wide_hist_kernel, sliced, dim3(kWideThreads), 0, s, a, w, shift);
+        hipLaunchKernelGGL(wide_digit_kernel, dim3(a.batch), dim3(kWideThreads), 0, s, a, w, shift);
+    }
+    hipLaunchKernelGGL(wide_ties_kernel, dim3(a.batch), dim3(kThreads), 0, s, a, w);
+    hipLaunchKernelGGL(wide_count_kernel, sliced, dim3(kWideThreads), 0, s, a, w);
+    hipLaunchKernelGGL(wide_plan_kernel, sliced, dim3(kWideThreads), 0, s, a, w);
     return hipGetLastError();
 }
 

@@ -98,6 +98,9 @@ SELECT_CASES = [
     (2, 101, 100, "ties"), (2, 101, 100, "equal"), (2, 50, 100, "random"), (2, 100, 100, "ties"),
     (2, 40000, 4000, "random"), (1, 40000, 4000, "ties"), (2, 3278, 3277, "random"), (2, 777, 1, "random"),
     (2, 777, 776, "ties"), (1, 5000, 123, "tiny"), (1, 1, 1, "random"),
+    # long sequences in a small batch: the multi-workgroup selection (slices of every sequence)
+    (4, 20000, 2000, "ties"), (2, 131073, 13107, "random"), (8, 32769, 3277, "equal"), (1, 16384, 16382, "random"),
+    (3, 50000, 100, "tiny"), (2, 20000, 19998, "ties"),
 ]
 
 

@@ -70,6 +70,8 @@ CASES = {
                                             nonrefresh_init="mean"), 12),
     "qwen_reduced": (QWEN.scaled(batch=3, layers=3, prefill_len=1000, budget=250), 5),
     "qwen_split_step1": (QWEN.scaled(batch=1, layers=2, prefill_len=3000, budget=750), 3),
+    # step 1 over 20,001 tokens at batch 2: the multi-workgroup selection and its compaction plan
+    "scorefree_wide_select": (SCOREFREE128K.scaled(batch=2, layers=2, prefill_len=20000, budget=2000), 4),
     "under_budget": (TINY.scaled(prefill_len=40, budget=45), 8),
     # Lazy steps that first only append (cache under budget), then evict one token each
     "lazy_under_budget": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=40, budget=44, nonrefresh_init="mean"), 9),
