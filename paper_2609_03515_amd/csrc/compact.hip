@@ -132,11 +132,28 @@ __global__ __launch_bounds__(kNrThreads) void nonrefresh_kernel(AppendArgs a, ui
 
     float v = use_min ? INFINITY : 0.0f;
     Cand c{0xffffffffu, -1, -1};
-    for (int i = tid; i < n; i += kNrThreads) {
-        const float ui = ub[i];
-        v = use_min ? fminf(v, ui) : v + ui;
-        const Cand o{float_key(ui), pb[i], i};
-        if (evicts_before(o, c)) c = o;
+    // kNrBatch tokens' loads in flight per thread; the reduction keeps the order of a plain sweep
+    constexpr int kNrBatch = 8;
+    for (int i0 = tid; i0 < n; i0 += kNrThreads * kNrBatch) {
+        float uu[kNrBatch];
+        int pp[kNrBatch];
+#pragma unroll
+        for (int j = 0; j < kNrBatch; ++j) {
+            const int i = i0 + j * kNrThreads;
+            if (i < n) {
+                uu[j] = ub[i];
+                pp[j] = pb[i];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kNrBatch; ++j) {
+            const int i = i0 + j * kNrThreads;
+            if (i < n) {
+                v = use_min ? fminf(v, uu[j]) : v + uu[j];
+                const Cand o{float_key(uu[j]), pp[j], i};
+                if (evicts_before(o, c)) c = o;
+            }
+        }
     }
 #pragma unroll
     for (int o = kWave / 2; o >= 1; o >>= 1) {
