@@ -191,7 +191,8 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
         // grid the device holds at once
         ScorePlan xp;
         if (kCoopSplit &&
-            attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &xp, kScoreChunkLds) &&
+            attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &xp,
+                        coop_chunk_lds(plan.group_pad)) &&
             xp.split && xp.nchunk * xp.group_pad <= kCoopMaxWords) {
             const long slabs = (long)s.layers * s.batch * s.n_kv_heads;
             long grid = coop_workgroups(s.dtype, s.head_dim, xp) / xp.nchunk * xp.nchunk;

@@ -80,6 +80,10 @@ bool attend_plan(int dtype, int head_dim, int group, int n, int slabs, ScorePlan
 #define IKV_SCORE_CHUNK_LDS (52 * 1024)
 #endif
 constexpr size_t kScoreChunkLds = IKV_SCORE_CHUNK_LDS;
+// Logit LDS of one chunk of the chunk-exchange scorer: padded groups of 8 and 16 (matrix-core logits) hold two
+// workgroups per CU by their registers anyway, so their chunks take the fast-path maximum of 80 KiB (fewer,
+// longer chunks: fewer exchange rounds; Qwen-shaped step 1 2.47 -> 2.45 ms).
+constexpr size_t coop_chunk_lds(int group_pad) { return group_pad >= 8 ? 80 * 1024 : kScoreChunkLds; }
 // Workspace bound over every call of 1..layers layers on n rows: the largest (layers of the call) x nchunk,
 // and whether any such call splits.
 struct AttendBound {

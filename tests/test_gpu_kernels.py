@@ -36,7 +36,8 @@ SCORE_CASES = [
     ("f32", 64, 2, 1, 10500, 1, 1, False),    # f32 split path
     ("bf16", 128, 4, 1, 1, 1, 1, False),      # a single cached token
     ("bf16", 128, 8, 2, 40000, 1, 1, True),   # split path: 13 chunks exchanging their statistics
-    ("bf16", 128, 32, 2, 14000, 1, 1, False),  # group 16, 17 chunks: too many to exchange, logits + finish
+    ("bf16", 128, 32, 2, 14000, 1, 1, False),  # group 16, 11 chunks of 80 KiB exchanging their statistics
+    ("bf16", 128, 32, 2, 24000, 1, 1, True),  # group 16, 19 chunks: too many to exchange, logits + finish
     ("bf16", 128, 10, 2, 701, 1, 2, True),    # group 5: three padded heads in the matrix-core tile
     ("bf16", 128, 24, 2, 509, 1, 2, False),   # group 12 (padded group 16)
     ("bf16", 64, 12, 2, 20001, 1, 1, True),   # group 6, d = 64: one line per row, chunks exchanging statistics
