@@ -15,8 +15,10 @@
  * Conventions for every call
  *  - Buffer pointers are DEVICE pointers owned by the caller; the library never allocates, frees or
  *    synchronises device memory and never reads them on the host.  Scratch comes from a caller workspace of
- *    at least kv_workspace_bytes() bytes, 256-byte aligned (contents need no initialisation); calls that
- *    share a workspace must not overlap in time.
+ *    at least kv_workspace_bytes() bytes, 256-byte aligned; calls that share a workspace must not overlap in
+ *    time.  The workspace's first 4 bytes are its sticky fault word (kv_fault bits, set by the device when a
+ *    call could not produce valid results): zero it once after allocating the workspace (kv_fault_status with
+ *    clear, or any zero fill) and read it with kv_fault_status.  The rest needs no initialisation.
  *  - Work is queued asynchronously on `stream` (a hipStream_t; NULL = the default stream) in stream order.
  *  - Arguments are validated on the host before anything is queued; an invalid call returns a negative
  *    kv_status and queues nothing.  KV_ERR_HIP reports a failed launch (hipGetLastError).
@@ -32,8 +34,14 @@
  *  - Preconditions not checked on the device: keys, queries and utilities are finite; utilities are >= 0
  *    when produced by this library; positions are unique within a sequence.
  *  - The calls keep no state between calls (apart from per-device caches of kernel attributes and occupancy,
- *    filled on first use under atomics) and may run concurrently, from several host threads, on different
- *    streams with disjoint buffers.
+ *    filled on first use under atomics, and the exchange wait limit below) and may run concurrently, from
+ *    several host threads, on different streams with disjoint buffers and workspaces, with one exception: a
+ *    refresh step whose slabs are too long for one workgroup's LDS (kv_score_plan reports path
+ *    KV_PATH_EXCHANGE, e.g. the first decode step over a 32k-token prefill) scores them with chunks that wait
+ *    for one another's softmax statistics, on a grid sized to the workgroups the device holds at once.  Such a
+ *    call needs the device to itself while it runs: when other work (another stream or process) holds CUs,
+ *    a slab's later chunks may not start while its earlier ones wait.  Every wait is bounded; a chunk that
+ *    gives up sets its scores to NaN and raises KV_FAULT_EXCHANGE_TIMEOUT in the workspace's fault word.
  */
 #ifndef INERTIAKV_H
 #define INERTIAKV_H
@@ -54,6 +62,11 @@ typedef enum {
 } kv_status;
 
 typedef enum { KV_F32 = 0, KV_BF16 = 1 } kv_dtype;
+
+/* Bits of the workspace's fault word.  KV_FAULT_EXCHANGE_TIMEOUT: a chunk of a long-slab scorer (path
+ * KV_PATH_EXCHANGE) did not receive its peers' softmax statistics within the wait limit; its scores, and
+ * everything computed from them by that call (utilities, retention decision, compaction), are invalid. */
+typedef enum { KV_FAULT_EXCHANGE_TIMEOUT = 1 } kv_fault;
 
 /* Prior utility of the token appended on a NON-refresh step (appendix "New token insertion": MEAN). */
 typedef enum { KV_INIT_MEAN = 0, KV_INIT_MIN = 1 } kv_init;
@@ -152,6 +165,29 @@ kv_status kv_workspace_bytes(const kv_shape* shape, int32_t n_max, size_t* bytes
  * the automatic choice reads the device's CU count.  KV_ERR_INVALID_ARG as kv_evict_step for bad params. */
 kv_status kv_score_merge(const kv_shape* shape, int32_t n, const kv_params* params, int32_t* merge);
 
+/* How a refresh step over n cached tokens (after the append) scores them on the current device (host only):
+ * merge as kv_score_merge; path KV_PATH_LDS (one workgroup per slab, logits in LDS), KV_PATH_EXCHANGE (slabs
+ * too long for that, cut into `chunks` chunks that exchange their softmax statistics: see the concurrency
+ * note above) or KV_PATH_LOGITS (chunks that write their logits to the workspace for a finish pass: slabs with
+ * more statistics than one exchange grid handles); chunks = workgroups per slab. */
+typedef enum { KV_PATH_LDS = 0, KV_PATH_EXCHANGE = 1, KV_PATH_LOGITS = 2 } kv_score_path;
+typedef struct {
+    int32_t merge;
+    int32_t path;
+    int32_t chunks;
+} kv_score_info;
+kv_status kv_score_plan(const kv_shape* shape, int32_t n, const kv_params* params, kv_score_info* info);
+
+/* Fault word of a workspace (see the conventions above), in stream order: *out (DEVICE, nullable) receives
+ * the kv_fault bits set since the word was last cleared; clear != 0 then zeroes the word.  Asynchronous like
+ * every call: read *out after synchronising the stream.  KV_ERR_INVALID_ARG when out is NULL and clear is 0. */
+kv_status kv_fault_status(void* ws, size_t ws_bytes, uint32_t* out, int32_t clear, void* stream);
+
+/* Polls a waiting chunk of the exchange path makes before it gives up (process-wide; default, or polls < 0:
+ * about 0.1 s of sleeps, far beyond any chunk's streaming time; 0: give up without waiting, every chunk then
+ * reports KV_FAULT_EXCHANGE_TIMEOUT).  For tests of the fault report.  Returns the previous limit. */
+int32_t kv_set_exchange_wait_limit(int32_t polls);
+
 /* Scoring + fold (Eq. 1 and Eq. 4, layer-sequential).  For every layer l = 1..K, query head h and cached
  * token i < n: z_h(i) = q_h . k_i / sqrt(d) (+ recency_bias if pos[i] >= cur_pos - (recency_window - 1)),
  * a_h = softmax over the n tokens, s_l(i) = (1/H) sum_h a_h(i); then u <- alpha u + (1 - alpha) s_l for
@@ -165,11 +201,13 @@ kv_status kv_score_ema(const kv_shape* shape, int32_t n, const void* q, const vo
 kv_status kv_topk_select(const kv_shape* shape, int32_t n, int32_t budget, const float* u, const int32_t* pos,
                          uint8_t* keep, void* ws, size_t ws_bytes, void* stream);
 
-/* Hole-fill compaction of a retention decision (which must keep exactly min(B, n) tokens per sequence):
- * with k = min(B, n), the kept rows in slots >= k move, in ascending order, into the dropped slots < k, in
- * ascending order, for every layer and KV head of K and V, and for u and pos.  Rows [0, k) then hold exactly
- * the retained tokens; rows >= k are left as they were.  A mask that keeps a different count is rejected on
- * the device by moving nothing beyond the smaller of the two lists. */
+/* Hole-fill compaction of a retention decision (which must keep exactly min(B, n) tokens per sequence).
+ * Sec. 3: eviction is irreversible, the evicted tokens' K/V pairs leave the cache and the retained ones stay;
+ * the paper leaves the row layout open (attention does not depend on row order), and this call reads it as
+ * the layout that moves the fewest rows: with k = min(B, n), the kept rows in slots >= k move, in ascending
+ * order, into the dropped slots < k, in ascending order, for every layer and KV head of K and V, and for u
+ * and pos.  Rows [0, k) then hold exactly the retained tokens; rows >= k are left as they were.  A mask that
+ * keeps a different count is rejected on the device by moving nothing beyond the smaller of the two lists. */
 kv_status kv_compact(const kv_shape* shape, int32_t n, int32_t budget, const uint8_t* keep, void* k, void* v,
                      float* u, int32_t* pos, void* ws, size_t ws_bytes, void* stream);
 

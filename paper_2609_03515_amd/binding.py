@@ -20,12 +20,14 @@ KV_INIT_MEAN, KV_INIT_MIN = 0, 1
 KV_RULE_EMA, KV_RULE_SINGLE_STEP, KV_RULE_CUMULATIVE = 0, 1, 2
 KV_SCORE_ATTENTION, KV_SCORE_VNORM, KV_SCORE_ENTROPY, KV_SCORE_NORMS_EMITTED = 0, 1, 2, 4
 KV_EMIT_SCORES, KV_EMIT_VNORMS = 1, 2
+KV_FAULT_EXCHANGE_TIMEOUT = 1
+KV_PATH_LDS, KV_PATH_EXCHANGE, KV_PATH_LOGITS = 0, 1, 2
 KV_PHASES = 5
 PHASES = ("append", "score", "fold", "select", "compact")
 
 EXPORTED = ("kv_workspace_bytes", "kv_score_ema", "kv_topk_select", "kv_compact", "kv_evict_step",
             "kv_append", "kv_attend_score", "kv_evict_finish", "kv_rank_trace_state_bytes", "kv_score_merge",
-            "kv_status_string")
+            "kv_score_plan", "kv_fault_status", "kv_set_exchange_wait_limit", "kv_status_string")
 KV_TRACE_COUNTS = 10
 
 
@@ -50,6 +52,10 @@ class KvParams(ctypes.Structure):
 
 class KvTrace(ctypes.Structure):
     _fields_ = [("begin", ctypes.c_void_p * KV_PHASES), ("end", ctypes.c_void_p * KV_PHASES)]
+
+
+class KvScoreInfo(ctypes.Structure):
+    _fields_ = [("merge", ctypes.c_int32), ("path", ctypes.c_int32), ("chunks", ctypes.c_int32)]
 
 
 class KvRankTrace(ctypes.Structure):
@@ -83,6 +89,9 @@ def load_library(path: str = LIB_PATH):
                                     vp]
     lib.kv_rank_trace_state_bytes.argtypes = [i32, i32, ctypes.POINTER(sz)]
     lib.kv_score_merge.argtypes = [shp, i32, prm, ctypes.POINTER(i32)]
+    lib.kv_score_plan.argtypes = [shp, i32, prm, ctypes.POINTER(KvScoreInfo)]
+    lib.kv_fault_status.argtypes = [vp, sz, vp, i32, vp]
+    lib.kv_set_exchange_wait_limit.argtypes = [i32]
     for fn in EXPORTED[:-1]:
         getattr(lib, fn).restype = i32
     lib.kv_status_string.argtypes = [i32]
@@ -149,6 +158,24 @@ def kv_score_merge(shape: KvShape, n: int, params: KvParams) -> int:
     _check("kv_score_merge", load_library().kv_score_merge(ctypes.byref(shape), int(n), ctypes.byref(params),
                                                             ctypes.byref(out)))
     return out.value
+
+
+def kv_score_plan(shape: KvShape, n: int, params: KvParams) -> KvScoreInfo:
+    out = KvScoreInfo()
+    _check("kv_score_plan", load_library().kv_score_plan(ctypes.byref(shape), int(n), ctypes.byref(params),
+                                                          ctypes.byref(out)))
+    return out
+
+
+def kv_fault_status(ws, out=None, clear=False, stream=None):
+    """Queues the copy of the workspace's fault word into `out` (a device int32/uint32 tensor of one element,
+    or None) and/or its clearing."""
+    _check("kv_fault_status", load_library().kv_fault_status(_ptr(ws), _ws_bytes(ws), _ptr(out), int(bool(clear)),
+                                                              _stream(stream)))
+
+
+def kv_set_exchange_wait_limit(polls: int) -> int:
+    return int(load_library().kv_set_exchange_wait_limit(int(polls)))
 
 
 def kv_score_ema(shape, n, q, k, pos, cur_pos, alpha, recency_bias, recency_window, u, s_out, ws, stream=None):
@@ -227,9 +254,19 @@ def kv_evict_finish(shape, params, t, n, k, v, u, pos, ws, keep_out=None, s_out=
 
 
 def workspace(shape: KvShape, n_max: int, device="cuda") -> torch.Tensor:
-    """A caller-owned workspace tensor of kv_workspace_bytes() bytes (256-byte aligned by the allocator)."""
+    """A caller-owned workspace tensor of kv_workspace_bytes() bytes (256-byte aligned by the allocator), its
+    fault word cleared on the current stream."""
     nbytes = kv_workspace_bytes(shape, n_max)
-    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+    ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+    kv_fault_status(ws, None, clear=True)
+    return ws
+
+
+def faults(ws, clear=False) -> int:
+    """The workspace's fault word (kv_fault bits), read after synchronising the current stream."""
+    out = torch.zeros(1, dtype=torch.int32, device=ws.device)
+    kv_fault_status(ws, out, clear=clear)
+    return int(out.item()) & 0xffffffff
 
 
 # --- HIP events for the timing hooks (runtime plumbing, no computation) -------------------------------------

@@ -23,6 +23,10 @@ constexpr size_t kSplitLogitBytes = (size_t)IKV_SPLIT_LOGIT_MIB << 20;
 #endif
 constexpr bool kCoopSplit = IKV_COOP_SPLIT != 0;
 
+// The workspace's first 256 bytes hold the sticky fault word (kv_fault bits), at the same place for every n.
+constexpr size_t kFaultBytes = 256;
+static_assert(kFaultExchangeTimeout == (uint32_t)KV_FAULT_EXCHANGE_TIMEOUT, "fault bits of the kernels and the ABI");
+
 struct Layout {
     int n_stride;
     int max_pairs;
@@ -74,7 +78,7 @@ Layout layout_for(const kv_shape& s, int n) {
             if (sp > part_bytes) part_bytes = sp;
         }
     }
-    size_t off = 0;
+    size_t off = kFaultBytes;
     L.r_off = off;
     off = align256(off + (size_t)s.layers * s.batch * s.n_kv_heads * L.n_stride * sizeof(float));
     L.z_off = off;
@@ -177,6 +181,51 @@ ScorePlan scorer_plan(const kv_shape& s, const Layout& L, int variant, int merge
     return plan;
 }
 
+// How a refresh step's scorer runs over n rows: one workgroup per slab with its logits in LDS; or, for slabs
+// too long for that, chunks that exchange their softmax statistics and write the group sums directly (on a
+// grid the device holds at once); or chunks that write logits for a finish kernel (slabs with more exchange
+// words than one chunk grid handles).
+struct ScoreRoute {
+    enum Kind { kLds = 0, kExchange = 1, kLogits = 2 } kind;
+    ScorePlan xp;  // kExchange: the chunk plan
+    long grid;     // kExchange: workgroups of the persistent grid
+};
+
+// Layers per launch of the logits path: groups whose logits fit kSplitLogitBytes (read back by the finish
+// kernel while they may still be cached).
+int logit_layer_group(const kv_shape& s, const Layout& L) {
+    const size_t layer_logits = (size_t)s.batch * s.n_q_heads * L.n_stride * sizeof(float);
+    const size_t fit = kSplitLogitBytes / layer_logits;
+    return fit < 1 ? 1 : (fit > (size_t)s.layers ? s.layers : (int)fit);
+}
+
+static_assert((int)ScoreRoute::kLds == KV_PATH_LDS && (int)ScoreRoute::kExchange == KV_PATH_EXCHANGE &&
+                  (int)ScoreRoute::kLogits == KV_PATH_LOGITS,
+              "scorer paths of the planner and the ABI");
+
+ScoreRoute score_route(const kv_shape& s, const Layout& L, int n, const ScorePlan& plan) {
+    ScoreRoute r{ScoreRoute::kLds, plan, 0};
+    if (!plan.split) return r;
+    r.kind = ScoreRoute::kLogits;
+    const int group = s.n_q_heads / s.n_kv_heads;
+    ScorePlan xp;
+    if (kCoopSplit &&
+        attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &xp,
+                    coop_chunk_lds(plan.group_pad)) &&
+        xp.split && xp.nchunk * xp.group_pad <= kCoopMaxWords) {
+        const long slabs = (long)s.layers * s.batch * s.n_kv_heads;
+        long grid = coop_workgroups(s.dtype, s.head_dim, xp) / xp.nchunk * xp.nchunk;
+        if (grid > slabs * xp.nchunk) grid = slabs * xp.nchunk;
+        if (grid >= xp.nchunk &&
+            (size_t)s.layers * s.batch * s.n_q_heads * xp.nchunk * sizeof(uint64_t) <= L.opart_off - L.part_off) {
+            r.kind = ScoreRoute::kExchange;
+            r.xp = xp;
+            r.grid = grid;
+        }
+    }
+    return r;
+}
+
 // Scoring (Eq. 1) of rows [0, n) of every layer into the workspace r: [layers][batch][n_kv / merge] rows.
 // k_new (one workgroup per slab only): row n - 1 is the step's newcomer, read from k_new instead of the cache,
 // with position cur_pos.
@@ -187,32 +236,18 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
     ScorePlan plan = splan;
     if (plan.split) {
         const int group = s.n_q_heads / s.n_kv_heads;
-        // long slabs: chunks that exchange their softmax statistics and write the group sums directly, on a
-        // grid the device holds at once
-        ScorePlan xp;
-        if (kCoopSplit &&
-            attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &xp,
-                        coop_chunk_lds(plan.group_pad)) &&
-            xp.split && xp.nchunk * xp.group_pad <= kCoopMaxWords) {
-            const long slabs = (long)s.layers * s.batch * s.n_kv_heads;
-            long grid = coop_workgroups(s.dtype, s.head_dim, xp) / xp.nchunk * xp.nchunk;
-            if (grid > slabs * xp.nchunk) grid = slabs * xp.nchunk;
-            if (grid >= xp.nchunk &&
-                (size_t)s.layers * s.batch * s.n_q_heads * xp.nchunk * sizeof(uint64_t) <= L.opart_off - L.part_off) {
-                a.v = k;
-                a.chunk_rows = xp.chunk_rows;
-                a.nchunk = xp.nchunk;
-                a.emit = 1;
-                return hip_status(launch_score_coop(s.dtype, s.head_dim, xp, a, at<uint64_t>(ws, L.part_off),
-                                                    (int)grid, st));
-            }
+        const ScoreRoute route = score_route(s, L, n, plan);
+        if (route.kind == ScoreRoute::kExchange) {
+            a.v = k;
+            a.chunk_rows = route.xp.chunk_rows;
+            a.nchunk = route.xp.nchunk;
+            a.emit = 1;
+            return hip_status(launch_score_coop(s.dtype, s.head_dim, route.xp, a, at<uint64_t>(ws, L.part_off),
+                                                (int)route.grid, at<uint32_t>(ws, 0), st));
         }
-        // otherwise LDS-resident chunks of the attention kernel's K pass that write logits, then the finish
-        // kernel, for groups of layers whose logits fit kSplitLogitBytes (read back while they may still be
-        // cached)
-        const size_t layer_logits = (size_t)s.batch * s.n_q_heads * L.n_stride * sizeof(float);
-        const size_t fit = kSplitLogitBytes / layer_logits;
-        const int lg = fit < 1 ? 1 : (fit > (size_t)s.layers ? s.layers : (int)fit);
+        // LDS-resident chunks of the attention kernel's K pass that write logits, then the finish kernel, per
+        // group of layers
+        const int lg = logit_layer_group(s, L);
         const size_t e = (size_t)esize(s);
         for (int l0 = 0; l0 < s.layers; l0 += lg) {
             const int lc = s.layers - l0 < lg ? s.layers - l0 : lg;
@@ -516,6 +551,94 @@ kv_status run_place(const kv_shape& s, const Layout& L, int n, int budget, const
     return hip_status(launch_place(a, st));
 }
 
+kv_status check_step(const kv_shape* shape, const kv_params* params, int t, int n_in, int new_pos, const void* q,
+                     const void* k_new, const void* v_new, const void* k, const void* v, const float* u,
+                     const int32_t* pos, const int32_t* n_out, const float* s_out, const kv_rank_trace* rank_trace) {
+    kv_status rc = check_shape(shape);
+    if (rc != KV_OK) return rc;
+    const kv_shape& s = *shape;
+    if ((rc = check_params(params)) != KV_OK) return rc;
+    if ((rc = check_rank_trace(rank_trace)) != KV_OK) return rc;
+    if ((rc = check_merge(s, *params)) != KV_OK) return rc;
+    if (!n_out) return KV_ERR_INVALID_ARG;
+    if (t < 1 || n_in < 0 || n_in + 1 > s.capacity || new_pos < 0) return KV_ERR_INVALID_ARG;
+    if (!q || !k_new || !v_new || !k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
+    if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k, 16) || !aligned(v, 16) ||
+        !aligned(u, 4) || !aligned(pos, 4) || !aligned(s_out, 4))
+        return KV_ERR_UNSUPPORTED;
+    return KV_OK;
+}
+
+// One decode step (a0 ... a5) on validated arguments, with the workspace ws laid out as L.
+kv_status evict_step(const kv_shape& s, const kv_params& p, int t, int n_in, int new_pos, const void* q,
+                     const void* k_new, const void* v_new, void* k, void* v, float* u, int32_t* pos, int32_t* n_out,
+                     uint8_t* keep_out, float* s_out, const kv_trace* trace, const kv_rank_trace* rank_trace,
+                     const Layout& L, void* ws, hipStream_t st) {
+    kv_status rc = KV_OK;
+    const int n = n_in + 1;
+    const bool refresh = is_refresh(p, t);
+    if (!refresh && n_in <= p.budget) {
+        // every Lazy / Score-Free step after the first: one kernel per sequence
+        AppendArgs ap = append_args(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos);
+        if (rank_trace && (rc = mark_untraced(s, rank_trace, st)) != KV_OK) return rc;
+        record(trace, 0, true, st);
+        // the per-sequence pair counts of the workspace are free on this path: they carry the newcomer's slot
+        rc = hip_status(launch_nonrefresh(ap, keep_out, p.budget, at<int32_t>(ws, L.np_off), st));
+        record(trace, 0, false, st);
+        if (rc != KV_OK) return rc;
+        *n_out = n < p.budget ? n : p.budget;
+        return KV_OK;
+    }
+    if (refresh && n_in <= p.budget && !rank_trace && !(p.score_variant & KV_SCORE_VNORM)) {
+        const ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
+        if (!plan.split) {
+            // A steady refresh step (one eviction, or none while under budget) in three kernels: the scorer
+            // takes the newcomer from k_new as row n - 1, the fold gives it the refresh prior and reports each
+            // workgroup's first token to leave, and the placement writes the newcomer's rows once, into the
+            // slot it takes (the append's and the compaction's row copies in one).
+            const int r_groups = s.n_kv_heads / plan.merge;
+            record(trace, 0, true, st);
+            record(trace, 0, false, st);
+            record(trace, 1, true, st);
+            rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, plan, ws, st, k_new);
+            if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st);
+            record(trace, 1, false, st);
+            FoldExtra ex;
+            ex.pos = pos;
+            ex.new_pos = new_pos;
+            ex.candidates = n > p.budget;
+            if (rc == KV_OK)
+                rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, r_groups, 1, false, ws, st, trace,
+                              ex);
+            record(trace, 3, true, st);
+            if (rc == KV_OK) rc = run_place(s, L, n, p.budget, k_new, v_new, k, v, u, pos, keep_out, ws, st);
+            record(trace, 3, false, st);
+            record(trace, 4, true, st);
+            record(trace, 4, false, st);
+            if (rc != KV_OK) return rc;
+            *n_out = n < p.budget ? n : p.budget;
+            return KV_OK;
+        }
+    }
+    if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, st, trace)) != KV_OK) return rc;
+    if (refresh) {
+        const ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
+        const int r_groups = s.n_kv_heads / plan.merge;
+        record(trace, 1, true, st);
+        rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, plan, ws, st);
+        if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st);
+        record(trace, 1, false, st);
+        if (rc == KV_OK)
+            rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, r_groups, 1, rank_trace != nullptr,
+                          ws, st, trace);
+        if (rc != KV_OK) return rc;
+    }
+    rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, trace);
+    if (rc != KV_OK) return rc;
+    *n_out = n < p.budget ? n : p.budget;
+    return KV_OK;
+}
+
 }  // namespace
 }  // namespace ikv
 
@@ -602,85 +725,13 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
                         float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
                         const kv_trace* trace, const kv_rank_trace* rank_trace, void* ws, size_t ws_bytes,
                         void* stream) {
-    kv_status rc = check_shape(shape);
+    kv_status rc = check_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, n_out, s_out,
+                              rank_trace);
     if (rc != KV_OK) return rc;
-    const kv_shape& s = *shape;
-    if ((rc = check_params(params)) != KV_OK) return rc;
-    if ((rc = check_rank_trace(rank_trace)) != KV_OK) return rc;
-    const kv_params& p = *params;
-    if ((rc = check_merge(s, p)) != KV_OK) return rc;
-    if (!n_out) return KV_ERR_INVALID_ARG;
-    if (t < 1 || n_in < 0 || n_in + 1 > s.capacity || new_pos < 0) return KV_ERR_INVALID_ARG;
-    if (!q || !k_new || !v_new || !k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
-    if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k, 16) || !aligned(v, 16) ||
-        !aligned(u, 4) || !aligned(pos, 4) || !aligned(s_out, 4))
-        return KV_ERR_UNSUPPORTED;
-    const int n = n_in + 1;
-    const Layout L = layout_for(s, n);
+    const Layout L = layout_for(*shape, n_in + 1);
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-
-    const bool refresh = is_refresh(p, t);
-    if (!refresh && n_in <= p.budget) {
-        // every Lazy / Score-Free step after the first: one kernel per sequence
-        AppendArgs ap = append_args(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos);
-        if (rank_trace && (rc = mark_untraced(s, rank_trace, st)) != KV_OK) return rc;
-        record(trace, 0, true, st);
-        // the per-sequence pair counts of the workspace are free on this path: they carry the newcomer's slot
-        rc = hip_status(launch_nonrefresh(ap, keep_out, p.budget, at<int32_t>(ws, L.np_off), st));
-        record(trace, 0, false, st);
-        if (rc != KV_OK) return rc;
-        *n_out = n < p.budget ? n : p.budget;
-        return KV_OK;
-    }
-    if (refresh && n_in <= p.budget && !rank_trace && !(p.score_variant & KV_SCORE_VNORM)) {
-        const ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
-        if (!plan.split) {
-            // A steady refresh step (one eviction, or none while under budget) in three kernels: the scorer
-            // takes the newcomer from k_new as row n - 1, the fold gives it the refresh prior and reports each
-            // workgroup's first token to leave, and the placement writes the newcomer's rows once, into the
-            // slot it takes (the append's and the compaction's row copies in one).
-            const int r_groups = s.n_kv_heads / plan.merge;
-            record(trace, 0, true, st);
-            record(trace, 0, false, st);
-            record(trace, 1, true, st);
-            rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, plan, ws, st, k_new);
-            if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st);
-            record(trace, 1, false, st);
-            FoldExtra ex;
-            ex.pos = pos;
-            ex.new_pos = new_pos;
-            ex.candidates = n > p.budget;
-            if (rc == KV_OK)
-                rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, r_groups, 1, false, ws, st, trace,
-                              ex);
-            record(trace, 3, true, st);
-            if (rc == KV_OK) rc = run_place(s, L, n, p.budget, k_new, v_new, k, v, u, pos, keep_out, ws, st);
-            record(trace, 3, false, st);
-            record(trace, 4, true, st);
-            record(trace, 4, false, st);
-            if (rc != KV_OK) return rc;
-            *n_out = n < p.budget ? n : p.budget;
-            return KV_OK;
-        }
-    }
-    if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, st, trace)) != KV_OK) return rc;
-    if (refresh) {
-        const ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
-        const int r_groups = s.n_kv_heads / plan.merge;
-        record(trace, 1, true, st);
-        rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, plan, ws, st);
-        if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st);
-        record(trace, 1, false, st);
-        if (rc == KV_OK)
-            rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, r_groups, 1, rank_trace != nullptr,
-                          ws, st, trace);
-        if (rc != KV_OK) return rc;
-    }
-    rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, trace);
-    if (rc != KV_OK) return rc;
-    *n_out = n < p.budget ? n : p.budget;
-    return KV_OK;
+    return evict_step(*shape, *params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, n_out, keep_out, s_out,
+                      trace, rank_trace, L, ws, static_cast<hipStream_t>(stream));
 }
 
 kv_status kv_append(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in, int32_t new_pos,
@@ -787,6 +838,41 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
     *n_out = n < p.budget ? n : p.budget;
     return KV_OK;
 }
+
+kv_status kv_score_plan(const kv_shape* shape, int32_t n, const kv_params* params, kv_score_info* info) {
+    kv_status rc = check_shape(shape);
+    if (rc != KV_OK) return rc;
+    if ((rc = check_params(params)) != KV_OK) return rc;
+    const kv_shape& s = *shape;
+    if ((rc = check_merge(s, *params)) != KV_OK) return rc;
+    if (!info || n < 1 || n > s.capacity) return KV_ERR_INVALID_ARG;
+    const Layout L = layout_for(s, n);
+    const ScorePlan plan = scorer_plan(s, L, params->score_variant, params->score_merge);
+    const ScoreRoute route = score_route(s, L, n, plan);
+    info->merge = plan.merge;
+    info->path = (int32_t)route.kind;
+    info->chunks = 1;
+    if (route.kind == ScoreRoute::kExchange) {
+        info->chunks = route.xp.nchunk;
+    } else if (route.kind == ScoreRoute::kLogits) {
+        ScorePlan cp;
+        const int group = s.n_q_heads / s.n_kv_heads;
+        const int lc = logit_layer_group(s, L);
+        if (!attend_plan(s.dtype, s.head_dim, group, n, lc * s.batch * s.n_kv_heads, &cp, kScoreChunkLds))
+            return KV_ERR_UNSUPPORTED;
+        info->chunks = cp.nchunk;
+    }
+    return KV_OK;
+}
+
+kv_status kv_fault_status(void* ws, size_t ws_bytes, uint32_t* out, int32_t clear, void* stream) {
+    if (!ws || ws_bytes < kFaultBytes) return KV_ERR_WORKSPACE;
+    if (!aligned(ws, 256) || !aligned(out, 4)) return KV_ERR_INVALID_ARG;
+    if (!out && !clear) return KV_ERR_INVALID_ARG;
+    return hip_status(launch_fault_word(static_cast<uint32_t*>(ws), out, clear != 0, static_cast<hipStream_t>(stream)));
+}
+
+int32_t kv_set_exchange_wait_limit(int32_t polls) { return set_exchange_wait_limit(polls); }
 
 kv_status kv_rank_trace_state_bytes(int32_t batch, int32_t max_pos, size_t* bytes) {
     if (batch < 1 || max_pos < 1 || !bytes) return KV_ERR_INVALID_ARG;

@@ -12,6 +12,12 @@ constexpr int kMaxGroup = 16;
 constexpr int kMaxMerge = 8;   // KV heads one scoring workgroup may add up
 constexpr size_t kLdsPerCu = 160 * 1024;  // gfx950
 
+// Bits of the workspace's sticky fault word (the ABI's kv_fault values).
+constexpr uint32_t kFaultExchangeTimeout = 1u;  // a first-step scoring chunk gave up waiting for its peers
+
+// Compute units of the current device (cached per device; 0 when the query fails).
+int device_cus();
+
 // Scoring of one step (Eq. 1).  One workgroup streams a whole (layer, sequence, KV head) slab and keeps its
 // logits in LDS, writing the group probability sums r.  Slabs too long for that are cut into chunks
 // (launch_score_chunks): the chunks write logits z and per-head partial (max, sum) pairs, and a finish kernel
@@ -98,11 +104,17 @@ hipError_t launch_score_chunks(int dtype, int head_dim, const ScorePlan& plan, c
 // Scoring of long slabs in chunks that exchange their softmax statistics instead of writing logits: plan
 // (chunk_rows, nchunk, lds_bytes) from attend_plan with at most kCoopMaxWords / group_pad chunks; grid = a
 // multiple of nchunk no larger than coop_workgroups() (the workgroups the device holds at once).  xchg: zeroed
-// here, then one 64-bit word per (layer, sequence, query head, chunk).
+// here, then one 64-bit word per (layer, sequence, query head, chunk).  A chunk whose peers' words do not all
+// arrive within the wait limit sets its group sums to NaN and ORs kFaultExchangeTimeout into *faults.
 constexpr int kCoopMaxWords = 4 * 64;
 int coop_workgroups(int dtype, int head_dim, const ScorePlan& plan);
 hipError_t launch_score_coop(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg,
-                             int grid, hipStream_t s);
+                             int grid, uint32_t* faults, hipStream_t s);
+// Polls of the exchange wait (< 0: the default, about 0.1 s of sleeps; 0: give up at once); returns the
+// previous limit.  Process-wide.
+int set_exchange_wait_limit(int polls);
+// Fault word: zeroes it, or copies it to `out` (device) and optionally zeroes it, in stream order.
+hipError_t launch_fault_word(uint32_t* word, uint32_t* out, bool clear, hipStream_t s);
 
 // Eviction candidate of a range of tokens: the token that leaves first under (u ascending, position
 // descending), as the order-preserving key of its utility, its position and its slot (-1: none).

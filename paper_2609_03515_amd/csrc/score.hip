@@ -329,6 +329,19 @@ hipError_t launch_d(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
 
 }  // namespace
 
+int device_cus() {
+    static std::atomic<int> cached[kMaxDevices];  // CU count + 1; 0 = not queried yet
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+    if (dev < kMaxDevices) {
+        const int c = cached[dev].load(std::memory_order_relaxed);
+        if (c > 0) return c - 1;
+    }
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) return 0;
+    if (dev < kMaxDevices) cached[dev].store(cus + 1, std::memory_order_relaxed);
+    return cus;
+}
+
 bool score_plan(int dtype, int head_dim, int group, int n, ScorePlan* plan) {
     if (group < 1 || group > kMaxGroup || n < 1) return false;
     if (head_dim != 64 && head_dim != 128) return false;
@@ -380,12 +393,10 @@ int score_merge(ScorePlan* plan, int dtype, int head_dim, int hkv, int lb_count,
     if (forced > 0) {
         best = forced;
     } else {
-        int dev = 0, cus = 0;
+        const int cus = device_cus();
         const int occ1 = kernel_occupancy(dtype, head_dim, plan->group_pad, false);
         const int occm = ldsm <= kFastLdsMax ? kernel_occupancy(dtype, head_dim, plan->group_pad, true) : 0;
-        if (occ1 < 1 || hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
-            return 1;
+        if (occ1 < 1 || cus < 1) return 1;
         long best_cost = -1;
         bool best_conc = false;
         for (int m = 1; m <= kMaxMerge && m <= hkv; ++m) {

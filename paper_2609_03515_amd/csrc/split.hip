@@ -11,8 +11,13 @@
 //
 // The grid is persistent and no larger than the workgroups the chip holds at once: workgroup w always takes
 // chunk w % C of slabs w / C, w / C + P, ... (P = grid / C slabs per round), so the C chunks of a slab are
-// consecutive workgroups that are dispatched together and only ever wait for one another.  Every wait is
-// bounded (kSpinLimit sleeps); the exchange words are zeroed by a fill kernel before each launch.
+// consecutive workgroups that are dispatched together and only ever wait for one another.  That holds only
+// while the grid has the device to itself: work of other streams or processes that holds CUs can keep a
+// slab's later chunks from being dispatched while its earlier ones wait.  Every wait is therefore bounded
+// (a limit of ~64-clock sleeps, about 0.1 s by default); a chunk that gives up sets its group sums to NaN
+// and raises KV_FAULT_EXCHANGE_TIMEOUT in the workspace's fault word, so the failure is visible to the caller
+// (kv_fault_status) instead of folding a softmax that misses part of the slab.  The exchange words are zeroed
+// by a fill kernel before each launch.
 #include <algorithm>
 
 #include "stream_lane.h"
@@ -20,8 +25,7 @@
 namespace ikv {
 namespace {
 
-constexpr int kSpinLimit = 1 << 22;  // 64-clock sleeps: about 0.1 s, far beyond any chunk's streaming time
-constexpr int kMaxWords = 4;         // exchange words per lane: chunks x padded group <= 256
+constexpr int kMaxWords = 4;  // exchange words per lane: chunks x padded group <= 256
 
 __device__ __forceinline__ uint64_t pack_ms(float m, float s) {
     return ((uint64_t)__float_as_uint(m) << 32) | (uint64_t)__float_as_uint(s);
@@ -34,7 +38,7 @@ constexpr int coop_waves_per_eu() {
 
 template <typename T, int D, int GP>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(coop_waves_per_eu<T, D, GP>())))
-void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round) {
+void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_t* faults, int spin_limit) {
     using L = Lane<T, D, GP>;
     using KP = KUnit<T, D, GP>;
     constexpr int RPW = L::RPW;
@@ -170,7 +174,9 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round) {
                 cs[k] = 0.0f;
                 done[k] = !(c < C && h < a.group);
             }
-            for (int spin = 0; spin < kSpinLimit; ++spin) {
+            // polls, at most spin_limit of them (0: none, every chunk gives up at once), with a sleep after each
+            // unsuccessful one
+            for (int spin = 0; spin < spin_limit; ++spin) {
                 bool all = true;
 #pragma unroll
                 for (int k = 0; k < kMaxWords; ++k) {
@@ -189,6 +195,13 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round) {
                 if (all) break;
                 __builtin_amdgcn_s_sleep(1);
             }
+            bool complete = true;
+#pragma unroll
+            for (int k = 0; k < kMaxWords; ++k) complete = complete && done[k];
+            // a peer's word never arrived: report it and poison this chunk's sums rather than fold a softmax
+            // that misses part of the slab (the atomic is a vector-memory instruction, as every store here)
+            const bool gave_up = __builtin_amdgcn_ballot_w64(!complete) != 0;
+            if (gave_up && ln.lane == 0) atomicOr(faults, kFaultExchangeTimeout);
             float M = cm[0];
 #pragma unroll
             for (int k = 1; k < kMaxWords; ++k) M = fmaxf(M, cm[k]);
@@ -200,7 +213,7 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round) {
                 if (cs[k] > 0.0f) S += cs[k] * __expf(cm[k] - M);
 #pragma unroll
             for (int o = GP; o < kWave; o <<= 1) S += __shfl_xor(S, o, kWave);
-            if (ln.lane < GP) fh[h] = (h < a.group && S > 0.0f) ? __expf(mh - M) / S : 0.0f;
+            if (ln.lane < GP) fh[h] = gave_up ? __builtin_nanf("") : ((h < a.group && S > 0.0f) ? __expf(mh - M) / S : 0.0f);
         }
         __syncthreads();
 
@@ -237,8 +250,21 @@ __global__ __launch_bounds__(256) void zero_words_kernel(uint64_t* w, size_t cou
     for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (size_t)gridDim.x * 256) w[i] = 0;
 }
 
+// The workspace's fault word: copied to `out` (when non-null), then zeroed when asked (one thread).
+__global__ __launch_bounds__(64) void fault_word_kernel(uint32_t* word, uint32_t* out, int clear) {
+    if (threadIdx.x != 0) return;
+    const uint32_t v = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (out) *out = v;
+    if (clear) __hip_atomic_store(word, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Polls a chunk makes before it gives up (process-wide; a test hook can lower it to force the report).
+constexpr int kDefaultSpinLimit = 1 << 22;  // 64-clock sleeps: about 0.1 s, far beyond any chunk's streaming
+std::atomic<int> g_spin_limit{kDefaultSpinLimit};
+
 template <typename T, int D, int GP>
-hipError_t launch_coop_gp(const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg, int grid, hipStream_t s) {
+hipError_t launch_coop_gp(const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg, int grid, uint32_t* faults,
+                          hipStream_t s) {
     if constexpr (Geometry<T, D, 1>::kChunks < GP) {
         return hipErrorInvalidValue;
     } else {
@@ -248,16 +274,27 @@ hipError_t launch_coop_gp(const ScorePlan& plan, const ScoreArgs& a, uint64_t* x
             const hipError_t e = raise_lds_limit(reinterpret_cast<const void*>(kern), raised);
             if (e != hipSuccess) return e;
         }
-        hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), plan.lds_bytes, s, a, xchg, grid / a.nchunk);
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), plan.lds_bytes, s, a, xchg, grid / a.nchunk, faults,
+                           g_spin_limit.load(std::memory_order_relaxed));
         return hipGetLastError();
     }
 }
 
+// Workgroups of the chunk-exchange kernel one CU holds with `lds` bytes of dynamic LDS (0 when the query
+// fails), cached per device and LDS size class (the plan's LDS is one of a few chunk sizes; a different size
+// on the same device re-queries).
 template <typename T, int D, int GP>
 int coop_occupancy(size_t lds) {
     if constexpr (Geometry<T, D, 1>::kChunks < GP) {
         return 0;
     } else {
+        static std::atomic<uint64_t> cached[kMaxDevices];  // (lds << 8) | (occupancy + 1); 0 = not queried
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = -1;
+        if (dev >= 0) {
+            const uint64_t c = cached[dev].load(std::memory_order_relaxed);
+            if (c != 0 && (c >> 8) == lds) return (int)(c & 0xff) - 1;
+        }
         int v = 0;
         static std::atomic<bool> raised[kMaxDevices];
         if (lds > 64 * 1024 &&
@@ -266,18 +303,21 @@ int coop_occupancy(size_t lds) {
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, score_coop_kernel<T, D, GP>, kThreads, lds) !=
             hipSuccess)
             return 0;
+        if (dev >= 0 && v >= 0 && v < 255) cached[dev].store(((uint64_t)lds << 8) | (uint64_t)(v + 1),
+                                                            std::memory_order_relaxed);
         return v;
     }
 }
 
 template <typename T, int D>
-hipError_t launch_coop_d(const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg, int grid, hipStream_t s) {
+hipError_t launch_coop_d(const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg, int grid, uint32_t* faults,
+                         hipStream_t s) {
     switch (plan.group_pad) {
-        case 1: return launch_coop_gp<T, D, 1>(plan, a, xchg, grid, s);
-        case 2: return launch_coop_gp<T, D, 2>(plan, a, xchg, grid, s);
-        case 4: return launch_coop_gp<T, D, 4>(plan, a, xchg, grid, s);
-        case 8: return launch_coop_gp<T, D, 8>(plan, a, xchg, grid, s);
-        case 16: return launch_coop_gp<T, D, 16>(plan, a, xchg, grid, s);
+        case 1: return launch_coop_gp<T, D, 1>(plan, a, xchg, grid, faults, s);
+        case 2: return launch_coop_gp<T, D, 2>(plan, a, xchg, grid, faults, s);
+        case 4: return launch_coop_gp<T, D, 4>(plan, a, xchg, grid, faults, s);
+        case 8: return launch_coop_gp<T, D, 8>(plan, a, xchg, grid, faults, s);
+        case 16: return launch_coop_gp<T, D, 16>(plan, a, xchg, grid, faults, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -304,26 +344,33 @@ int coop_workgroups(int dtype, int head_dim, const ScorePlan& plan) {
     else
         occ = head_dim == 64 ? coop_occupancy_d<bf16_t, 64>(plan.group_pad, plan.lds_bytes)
                              : coop_occupancy_d<bf16_t, 128>(plan.group_pad, plan.lds_bytes);
-    int dev = 0, cus = 0;
-    if (occ < 1 || hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
-        return 0;
+    const int cus = device_cus();
+    if (occ < 1 || cus < 1) return 0;
     return occ * cus;
 }
 
+hipError_t launch_fault_word(uint32_t* word, uint32_t* out, bool clear, hipStream_t s) {
+    hipLaunchKernelGGL(fault_word_kernel, dim3(1), dim3(64), 0, s, word, out, clear ? 1 : 0);
+    return hipGetLastError();
+}
+
+int set_exchange_wait_limit(int polls) {
+    return g_spin_limit.exchange(polls < 0 ? kDefaultSpinLimit : polls, std::memory_order_relaxed);
+}
+
 hipError_t launch_score_coop(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg,
-                             int grid, hipStream_t s) {
+                             int grid, uint32_t* faults, hipStream_t s) {
     const size_t words = (size_t)a.layers * a.batch * a.hq * a.nchunk;
     const unsigned zb = (unsigned)std::min<size_t>((words + 255) / 256, 2048);
     hipLaunchKernelGGL(zero_words_kernel, dim3(zb), dim3(256), 0, s, xchg, words);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (dtype == 0) {
-        if (head_dim == 64) return launch_coop_d<float, 64>(plan, a, xchg, grid, s);
-        if (head_dim == 128) return launch_coop_d<float, 128>(plan, a, xchg, grid, s);
+        if (head_dim == 64) return launch_coop_d<float, 64>(plan, a, xchg, grid, faults, s);
+        if (head_dim == 128) return launch_coop_d<float, 128>(plan, a, xchg, grid, faults, s);
     } else {
-        if (head_dim == 64) return launch_coop_d<bf16_t, 64>(plan, a, xchg, grid, s);
-        if (head_dim == 128) return launch_coop_d<bf16_t, 128>(plan, a, xchg, grid, s);
+        if (head_dim == 64) return launch_coop_d<bf16_t, 64>(plan, a, xchg, grid, faults, s);
+        if (head_dim == 128) return launch_coop_d<bf16_t, 128>(plan, a, xchg, grid, faults, s);
     }
     return hipErrorInvalidValue;
 }

@@ -58,6 +58,23 @@ int main(void) {
                           NULL) == KV_ERR_INVALID_ARG); /* layers 30..32 past the last */
     CHECK(kv_rank_trace_state_bytes(8, 40000, &st) == KV_OK && st == 8 * (4 + 2 * 1250) * 4);
 
+    /* scorer plan of a steady step (slabs of 3,278 rows fit one workgroup's LDS) */
+    kv_score_info info = {-1, -1, -1};
+    p.score_variant = 0;
+    CHECK(kv_score_plan(&s, 3278, &p, &info) == KV_OK);
+    CHECK(info.path == KV_PATH_LDS && info.chunks == 1 && info.merge >= 1 && 8 % info.merge == 0);
+    CHECK(kv_score_plan(&s, 32770, &p, &info) == KV_ERR_INVALID_ARG);
+    /* fault word: validated on the host (nothing queued) */
+    CHECK(kv_fault_status(NULL, ws, (uint32_t*)fake, 0, NULL) == KV_ERR_WORKSPACE);
+    CHECK(kv_fault_status(fake, ws, NULL, 0, NULL) == KV_ERR_INVALID_ARG);
+    {
+        const int32_t def = kv_set_exchange_wait_limit(3);
+        CHECK(def > 0);
+        CHECK(kv_set_exchange_wait_limit(-1) == 3);
+        CHECK(kv_set_exchange_wait_limit(-1) == def);
+    }
+    (void)KV_FAULT_EXCHANGE_TIMEOUT;
+
     CHECK(strcmp(kv_status_string(KV_OK), "ok") == 0);
     CHECK(strlen(kv_status_string(KV_ERR_HIP)) > 0);
     CHECK(strlen(kv_status_string((kv_status)-99)) > 0);

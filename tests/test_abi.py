@@ -14,7 +14,7 @@ HEADER = os.path.join(ROOT, "include", "inertiakv.h")
 
 def declared_functions():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^(?:kv_status|const char\*)\s+(kv_\w+)\s*\(", text, flags=re.M)))
+    return sorted(set(re.findall(r"^(?:kv_status|const char\*|int32_t)\s+(kv_\w+)\s*\(", text, flags=re.M)))
 
 
 @pytest.fixture(scope="module")
@@ -245,3 +245,32 @@ def test_rank_trace_validation(lib):
         assert _step(s, good, rt=ctypes.byref(bad), ws=FAKE, ws_bytes=need)[0] == B.KV_ERR_INVALID_ARG
     assert _step(s, good, rt=ctypes.byref(B.KvRankTrace(5, 100, FAKE + 2, FAKE)), ws=FAKE,
                  ws_bytes=need)[0] == B.KV_ERR_UNSUPPORTED
+
+
+def test_score_plan_query(lib):
+    s = shape()
+    info = B.kv_score_plan(s, 50, B.make_params(0.9, 20, score_merge=2))
+    assert (info.merge, info.path, info.chunks) == (2, B.KV_PATH_LDS, 1)
+    L = lib_()
+    out = B.KvScoreInfo(-7, -7, -7)
+    for p, n in ((B.make_params(0.9, 20, score_merge=4), 50), (B.make_params(0.9, 20), 0),
+                 (B.make_params(0.9, 20), 101)):
+        assert L.kv_score_plan(ctypes.byref(s), n, ctypes.byref(p), ctypes.byref(out)) == B.KV_ERR_INVALID_ARG
+    assert L.kv_score_plan(ctypes.byref(s), 50, ctypes.byref(B.make_params(0.9, 20)), None) == B.KV_ERR_INVALID_ARG
+    assert (out.merge, out.path, out.chunks) == (-7, -7, -7)
+
+
+def test_fault_status_validation(lib):
+    L = lib_()
+    assert L.kv_fault_status(None, 1 << 20, FAKE, 0, None) == B.KV_ERR_WORKSPACE
+    assert L.kv_fault_status(FAKE, 255, FAKE, 0, None) == B.KV_ERR_WORKSPACE
+    assert L.kv_fault_status(FAKE + 16, 1 << 20, FAKE, 0, None) == B.KV_ERR_INVALID_ARG   # workspace not aligned
+    assert L.kv_fault_status(FAKE, 1 << 20, FAKE + 2, 0, None) == B.KV_ERR_INVALID_ARG    # misaligned output word
+    assert L.kv_fault_status(FAKE, 1 << 20, None, 0, None) == B.KV_ERR_INVALID_ARG        # nothing asked for
+
+
+def test_exchange_wait_limit_setter(lib):
+    default = B.kv_set_exchange_wait_limit(7)
+    assert default > 1000                       # about 0.1 s of sleeps
+    assert B.kv_set_exchange_wait_limit(-1) == 7
+    assert B.kv_set_exchange_wait_limit(-1) == default
