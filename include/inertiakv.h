@@ -226,6 +226,24 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
                         const kv_trace* trace, const kv_rank_trace* rank_trace, void* ws, size_t ws_bytes,
                         void* stream);
 
+/* ---- Allocation-free decode step: for callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that forbid allocation) ----
+ * kv_evict_step without the workspace: its scratch is a static device array inside the library of
+ * KV_STATIC_SCRATCH_BYTES per device (one copy on each GPU the library runs on, held until the process ends;
+ * no call allocates or frees anything).  Supported steps: those whose slabs are scored in one workgroup each
+ * (kv_score_plan path KV_PATH_LDS on refresh steps; any non-refresh step) and whose scratch fits (the
+ * workspace of kv_evict_step without the regions of chunked scoring and of the attention calls: e.g. every
+ * steady step of a batch-8, 32-layer, 8-KV-head cache of ~3,300 tokens).  Otherwise, before anything is
+ * queued: KV_ERR_UNSUPPORTED (chunked scoring, e.g. a first step over a long prefill: use kv_evict_step) or
+ * KV_ERR_WORKSPACE (scratch too small).  Every call on one device shares that device's scratch, which keeps
+ * the last call's contents: calls that overlap in time on one GPU (several streams or host threads) race, and
+ * the caller must serialise them.  Arguments and results are kv_evict_step's. */
+#define KV_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+kv_status kv_evict_step_static(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in,
+                               int32_t new_pos, const void* q, const void* k_new, const void* v_new, void* k,
+                               void* v, float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
+                               const kv_trace* trace, const kv_rank_trace* rank_trace, void* stream);
+
 /* ---- Decode step around the model's own attention (fused decode attention + score) ----
  * A decoder that attends the cache anyway can take the step's score from its attention (Eq. 1 is the softmax
  * of the last query, the one that produces the attention output): K is then read once for both, instead of

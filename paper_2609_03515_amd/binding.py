@@ -27,7 +27,9 @@ PHASES = ("append", "score", "fold", "select", "compact")
 
 EXPORTED = ("kv_workspace_bytes", "kv_score_ema", "kv_topk_select", "kv_compact", "kv_evict_step",
             "kv_append", "kv_attend_score", "kv_evict_finish", "kv_rank_trace_state_bytes", "kv_score_merge",
-            "kv_score_plan", "kv_fault_status", "kv_set_exchange_wait_limit", "kv_status_string")
+            "kv_score_plan", "kv_fault_status", "kv_set_exchange_wait_limit", "kv_evict_step_static",
+            "kv_status_string")
+KV_STATIC_SCRATCH_BYTES = 64 << 20
 KV_TRACE_COUNTS = 10
 
 
@@ -92,6 +94,8 @@ def load_library(path: str = LIB_PATH):
     lib.kv_score_plan.argtypes = [shp, i32, prm, ctypes.POINTER(KvScoreInfo)]
     lib.kv_fault_status.argtypes = [vp, sz, vp, i32, vp]
     lib.kv_set_exchange_wait_limit.argtypes = [i32]
+    lib.kv_evict_step_static.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+                                         ctypes.POINTER(i32), vp, vp, trc, rtr, vp]
     for fn in EXPORTED[:-1]:
         getattr(lib, fn).restype = i32
     lib.kv_status_string.argtypes = [i32]
@@ -208,6 +212,19 @@ def kv_evict_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos
         ctypes.byref(trace) if trace is not None else None,
         ctypes.byref(rank_trace) if rank_trace is not None else None, _ptr(ws),
         ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+    return n_out.value
+
+
+def kv_evict_step_static(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, keep_out=None,
+                         s_out=None, trace: KvTrace | None = None, rank_trace: KvRankTrace | None = None,
+                         stream=None) -> int:
+    """kv_evict_step with the library's static scratch instead of a workspace.  Returns n_out."""
+    n_out = ctypes.c_int32(-1)
+    _check("kv_evict_step_static", load_library().kv_evict_step_static(
+        ctypes.byref(shape), ctypes.byref(params), int(t), int(n_in), int(new_pos), _ptr(q), _ptr(k_new),
+        _ptr(v_new), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out),
+        ctypes.byref(trace) if trace is not None else None,
+        ctypes.byref(rank_trace) if rank_trace is not None else None, _stream(stream)))
     return n_out.value
 
 

@@ -3,12 +3,36 @@
 #include <math.h>
 #include <string.h>
 
+#include <atomic>
+
 #include "../../include/inertiakv.h"
 #include "kernels.h"
 #include "kv_common.h"
 
+// Scratch of kv_evict_step_static, the variant for callers that cannot allocate: one copy per device, held
+// until the process ends.  On the host this name is only a stand-in for the symbol, never a device address:
+// host code takes the device's copy from hipGetSymbolAddress (static_scratch below) and passes that pointer.
+static __device__ __align__(256) unsigned char scratch[KV_STATIC_SCRATCH_BYTES];
+
 namespace ikv {
 namespace {
+
+constexpr size_t kStaticScratchBytes = KV_STATIC_SCRATCH_BYTES;
+
+// Device address of this device's scratch copy, looked up once per device with that device current.
+kv_status static_scratch(void** out) {
+    constexpr int kDevices = 64;
+    static std::atomic<void*> addr[kDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevices) return KV_ERR_HIP;
+    void* p = addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return KV_ERR_HIP;
+        addr[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return KV_OK;
+}
 
 // Long slabs (first steps) are scored in groups of layers whose logits stay within this many bytes, so that
 // the finish kernel reads them back while the 256 MiB last-level cache may still hold them: measured with 1,
@@ -59,19 +83,22 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 // One layout serves every entry point for a given n, so that the group sums r written by the attention
 // calls of a step are where kv_evict_finish folds them.  The logits / partial regions are shared by the
 // scorer's split path and the attention's chunked path (never live at the same time).
-Layout layout_for(const kv_shape& s, int n) {
+// step_lds_only: the regions of a kv_evict_step whose slabs are scored in one workgroup each (no logits,
+// chunk partials or attention partials), for the allocation-free variant.
+Layout layout_for(const kv_shape& s, int n, bool step_lds_only = false) {
     Layout L{};
     L.n_stride = (n + 63) / 64 * 64;
     L.max_pairs = n;
     const int group = s.n_q_heads / s.n_kv_heads;
     score_plan(s.dtype, s.head_dim, group, n, &L.plan);
-    const AttendBound ab = attend_bound(s.dtype, s.head_dim, group, n, s.batch * s.n_kv_heads, s.layers);
+    AttendBound ab = attend_bound(s.dtype, s.head_dim, group, n, s.batch * s.n_kv_heads, s.layers);
+    if (step_lds_only) ab = AttendBound{0, false};
     const size_t heads = (size_t)s.layers * s.batch * s.n_q_heads;
     const size_t logits = heads * L.n_stride * sizeof(float);
-    const size_t z_bytes = (L.plan.split || ab.may_split) ? logits : 0;
+    const size_t z_bytes = ((L.plan.split && !step_lds_only) || ab.may_split) ? logits : 0;
     // chunk partials of long slabs (scorer) and of the attention
     size_t part_bytes = (size_t)ab.chunk_layers * s.batch * s.n_q_heads * sizeof(float2);
-    if (L.plan.split) {
+    if (L.plan.split && !step_lds_only) {
         ScorePlan cp;
         if (attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &cp, kScoreChunkLds)) {
             const size_t sp = heads * cp.nchunk * sizeof(float2);
@@ -732,6 +759,26 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
     return evict_step(*shape, *params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, n_out, keep_out, s_out,
                       trace, rank_trace, L, ws, static_cast<hipStream_t>(stream));
+}
+
+kv_status kv_evict_step_static(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in,
+                               int32_t new_pos, const void* q, const void* k_new, const void* v_new, void* k,
+                               void* v, float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
+                               const kv_trace* trace, const kv_rank_trace* rank_trace, void* stream) {
+    kv_status rc = check_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, n_out, s_out,
+                              rank_trace);
+    if (rc != KV_OK) return rc;
+    const kv_shape& s = *shape;
+    const kv_params& p = *params;
+    const int n = n_in + 1;
+    const Layout L = layout_for(s, n, true);
+    // slabs too long for one workgroup (the chunked scorers) need the workspace variant
+    if (is_refresh(p, t) && scorer_plan(s, L, p.score_variant, p.score_merge).split) return KV_ERR_UNSUPPORTED;
+    if (L.total > kStaticScratchBytes) return KV_ERR_WORKSPACE;
+    void* ws = nullptr;
+    if ((rc = static_scratch(&ws)) != KV_OK) return rc;
+    return evict_step(s, p, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, n_out, keep_out, s_out, trace,
+                      rank_trace, L, ws, static_cast<hipStream_t>(stream));
 }
 
 kv_status kv_append(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in, int32_t new_pos,

@@ -274,3 +274,20 @@ def test_exchange_wait_limit_setter(lib):
     assert default > 1000                       # about 0.1 s of sleeps
     assert B.kv_set_exchange_wait_limit(-1) == 7
     assert B.kv_set_exchange_wait_limit(-1) == default
+
+
+def test_static_step_rejects_what_its_scratch_cannot_hold(lib):
+    """The allocation-free step refuses, on the host, a step whose slabs need chunked scoring (first step over
+    32k tokens) and one whose scratch exceeds the static array (batch 64 x 4,097 tokens), queueing nothing."""
+    out = ctypes.c_int32(-7)
+
+    def call(s, p, t, n_in, new_pos):
+        return lib_().kv_evict_step_static(ctypes.byref(s), ctypes.byref(p), t, n_in, new_pos, *(FAKE,) * 7,
+                                           ctypes.byref(out), None, None, None, None, None)
+    s = B.make_shape(8, 32, 32, 8, 128, 32769, "bf16")
+    assert call(s, B.make_params(0.9, 3277), 1, 32768, 32768) == B.KV_ERR_UNSUPPORTED
+    big = B.make_shape(64, 32, 32, 8, 128, 4097, "bf16")
+    assert call(big, B.make_params(0.9, 4096), 2, 4096, 5000) == B.KV_ERR_WORKSPACE
+    assert call(s, B.make_params(0.9, 3277), 0, 3277, 40000) == B.KV_ERR_INVALID_ARG   # argument checks as the step
+    assert call(s, B.make_params(1.0, 3277), 2, 3277, 40000) == B.KV_ERR_INVALID_ARG
+    assert out.value == -7
