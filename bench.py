@@ -345,13 +345,13 @@ def extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, full_
             B.kv_attend_score(shape, 0, L, n, q, k, v, pos, inputs[state["t"] - 1]["new_pos"], cfg.recency_bias,
                               cfg.recency_window, emit, o, ws)
 
-    def fused_step(per_layer, p=full, emit=B.KV_EMIT_SCORES):
+    def fused_step(per_layer, p=full, emit=B.KV_EMIT_SCORES, norms=None):
         state["t"] += 1
         si = inputs[state["t"] - 1]
         n = state["n"]
-        B.kv_append(shape, p, state["t"], n, si["new_pos"], si["k_new"], si["v_new"], k, v, u, pos)
+        B.kv_append(shape, p, state["t"], n, si["new_pos"], si["k_new"], si["v_new"], k, v, u, pos, v_norms=norms)
         attend(n + 1, si["q"], emit, per_layer)
-        state["n"] = B.kv_evict_finish(shape, p, state["t"], n + 1, k, v, u, pos, ws)
+        state["n"] = B.kv_evict_finish(shape, p, state["t"], n + 1, k, v, u, pos, ws, v_norms=norms)
 
     def separate_step(per_layer, p=full):
         state["t"] += 1
@@ -364,11 +364,11 @@ def extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, full_
         state["t"] += 1
         attend(state["n"] + 1, inputs[state["t"] - 1]["q"], 0, per_layer)
 
-    def plain_step(p, rank_trace=None):
+    def plain_step(p, rank_trace=None, norms=None):
         state["t"] += 1
         si = inputs[state["t"] - 1]
         state["n"] = B.kv_evict_step(shape, p, state["t"], state["n"], si["new_pos"], si["q"], si["k_new"],
-                                     si["v_new"], k, v, u, pos, ws, rank_trace=rank_trace)
+                                     si["v_new"], k, v, u, pos, ws, rank_trace=rank_trace, v_norms=norms)
 
     def ms_of(fn, *a, **kw):
         fn(*a, **kw)  # one untimed call (first use of a configuration)
@@ -401,10 +401,20 @@ def extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, full_
                      "eviction step; fused = attention emits the score (kv_append, kv_attend_score, "
                      "kv_evict_finish), separate = attention without score + kv_evict_step's own scoring pass",
              **res}
-    variants = {"attention_ms": round(full_ms, 4)}
+    variants = {"what": "kv_evict_step with each scorer perturbation, KF steps each; VNorm reads V (1.72 GB per "
+                        "step) unless the value-norm cache is given (filled once by kv_value_norms, then kept by "
+                        "the steps: 4 bytes per row)",
+                "attention_ms": round(full_ms, 4)}
     for name, kw in (("vnorm", dict(vnorm=True)), ("entropy", dict(entropy=True)),
                      ("vnorm_entropy", dict(vnorm=True, entropy=True))):
         variants[name + "_ms"] = round(ms_of(plain_step, params(**kw)), 4)
+    norms = torch.empty((L, cfg.batch, cfg.n_kv_heads, k.shape[3]), dtype=torch.float32, device=u.device)
+    B.kv_value_norms(shape, state["n"], v, norms)
+    for name, kw in (("vnorm_norm_cache", dict(vnorm=True)), ("vnorm_entropy_norm_cache", dict(vnorm=True, entropy=True))):
+        variants[name + "_ms"] = round(ms_of(plain_step, params(**kw), None, norms), 4)
+    res["all_layers_one_call"]["fused_vnorm_norm_cache_decode_step_ms"] = round(
+        ms_of(fused_step, False, params(vnorm=True), B.KV_EMIT_SCORES, norms), 4)
+    del norms
     max_pos = inputs[-1]["new_pos"] + 1
     tstate = torch.zeros(B.kv_rank_trace_state_bytes(cfg.batch, max_pos) // 4, dtype=torch.int32,
                          device=u.device)
@@ -462,7 +472,7 @@ def main():
     ws = B.workspace(shape, cap, device=dev)
     K, W = args.steps, args.warmup
     KF = min(K, 50)   # steps per configuration of the extra measurements (fused attention, variants, trace)
-    total = max(64, 1 + W + 9 * K + 12 * KF)
+    total = max(64, 1 + W + 9 * K + 16 * KF)   # step 1, warmup, the timed schedules, the extra rows (15 x KF)
     inputs = [w.step_inputs(t) for t in range(1, total + 1)]
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup

@@ -30,6 +30,7 @@
  *      pos         [batch][cap] int32                    absolute position per cached token (unique, >= 0)
  *      keep        [batch][cap] uint8                    1 = retained (first n entries written)
  *      s_out       [layers][batch][n] float              per-layer pooled score s_l (optional, may be NULL)
+ *      v_norms     [layers][batch][n_kv_heads][cap] float  optional value-norm cache (see kv_value_norms)
  *    Query head h reads KV head h / (n_q_heads / n_kv_heads).  Every sequence holds the same n tokens.
  *  - Preconditions not checked on the device: keys, queries and utilities are finite; utilities are >= 0
  *    when produced by this library; positions are unique within a sequence.
@@ -201,6 +202,16 @@ kv_status kv_score_ema(const kv_shape* shape, int32_t n, const void* q, const vo
 kv_status kv_topk_select(const kv_shape* shape, int32_t n, int32_t budget, const float* u, const int32_t* pos,
                          uint8_t* keep, void* ws, size_t ws_bytes, void* stream);
 
+/* Value-norm cache for VNorm (Sec. 5.1; implementation appendix "Per-step scoring": VNorm weights a token's
+ * attention by the l2 norm of its value row over the mean norm of the cached tokens of that layer and KV head).
+ * A value row never changes once cached, it only moves, so its norm can be computed once: kv_value_norms
+ * fills v_norms[l][b][g][i] = |V[l][b][g][i]| for the rows i < n of every slab (once, after the prefill).
+ * Every call below that takes a non-NULL v_norms keeps it in step with V: the appended token's norm is written
+ * where its V row goes, and the compaction moves norms with their rows.  VNorm refresh steps given v_norms read
+ * the cached norms (4 bytes per row) instead of V (d elements per row), and the steady refresh step then keeps
+ * its three-kernel form.  Rows of v_norms at and beyond the cache's n are unspecified, like those of V. */
+kv_status kv_value_norms(const kv_shape* shape, int32_t n, const void* v, float* v_norms, void* stream);
+
 /* Hole-fill compaction of a retention decision (which must keep exactly min(B, n) tokens per sequence).
  * Sec. 3: eviction is irreversible, the evicted tokens' K/V pairs leave the cache and the retained ones stay;
  * the paper leaves the row layout open (attention does not depend on row order), and this call reads it as
@@ -209,7 +220,7 @@ kv_status kv_topk_select(const kv_shape* shape, int32_t n, int32_t budget, const
  * and pos.  Rows [0, k) then hold exactly the retained tokens; rows >= k are left as they were.  A mask that
  * keeps a different count is rejected on the device by moving nothing beyond the smaller of the two lists. */
 kv_status kv_compact(const kv_shape* shape, int32_t n, int32_t budget, const uint8_t* keep, void* k, void* v,
-                     float* u, int32_t* pos, void* ws, size_t ws_bytes, void* stream);
+                     float* u, int32_t* pos, float* v_norms, void* ws, size_t ws_bytes, void* stream);
 
 /* One decode step t >= 1 on a cache of n_in tokens (n_in + 1 <= capacity):
  *  1. append k_new/v_new at slot n_in, pos = new_pos, u = 0 on refresh steps, else the mean (or min) of the
@@ -217,12 +228,12 @@ kv_status kv_compact(const kv_shape* shape, int32_t n, int32_t budget, const uin
  *  2. refresh steps only: kv_score_ema over the n_in + 1 tokens with q, cur_pos = new_pos;
  *  3. if n_in + 1 > B: select the top B (stale utilities on non-refresh steps) and compact as kv_compact.
  * *n_out (HOST pointer) receives min(B, n_in + 1); cache rows at and beyond *n_out are unspecified
- * afterwards.  keep_out (nullable) receives the decision over the
- * n_in + 1 slots before compaction; s_out (nullable) the per-layer scores of a refresh step; trace (nullable)
- * timing events; rank_trace (nullable) the diagnostics above. */
+ * afterwards.  v_norms (nullable) is the value-norm cache, kept in step and read by VNorm; keep_out (nullable)
+ * receives the decision over the n_in + 1 slots before compaction; s_out (nullable) the per-layer scores of a
+ * refresh step; trace (nullable) timing events; rank_trace (nullable) the diagnostics above. */
 kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in,
                         int32_t new_pos, const void* q, const void* k_new, const void* v_new, void* k, void* v,
-                        float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
+                        float* u, int32_t* pos, float* v_norms, int32_t* n_out, uint8_t* keep_out, float* s_out,
                         const kv_trace* trace, const kv_rank_trace* rank_trace, void* ws, size_t ws_bytes,
                         void* stream);
 
@@ -241,8 +252,8 @@ kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t 
 #define KV_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
 kv_status kv_evict_step_static(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in,
                                int32_t new_pos, const void* q, const void* k_new, const void* v_new, void* k,
-                               void* v, float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
-                               const kv_trace* trace, const kv_rank_trace* rank_trace, void* stream);
+                               void* v, float* u, int32_t* pos, float* v_norms, int32_t* n_out, uint8_t* keep_out,
+                               float* s_out, const kv_trace* trace, const kv_rank_trace* rank_trace, void* stream);
 
 /* ---- Decode step around the model's own attention (fused decode attention + score) ----
  * A decoder that attends the cache anyway can take the step's score from its attention (Eq. 1 is the softmax
@@ -256,9 +267,11 @@ kv_status kv_evict_step_static(const kv_shape* shape, const kv_params* params, i
  * attention calls and the finish), sized by kv_workspace_bytes for at least n_in + 1 tokens.
  *
  * kv_append: step 1 of kv_evict_step alone (appendix "New token insertion"; the refresh decision of Eq. 5
- * picks the prior: 0 on refresh steps, else the mean or min of the existing utilities). */
+ * picks the prior: 0 on refresh steps, else the mean or min of the existing utilities); v_norms (nullable)
+ * receives the new row's value norm. */
 kv_status kv_append(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in, int32_t new_pos,
-                    const void* k_new, const void* v_new, void* k, void* v, float* u, int32_t* pos, void* stream);
+                    const void* k_new, const void* v_new, void* k, void* v, float* u, int32_t* pos, float* v_norms,
+                    void* stream);
 
 /* What kv_attend_score records in the workspace besides the output (bit mask): the layers' pooled scores
  * (Eq. 1), and the value-row norms that VNorm weights them by (read from V while the attention streams it). */
@@ -278,10 +291,11 @@ kv_status kv_attend_score(const kv_shape* shape, int32_t layer0, int32_t layer_c
 
 /* Steps 2-3 of kv_evict_step after the attention calls: on refresh steps (Eq. 5) the layer fold of the
  * emitted scores of ALL layers (Eq. 4 by params->rule), then the top-B selection and compaction over the n
- * cached tokens (n = n_in + 1 of the step).  *n_out (HOST) = min(B, n); keep_out / s_out / rank_trace as
- * kv_evict_step. */
+ * cached tokens (n = n_in + 1 of the step).  *n_out (HOST) = min(B, n); v_norms / keep_out / s_out / rank_trace
+ * as kv_evict_step (VNorm takes the norms the attention emitted when KV_SCORE_NORMS_EMITTED is set, else those
+ * of v_norms, else reads V). */
 kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n, void* k, void* v,
-                          float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
+                          float* u, int32_t* pos, float* v_norms, int32_t* n_out, uint8_t* keep_out, float* s_out,
                           const kv_rank_trace* rank_trace, void* ws, size_t ws_bytes, void* stream);
 
 /* Static description of a status code. */

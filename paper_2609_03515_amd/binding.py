@@ -28,7 +28,7 @@ PHASES = ("append", "score", "fold", "select", "compact")
 EXPORTED = ("kv_workspace_bytes", "kv_score_ema", "kv_topk_select", "kv_compact", "kv_evict_step",
             "kv_append", "kv_attend_score", "kv_evict_finish", "kv_rank_trace_state_bytes", "kv_score_merge",
             "kv_score_plan", "kv_fault_status", "kv_set_exchange_wait_limit", "kv_evict_step_static",
-            "kv_status_string")
+            "kv_value_norms", "kv_status_string")
 KV_STATIC_SCRATCH_BYTES = 64 << 20
 KV_TRACE_COUNTS = 10
 
@@ -82,19 +82,20 @@ def load_library(path: str = LIB_PATH):
     lib.kv_workspace_bytes.argtypes = [shp, i32, ctypes.POINTER(sz)]
     lib.kv_score_ema.argtypes = [shp, i32, vp, vp, vp, i32, f32, f32, i32, vp, vp, vp, sz, vp]
     lib.kv_topk_select.argtypes = [shp, i32, i32, vp, vp, vp, vp, sz, vp]
-    lib.kv_compact.argtypes = [shp, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp]
-    lib.kv_evict_step.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+    lib.kv_compact.argtypes = [shp, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.kv_evict_step.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp,
                                   ctypes.POINTER(i32), vp, vp, trc, rtr, vp, sz, vp]
-    lib.kv_append.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
+    lib.kv_append.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.kv_attend_score.argtypes = [shp, i32, i32, i32, vp, vp, vp, vp, i32, f32, i32, i32, vp, vp, sz, vp]
-    lib.kv_evict_finish.argtypes = [shp, prm, i32, i32, vp, vp, vp, vp, ctypes.POINTER(i32), vp, vp, rtr, vp, sz,
-                                    vp]
+    lib.kv_evict_finish.argtypes = [shp, prm, i32, i32, vp, vp, vp, vp, vp, ctypes.POINTER(i32), vp, vp, rtr, vp,
+                                    sz, vp]
+    lib.kv_value_norms.argtypes = [shp, i32, vp, vp, vp]
     lib.kv_rank_trace_state_bytes.argtypes = [i32, i32, ctypes.POINTER(sz)]
     lib.kv_score_merge.argtypes = [shp, i32, prm, ctypes.POINTER(i32)]
     lib.kv_score_plan.argtypes = [shp, i32, prm, ctypes.POINTER(KvScoreInfo)]
     lib.kv_fault_status.argtypes = [vp, sz, vp, i32, vp]
     lib.kv_set_exchange_wait_limit.argtypes = [i32]
-    lib.kv_evict_step_static.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+    lib.kv_evict_step_static.argtypes = [shp, prm, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp,
                                          ctypes.POINTER(i32), vp, vp, trc, rtr, vp]
     for fn in EXPORTED[:-1]:
         getattr(lib, fn).restype = i32
@@ -195,20 +196,27 @@ def kv_topk_select(shape, n, budget, u, pos, keep, ws, stream=None):
         ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
 
 
-def kv_compact(shape, n, budget, keep, k, v, u, pos, ws, stream=None):
+def kv_compact(shape, n, budget, keep, k, v, u, pos, ws, stream=None, v_norms=None):
     _check("kv_compact", load_library().kv_compact(
-        ctypes.byref(shape), int(n), int(budget), _ptr(keep), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), _ptr(ws),
-        ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+        ctypes.byref(shape), int(n), int(budget), _ptr(keep), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), _ptr(v_norms),
+        _ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+
+
+def kv_value_norms(shape, n, v, v_norms, stream=None):
+    """Fills the value-norm cache v_norms [layers][batch][n_kv][cap] float for rows [0, n) from V."""
+    _check("kv_value_norms", load_library().kv_value_norms(ctypes.byref(shape), int(n), _ptr(v), _ptr(v_norms),
+                                                            _stream(stream)))
 
 
 def kv_evict_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, ws, keep_out=None,
                   s_out=None, trace: KvTrace | None = None, rank_trace: KvRankTrace | None = None,
-                  stream=None) -> int:
+                  stream=None, v_norms=None) -> int:
     """Returns n_out = min(B, n_in + 1)."""
     n_out = ctypes.c_int32(-1)
     _check("kv_evict_step", load_library().kv_evict_step(
         ctypes.byref(shape), ctypes.byref(params), int(t), int(n_in), int(new_pos), _ptr(q), _ptr(k_new),
-        _ptr(v_new), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out),
+        _ptr(v_new), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), _ptr(v_norms), ctypes.byref(n_out), _ptr(keep_out),
+        _ptr(s_out),
         ctypes.byref(trace) if trace is not None else None,
         ctypes.byref(rank_trace) if rank_trace is not None else None, _ptr(ws),
         ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
@@ -217,12 +225,13 @@ def kv_evict_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos
 
 def kv_evict_step_static(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, keep_out=None,
                          s_out=None, trace: KvTrace | None = None, rank_trace: KvRankTrace | None = None,
-                         stream=None) -> int:
+                         stream=None, v_norms=None) -> int:
     """kv_evict_step with the library's static scratch instead of a workspace.  Returns n_out."""
     n_out = ctypes.c_int32(-1)
     _check("kv_evict_step_static", load_library().kv_evict_step_static(
         ctypes.byref(shape), ctypes.byref(params), int(t), int(n_in), int(new_pos), _ptr(q), _ptr(k_new),
-        _ptr(v_new), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out),
+        _ptr(v_new), _ptr(k), _ptr(v), _ptr(u), _ptr(pos), _ptr(v_norms), ctypes.byref(n_out), _ptr(keep_out),
+        _ptr(s_out),
         ctypes.byref(trace) if trace is not None else None,
         ctypes.byref(rank_trace) if rank_trace is not None else None, _stream(stream)))
     return n_out.value
@@ -245,10 +254,10 @@ def _ws_bytes(ws):
     return ws.numel() * ws.element_size() if ws is not None else 0
 
 
-def kv_append(shape, params, t, n_in, new_pos, k_new, v_new, k, v, u, pos, stream=None):
+def kv_append(shape, params, t, n_in, new_pos, k_new, v_new, k, v, u, pos, stream=None, v_norms=None):
     _check("kv_append", load_library().kv_append(
         ctypes.byref(shape), ctypes.byref(params), int(t), int(n_in), int(new_pos), _ptr(k_new), _ptr(v_new),
-        _ptr(k), _ptr(v), _ptr(u), _ptr(pos), _stream(stream)))
+        _ptr(k), _ptr(v), _ptr(u), _ptr(pos), _ptr(v_norms), _stream(stream)))
 
 
 def kv_attend_score(shape, layer0, layer_count, n, q, k, v, pos, cur_pos, recency_bias, recency_window,
@@ -260,12 +269,12 @@ def kv_attend_score(shape, layer0, layer_count, n, q, k, v, pos, cur_pos, recenc
 
 
 def kv_evict_finish(shape, params, t, n, k, v, u, pos, ws, keep_out=None, s_out=None,
-                    rank_trace: KvRankTrace | None = None, stream=None) -> int:
+                    rank_trace: KvRankTrace | None = None, stream=None, v_norms=None) -> int:
     """Returns n_out = min(B, n)."""
     n_out = ctypes.c_int32(-1)
     _check("kv_evict_finish", load_library().kv_evict_finish(
         ctypes.byref(shape), ctypes.byref(params), int(t), int(n), _ptr(k), _ptr(v), _ptr(u), _ptr(pos),
-        ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out),
+        _ptr(v_norms), ctypes.byref(n_out), _ptr(keep_out), _ptr(s_out),
         ctypes.byref(rank_trace) if rank_trace is not None else None, _ptr(ws), _ws_bytes(ws), _stream(stream)))
     return n_out.value
 

@@ -307,14 +307,18 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
     return hip_status(launch_score(s.dtype, s.head_dim, plan, a, st));
 }
 
-// Scorer perturbations (Sec. 5.1) of a refresh step: value-row norms and entropy factors for the fold.
+// Scorer perturbations (Sec. 5.1) of a refresh step: value-row norms and entropy factors for the fold.  With
+// the caller's norm cache (norms, [layers][batch][n_kv][cap]) VNorm reads the cached norms instead of V; v_new
+// set: row n - 1 is the step's newcomer, whose norm is computed from v_new and cached first.
 kv_status run_variants(const kv_shape& s, const Layout& L, int n, const void* v, int variant, int r_groups,
-                       int rblock, void* ws, hipStream_t st) {
+                       int rblock, void* ws, hipStream_t st, float* norms = nullptr, const void* v_new = nullptr) {
     if (!variant) return KV_OK;
     VariantArgs a{};
     a.v = v;
     a.r = at<float>(ws, L.r_off);
-    a.vnorm = at<float>(ws, L.vn_off);
+    a.vnorm = norms ? norms : at<float>(ws, L.vn_off);
+    a.vnorm_stride = norms ? s.capacity : L.n_stride;
+    a.v_new = v_new;
     a.vnorm_inv_mean = at<float>(ws, L.vinv_off);
     a.entropy = at<float>(ws, L.eta_off);
     a.batch = s.batch;
@@ -328,7 +332,8 @@ kv_status run_variants(const kv_shape& s, const Layout& L, int n, const void* v,
     a.inv_hq = 1.0f / (float)s.n_q_heads;
     kv_status rc = KV_OK;
     if (variant & KV_SCORE_ENTROPY) rc = hip_status(launch_entropy(a, st));
-    if (rc == KV_OK && (variant & KV_SCORE_VNORM)) rc = hip_status(launch_vnorm(s.dtype, s.head_dim, a, st));
+    if (rc == KV_OK && (variant & KV_SCORE_VNORM))
+        rc = hip_status(norms ? launch_vnorm_mean(s.dtype, s.head_dim, a, st) : launch_vnorm(s.dtype, s.head_dim, a, st));
     return rc;
 }
 
@@ -339,6 +344,7 @@ struct FoldExtra {
     int32_t* pos = nullptr;
     int new_pos = -1;
     bool candidates = false;
+    const float* norms = nullptr;  // VNorm's norms from the caller's cache (stride cap) instead of the workspace
 };
 kv_status run_fold(const kv_shape& s, const Layout& L, int n, float* u, float* s_out, int rule, float alpha,
                    int variant, int r_groups, int rblock, bool raw_out, void* ws, hipStream_t st,
@@ -350,7 +356,8 @@ kv_status run_fold(const kv_shape& s, const Layout& L, int n, float* u, float* s
     f.raw = raw_out ? at<float>(ws, L.raw_off) : nullptr;
     f.raw_scale = (float)(1.0 / ((double)s.layers * s.n_q_heads));
     f.r = at<float>(ws, L.r_off);
-    f.vnorm = (variant & KV_SCORE_VNORM) ? at<float>(ws, L.vn_off) : nullptr;
+    f.vnorm = (variant & KV_SCORE_VNORM) ? (ex.norms ? ex.norms : at<float>(ws, L.vn_off)) : nullptr;
+    f.vnorm_stride = ex.norms ? s.capacity : L.n_stride;
     f.vnorm_inv_mean = at<float>(ws, L.vinv_off);
     f.entropy = (variant & KV_SCORE_ENTROPY) ? at<float>(ws, L.eta_off) : nullptr;
     f.u = u;
@@ -405,8 +412,9 @@ SelectArgs select_args(const kv_shape& s, const Layout& L, int n, int budget, co
 }
 
 MoveArgs move_args(const kv_shape& s, const Layout& L, int n, int budget, void* k, void* v, float* u,
-                   int32_t* pos, void* ws) {
+                   int32_t* pos, float* norms, void* ws) {
     MoveArgs m{};
+    m.norms = norms;
     m.k = k;
     m.v = v;
     m.u = u;
@@ -447,8 +455,10 @@ kv_status check_merge(const kv_shape& s, const kv_params& p) {
 bool is_refresh(const kv_params& p, int t) { return p.score_free ? (t == 1) : ((t - 1) % p.refresh_period == 0); }
 
 AppendArgs append_args(const kv_shape& s, const kv_params& p, int t, int n_in, int new_pos, const void* k_new,
-                       const void* v_new, void* k, void* v, float* u, int32_t* pos) {
+                       const void* v_new, void* k, void* v, float* u, int32_t* pos, float* norms) {
     AppendArgs ap{};
+    ap.norms = norms;
+    ap.bf16 = s.dtype == KV_BF16;
     ap.k = k;
     ap.v = v;
     ap.k_new = k_new;
@@ -467,9 +477,9 @@ AppendArgs append_args(const kv_shape& s, const kv_params& p, int t, int n_in, i
 }
 
 kv_status run_append(const kv_shape& s, const kv_params& p, int t, int n_in, int new_pos, const void* k_new,
-                     const void* v_new, void* k, void* v, float* u, int32_t* pos, hipStream_t st,
+                     const void* v_new, void* k, void* v, float* u, int32_t* pos, float* norms, hipStream_t st,
                      const kv_trace* tr) {
-    AppendArgs ap = append_args(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos);
+    AppendArgs ap = append_args(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, norms);
     record(tr, 0, true, st);
     kv_status rc = hip_status(launch_append(ap, st));
     record(tr, 0, false, st);
@@ -497,8 +507,8 @@ kv_status mark_untraced(const kv_shape& s, const kv_rank_trace* rt, hipStream_t 
 // on a refresh step, the traced top-k decisions (raw score from the fold; the EMA set is the retention
 // decision itself when k = B) and their statistics are taken before the compaction, on the same slots.
 kv_status run_select_compact(const kv_shape& s, const Layout& L, int n, int budget, void* k, void* v, float* u,
-                             int32_t* pos, uint8_t* keep_out, const kv_rank_trace* rt, bool refresh, void* ws,
-                             hipStream_t st, const kv_trace* tr) {
+                             int32_t* pos, float* norms, uint8_t* keep_out, const kv_rank_trace* rt, bool refresh,
+                             void* ws, hipStream_t st, const kv_trace* tr) {
     TraceArgs ta{};
     kv_status rc = KV_OK;
     const bool traced = rt && refresh;
@@ -540,7 +550,7 @@ kv_status run_select_compact(const kv_shape& s, const Layout& L, int n, int budg
     record(tr, 3, false, st);
     if (rc != KV_OK || n <= budget) return rc;
     record(tr, 4, true, st);
-    rc = hip_status(launch_move(move_args(s, L, n, budget, k, v, u, pos, ws), st));
+    rc = hip_status(launch_move(move_args(s, L, n, budget, k, v, u, pos, norms, ws), st));
     record(tr, 4, false, st);
     return rc;
 }
@@ -548,8 +558,11 @@ kv_status run_select_compact(const kv_shape& s, const Layout& L, int n, int budg
 // Placement of the newcomer of a single-eviction refresh step (n <= budget + 1) after a fold with
 // candidates: its K/V rows come from k_new / v_new, or from row n - 1 of the cache when those are null.
 kv_status run_place(const kv_shape& s, const Layout& L, int n, int budget, const void* k_new, const void* v_new,
-                    void* k, void* v, float* u, int32_t* pos, uint8_t* keep_out, void* ws, hipStream_t st) {
+                    void* k, void* v, float* u, int32_t* pos, float* norms, uint8_t* keep_out, void* ws,
+                    hipStream_t st) {
     PlaceArgs a{};
+    a.norms = norms;
+    a.bf16 = s.dtype == KV_BF16;
     a.k = k;
     a.v = v;
     a.u = u;
@@ -580,7 +593,8 @@ kv_status run_place(const kv_shape& s, const Layout& L, int n, int budget, const
 
 kv_status check_step(const kv_shape* shape, const kv_params* params, int t, int n_in, int new_pos, const void* q,
                      const void* k_new, const void* v_new, const void* k, const void* v, const float* u,
-                     const int32_t* pos, const int32_t* n_out, const float* s_out, const kv_rank_trace* rank_trace) {
+                     const int32_t* pos, const float* v_norms, const int32_t* n_out, const float* s_out,
+                     const kv_rank_trace* rank_trace) {
     kv_status rc = check_shape(shape);
     if (rc != KV_OK) return rc;
     const kv_shape& s = *shape;
@@ -591,22 +605,23 @@ kv_status check_step(const kv_shape* shape, const kv_params* params, int t, int 
     if (t < 1 || n_in < 0 || n_in + 1 > s.capacity || new_pos < 0) return KV_ERR_INVALID_ARG;
     if (!q || !k_new || !v_new || !k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
     if (!aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k, 16) || !aligned(v, 16) ||
-        !aligned(u, 4) || !aligned(pos, 4) || !aligned(s_out, 4))
+        !aligned(u, 4) || !aligned(pos, 4) || !aligned(s_out, 4) || !aligned(v_norms, 4))
         return KV_ERR_UNSUPPORTED;
     return KV_OK;
 }
 
-// One decode step (a0 ... a5) on validated arguments, with the workspace ws laid out as L.
+// One decode step (a0 ... a5) on validated arguments, with the workspace ws laid out as L.  v_norms (nullable):
+// the caller's value-norm cache, kept in step with V by every row write and move; VNorm reads it.
 kv_status evict_step(const kv_shape& s, const kv_params& p, int t, int n_in, int new_pos, const void* q,
-                     const void* k_new, const void* v_new, void* k, void* v, float* u, int32_t* pos, int32_t* n_out,
-                     uint8_t* keep_out, float* s_out, const kv_trace* trace, const kv_rank_trace* rank_trace,
-                     const Layout& L, void* ws, hipStream_t st) {
+                     const void* k_new, const void* v_new, void* k, void* v, float* u, int32_t* pos,
+                     float* v_norms, int32_t* n_out, uint8_t* keep_out, float* s_out, const kv_trace* trace,
+                     const kv_rank_trace* rank_trace, const Layout& L, void* ws, hipStream_t st) {
     kv_status rc = KV_OK;
     const int n = n_in + 1;
     const bool refresh = is_refresh(p, t);
     if (!refresh && n_in <= p.budget) {
         // every Lazy / Score-Free step after the first: one kernel per sequence
-        AppendArgs ap = append_args(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos);
+        AppendArgs ap = append_args(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, v_norms);
         if (rank_trace && (rc = mark_untraced(s, rank_trace, st)) != KV_OK) return rc;
         record(trace, 0, true, st);
         // the per-sequence pair counts of the workspace are free on this path: they carry the newcomer's slot
@@ -616,29 +631,33 @@ kv_status evict_step(const kv_shape& s, const kv_params& p, int t, int n_in, int
         *n_out = n < p.budget ? n : p.budget;
         return KV_OK;
     }
-    if (refresh && n_in <= p.budget && !rank_trace && !(p.score_variant & KV_SCORE_VNORM)) {
+    const bool vnorm = (p.score_variant & KV_SCORE_VNORM) != 0;
+    if (refresh && n_in <= p.budget && !rank_trace && (!vnorm || v_norms)) {
         const ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
         if (!plan.split) {
             // A steady refresh step (one eviction, or none while under budget) in three kernels: the scorer
             // takes the newcomer from k_new as row n - 1, the fold gives it the refresh prior and reports each
             // workgroup's first token to leave, and the placement writes the newcomer's rows once, into the
-            // slot it takes (the append's and the compaction's row copies in one).
+            // slot it takes (the append's and the compaction's row copies in one).  VNorm (with the norm cache
+            // only: V's row n - 1 is not written yet) adds the norms' mean, the newcomer's norm from v_new.
             const int r_groups = s.n_kv_heads / plan.merge;
             record(trace, 0, true, st);
             record(trace, 0, false, st);
             record(trace, 1, true, st);
             rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, plan, ws, st, k_new);
-            if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st);
+            if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st, v_norms, v_new);
             record(trace, 1, false, st);
             FoldExtra ex;
             ex.pos = pos;
             ex.new_pos = new_pos;
             ex.candidates = n > p.budget;
+            ex.norms = v_norms;
             if (rc == KV_OK)
                 rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, r_groups, 1, false, ws, st, trace,
                               ex);
             record(trace, 3, true, st);
-            if (rc == KV_OK) rc = run_place(s, L, n, p.budget, k_new, v_new, k, v, u, pos, keep_out, ws, st);
+            if (rc == KV_OK)
+                rc = run_place(s, L, n, p.budget, k_new, v_new, k, v, u, pos, v_norms, keep_out, ws, st);
             record(trace, 3, false, st);
             record(trace, 4, true, st);
             record(trace, 4, false, st);
@@ -647,20 +666,23 @@ kv_status evict_step(const kv_shape& s, const kv_params& p, int t, int n_in, int
             return KV_OK;
         }
     }
-    if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, st, trace)) != KV_OK) return rc;
+    if ((rc = run_append(s, p, t, n_in, new_pos, k_new, v_new, k, v, u, pos, v_norms, st, trace)) != KV_OK)
+        return rc;
     if (refresh) {
         const ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
         const int r_groups = s.n_kv_heads / plan.merge;
         record(trace, 1, true, st);
         rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, plan, ws, st);
-        if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st);
+        if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st, v_norms);
         record(trace, 1, false, st);
+        FoldExtra ex;
+        ex.norms = v_norms;
         if (rc == KV_OK)
             rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, r_groups, 1, rank_trace != nullptr,
-                          ws, st, trace);
+                          ws, st, trace, ex);
         if (rc != KV_OK) return rc;
     }
-    rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, trace);
+    rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, v_norms, keep_out, rank_trace, refresh, ws, st, trace);
     if (rc != KV_OK) return rc;
     *n_out = n < p.budget ? n : p.budget;
     return KV_OK;
@@ -730,13 +752,14 @@ kv_status kv_topk_select(const kv_shape* shape, int32_t n, int32_t budget, const
 }
 
 kv_status kv_compact(const kv_shape* shape, int32_t n, int32_t budget, const uint8_t* keep, void* k, void* v,
-                     float* u, int32_t* pos, void* ws, size_t ws_bytes, void* stream) {
+                     float* u, int32_t* pos, float* v_norms, void* ws, size_t ws_bytes, void* stream) {
     kv_status rc = check_shape(shape);
     if (rc != KV_OK) return rc;
     const kv_shape& s = *shape;
     if (n < 1 || n > s.capacity || budget < 1) return KV_ERR_INVALID_ARG;
     if (!keep || !k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
-    if (!aligned(k, 16) || !aligned(v, 16) || !aligned(u, 4) || !aligned(pos, 4)) return KV_ERR_UNSUPPORTED;
+    if (!aligned(k, 16) || !aligned(v, 16) || !aligned(u, 4) || !aligned(pos, 4) || !aligned(v_norms, 4))
+        return KV_ERR_UNSUPPORTED;
     const Layout L = layout_for(s, n);
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
     if (n <= budget) return KV_OK;  // nothing is dropped, nothing moves
@@ -744,29 +767,29 @@ kv_status kv_compact(const kv_shape* shape, int32_t n, int32_t budget, const uin
     SelectArgs a = select_args(s, L, n, budget, u, pos, ws);
     a.keep_in = keep;
     if ((rc = hip_status(launch_select(a, true, st))) != KV_OK) return rc;
-    return hip_status(launch_move(move_args(s, L, n, budget, k, v, u, pos, ws), st));
+    return hip_status(launch_move(move_args(s, L, n, budget, k, v, u, pos, v_norms, ws), st));
 }
 
 kv_status kv_evict_step(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in,
                         int32_t new_pos, const void* q, const void* k_new, const void* v_new, void* k, void* v,
-                        float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
+                        float* u, int32_t* pos, float* v_norms, int32_t* n_out, uint8_t* keep_out, float* s_out,
                         const kv_trace* trace, const kv_rank_trace* rank_trace, void* ws, size_t ws_bytes,
                         void* stream) {
-    kv_status rc = check_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, n_out, s_out,
-                              rank_trace);
+    kv_status rc = check_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, v_norms, n_out,
+                              s_out, rank_trace);
     if (rc != KV_OK) return rc;
     const Layout L = layout_for(*shape, n_in + 1);
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
-    return evict_step(*shape, *params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, n_out, keep_out, s_out,
-                      trace, rank_trace, L, ws, static_cast<hipStream_t>(stream));
+    return evict_step(*shape, *params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, v_norms, n_out, keep_out,
+                      s_out, trace, rank_trace, L, ws, static_cast<hipStream_t>(stream));
 }
 
 kv_status kv_evict_step_static(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in,
                                int32_t new_pos, const void* q, const void* k_new, const void* v_new, void* k,
-                               void* v, float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
-                               const kv_trace* trace, const kv_rank_trace* rank_trace, void* stream) {
-    kv_status rc = check_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, n_out, s_out,
-                              rank_trace);
+                               void* v, float* u, int32_t* pos, float* v_norms, int32_t* n_out, uint8_t* keep_out,
+                               float* s_out, const kv_trace* trace, const kv_rank_trace* rank_trace, void* stream) {
+    kv_status rc = check_step(shape, params, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, v_norms, n_out,
+                              s_out, rank_trace);
     if (rc != KV_OK) return rc;
     const kv_shape& s = *shape;
     const kv_params& p = *params;
@@ -777,12 +800,13 @@ kv_status kv_evict_step_static(const kv_shape* shape, const kv_params* params, i
     if (L.total > kStaticScratchBytes) return KV_ERR_WORKSPACE;
     void* ws = nullptr;
     if ((rc = static_scratch(&ws)) != KV_OK) return rc;
-    return evict_step(s, p, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, n_out, keep_out, s_out, trace,
-                      rank_trace, L, ws, static_cast<hipStream_t>(stream));
+    return evict_step(s, p, t, n_in, new_pos, q, k_new, v_new, k, v, u, pos, v_norms, n_out, keep_out, s_out,
+                      trace, rank_trace, L, ws, static_cast<hipStream_t>(stream));
 }
 
 kv_status kv_append(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n_in, int32_t new_pos,
-                    const void* k_new, const void* v_new, void* k, void* v, float* u, int32_t* pos, void* stream) {
+                    const void* k_new, const void* v_new, void* k, void* v, float* u, int32_t* pos, float* v_norms,
+                    void* stream) {
     kv_status rc = check_shape(shape);
     if (rc != KV_OK) return rc;
     const kv_shape& s = *shape;
@@ -790,10 +814,10 @@ kv_status kv_append(const kv_shape* shape, const kv_params* params, int32_t t, i
     if (t < 1 || n_in < 0 || n_in + 1 > s.capacity || new_pos < 0) return KV_ERR_INVALID_ARG;
     if (!k_new || !v_new || !k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
     if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(u, 4) ||
-        !aligned(pos, 4))
+        !aligned(pos, 4) || !aligned(v_norms, 4))
         return KV_ERR_UNSUPPORTED;
-    return run_append(s, *params, t, n_in, new_pos, k_new, v_new, k, v, u, pos, static_cast<hipStream_t>(stream),
-                      nullptr);
+    return run_append(s, *params, t, n_in, new_pos, k_new, v_new, k, v, u, pos, v_norms,
+                      static_cast<hipStream_t>(stream), nullptr);
 }
 
 kv_status kv_attend_score(const kv_shape* shape, int32_t layer0, int32_t layer_count, int32_t n, const void* q,
@@ -836,7 +860,7 @@ kv_status kv_attend_score(const kv_shape* shape, int32_t layer0, int32_t layer_c
 }
 
 kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_t t, int32_t n, void* k, void* v,
-                          float* u, int32_t* pos, int32_t* n_out, uint8_t* keep_out, float* s_out,
+                          float* u, int32_t* pos, float* v_norms, int32_t* n_out, uint8_t* keep_out, float* s_out,
                           const kv_rank_trace* rank_trace, void* ws, size_t ws_bytes, void* stream) {
     kv_status rc = check_shape(shape);
     if (rc != KV_OK) return rc;
@@ -847,7 +871,8 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
     if ((rc = check_merge(s, p)) != KV_OK) return rc;
     if (!n_out || t < 1 || n < 1 || n > s.capacity) return KV_ERR_INVALID_ARG;
     if (!k || !v || !u || !pos) return KV_ERR_INVALID_ARG;
-    if (!aligned(k, 16) || !aligned(v, 16) || !aligned(u, 4) || !aligned(pos, 4) || !aligned(s_out, 4))
+    if (!aligned(k, 16) || !aligned(v, 16) || !aligned(u, 4) || !aligned(pos, 4) || !aligned(s_out, 4) ||
+        !aligned(v_norms, 4))
         return KV_ERR_UNSUPPORTED;
     const Layout L = layout_for(s, n);
     if ((rc = check_ws(L, ws, ws_bytes)) != KV_OK) return rc;
@@ -857,30 +882,34 @@ kv_status kv_evict_finish(const kv_shape* shape, const kv_params* params, int32_
     // eviction and moves the newcomer (row n - 1, appended by kv_append) into its slot
     const bool single = refresh && n <= p.budget + 1 && !rank_trace;
     if (refresh) {
-        // value norms already written by the step's attention calls: only the entropy factors remain
-        const int computed = (p.score_variant & KV_SCORE_NORMS_EMITTED) ? (p.score_variant & ~KV_SCORE_VNORM)
-                                                                         : p.score_variant;
+        // value norms already written by the step's attention calls: only the entropy factors remain; else the
+        // norms come from the caller's norm cache (kv_append cached the newcomer's) or from V
+        const bool emitted = (p.score_variant & KV_SCORE_NORMS_EMITTED) != 0;
+        const int computed = emitted ? (p.score_variant & ~KV_SCORE_VNORM) : p.score_variant;
+        float* cache_norms = emitted ? nullptr : v_norms;
         // the attention wrote one row of r per KV head; they are added in the blocks the scorer would merge,
         // so the fused and the separate step give identical utilities
         const int rblock = scorer_plan(s, L, p.score_variant, p.score_merge).merge;
         if ((rc = run_variants(s, L, n, v, computed & (KV_SCORE_VNORM | KV_SCORE_ENTROPY), s.n_kv_heads, rblock,
-                               ws, st)) != KV_OK)
+                               ws, st, cache_norms)) != KV_OK)
             return rc;
         FoldExtra ex;
         ex.pos = pos;
         ex.candidates = single && n > p.budget;
+        ex.norms = cache_norms;
         rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, s.n_kv_heads, rblock,
                       rank_trace != nullptr, ws, st, nullptr, ex);
         if (rc != KV_OK) return rc;
     }
     if (single) {
         if (n > p.budget || keep_out)
-            rc = run_place(s, L, n, p.budget, nullptr, nullptr, k, v, u, pos, keep_out, ws, st);
+            rc = run_place(s, L, n, p.budget, nullptr, nullptr, k, v, u, pos, v_norms, keep_out, ws, st);
         if (rc != KV_OK) return rc;
         *n_out = n < p.budget ? n : p.budget;
         return KV_OK;
     }
-    rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, keep_out, rank_trace, refresh, ws, st, nullptr);
+    rc = run_select_compact(s, L, n, p.budget, k, v, u, pos, v_norms, keep_out, rank_trace, refresh, ws, st,
+                            nullptr);
     if (rc != KV_OK) return rc;
     *n_out = n < p.budget ? n : p.budget;
     return KV_OK;
@@ -910,6 +939,26 @@ kv_status kv_score_plan(const kv_shape* shape, int32_t n, const kv_params* param
         info->chunks = cp.nchunk;
     }
     return KV_OK;
+}
+
+kv_status kv_value_norms(const kv_shape* shape, int32_t n, const void* v, float* v_norms, void* stream) {
+    kv_status rc = check_shape(shape);
+    if (rc != KV_OK) return rc;
+    const kv_shape& s = *shape;
+    if (n < 1 || n > s.capacity || !v || !v_norms) return KV_ERR_INVALID_ARG;
+    if (!aligned(v, 16) || !aligned(v_norms, 4)) return KV_ERR_UNSUPPORTED;
+    VariantArgs a{};
+    a.v = v;
+    a.vnorm = v_norms;
+    a.vnorm_stride = s.capacity;
+    a.batch = s.batch;
+    a.layers = s.layers;
+    a.hkv = s.n_kv_heads;
+    a.cap = s.capacity;
+    a.n = n;
+    a.n_stride = (n + 63) / 64 * 64;
+    a.norms_direct = 1;  // the cache is not padded: one store per live row
+    return hip_status(launch_vnorm(s.dtype, s.head_dim, a, static_cast<hipStream_t>(stream)));
 }
 
 kv_status kv_fault_status(void* ws, size_t ws_bytes, uint32_t* out, int32_t clear, void* stream) {

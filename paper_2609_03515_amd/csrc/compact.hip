@@ -48,6 +48,14 @@ __global__ __launch_bounds__(kThreads) void move_kernel(MoveArgs a) {
 #pragma unroll
     for (int i = 0; i < kMoveUnroll; ++i)
         if (dst[i] >= 0) __builtin_nontemporal_store(x[i], reinterpret_cast<u32x4*>(base + (size_t)dst[i] * a.row_bytes) + c);
+    if (a.norms && tensor == 1 && c == 0) {  // V blocks also move their slab's value norms
+        float* nb = a.norms + ((size_t)(l * a.batch + b) * a.hkv + g) * a.cap;
+#pragma unroll
+        for (int i = 0; i < kMoveUnroll; ++i) {
+            const int j = j0 + i * rows_per_pass;
+            if (j < np) nb[pd[j]] = nb[ps[j]];
+        }
+    }
     if (blockIdx.y == 0 && c == 0) {  // layer 0, KV head 0, K: the rows' utilities and positions
 #pragma unroll
         for (int i = 0; i < kMoveUnroll; ++i) {
@@ -62,7 +70,8 @@ __global__ __launch_bounds__(kThreads) void move_kernel(MoveArgs a) {
 }
 
 // Blocks [0, batch): prior utility and position of the appended token of one sequence.
-// Blocks >= batch: copies of the new K/V rows into slot n_in of every slab.
+// Blocks [batch, batch + copy blocks): copies of the new K/V rows into slot n_in of every slab.
+// Blocks after those (with a norm cache): the new V rows' norms into slot n_in of the cache.
 __global__ __launch_bounds__(kThreads) void append_kernel(AppendArgs a) {
     if ((int)blockIdx.x < a.batch) {
         __shared__ float red[kThreads / kWave];
@@ -94,8 +103,19 @@ __global__ __launch_bounds__(kThreads) void append_kernel(AppendArgs a) {
         return;
     }
     const int lpr = a.row_bytes / 16;
-    const long long gid = (long long)(blockIdx.x - a.batch) * blockDim.x + threadIdx.x;
     const long long total = (long long)a.layers * a.batch * a.hkv * 2 * lpr;
+    const long long copy_blocks = (total + kThreads - 1) / kThreads;
+    if ((long long)blockIdx.x >= a.batch + copy_blocks) {
+        // one aligned lane group per row (l, b, g); groups leave or stay together
+        const int nl = norm_lanes(a.row_bytes);
+        const long long r = ((long long)blockIdx.x - a.batch - copy_blocks) * (kThreads / nl) + threadIdx.x / nl;
+        if (r >= (long long)a.layers * a.batch * a.hkv) return;
+        const float nrm = row_norm(static_cast<const char*>(a.v_new) + r * a.row_bytes, a.row_bytes, a.bf16 != 0,
+                                   (int)threadIdx.x % nl);
+        if ((int)threadIdx.x % nl == 0) a.norms[r * a.cap + a.n_in] = nrm;
+        return;
+    }
+    const long long gid = (long long)(blockIdx.x - a.batch) * blockDim.x + threadIdx.x;
     if (gid >= total) return;
     const int c = (int)(gid % lpr);
     long long row = gid / lpr;  // (tensor, l, b, g) with tensor outermost
@@ -193,7 +213,17 @@ __global__ __launch_bounds__(kNrThreads) void nonrefresh_kernel(AppendArgs a, ui
         const int evicted = slot < 0 ? n : (slot < n ? slot : -1);
         for (int i = tid; i <= n; i += kNrThreads) keep_out[(size_t)b * a.cap + i] = i != evicted;
     }
-    if (!copy_rows || slot < 0) return;
+    if (slot < 0) return;
+    if (a.norms) {  // the newcomer's value norms, one aligned lane group per (layer, KV head) row
+        const int nl = norm_lanes(a.row_bytes);
+        for (int r = tid / nl; r < a.layers * a.hkv; r += kNrThreads / nl) {
+            const size_t row = ((size_t)(r / a.hkv) * a.batch + b) * a.hkv + r % a.hkv;
+            const float nrm = row_norm(static_cast<const char*>(a.v_new) + row * a.row_bytes, a.row_bytes,
+                                       a.bf16 != 0, tid % nl);
+            if (tid % nl == 0) a.norms[row * a.cap + slot] = nrm;
+        }
+    }
+    if (!copy_rows) return;
     // rows r = (tensor, l, g) in [0, 2 L hkv), 16-byte chunk ch; quotients by float reciprocals (exact: the
     // numerators are far below 2^22 and the +0.5 keeps them off integer boundaries)
     const int lpr = a.row_bytes / 16;
@@ -301,6 +331,15 @@ __global__ __launch_bounds__(kPlaceThreads) void place_kernel(PlaceArgs a) {
         for (int i = l * per + tid; i < i1; i += kPlaceThreads) a.keep_out[(size_t)b * a.cap + i] = i != evicted;
     }
     if (slot < 0) return;
+    if (a.norms) {  // the newcomer's value norms of this layer, into the slot it takes
+        const int nl = norm_lanes(a.row_bytes);
+        for (int g = tid / nl; g < a.hkv; g += kPlaceThreads / nl) {
+            const size_t slab = ((size_t)l * a.batch + b) * a.hkv + g;
+            const float nrm = row_norm(static_cast<const char*>(a.src_v) + (slab * a.src_slab_rows + a.src_row0) *
+                                       a.row_bytes, a.row_bytes, a.bf16 != 0, tid % nl);
+            if (tid % nl == 0) a.norms[slab * a.cap + slot] = nrm;
+        }
+    }
     if (l == 0 && tid == 0 && slot != n - 1) {
         a.u[(size_t)b * a.cap + slot] = a.u[(size_t)b * a.cap + n - 1];
         a.pos[(size_t)b * a.cap + slot] = a.pos[(size_t)b * a.cap + n - 1];
@@ -357,7 +396,9 @@ hipError_t launch_move(const MoveArgs& a, hipStream_t s) {
 
 hipError_t launch_append(const AppendArgs& a, hipStream_t s) {
     const long long threads = (long long)a.layers * a.batch * a.hkv * 2 * (a.row_bytes / 16);
-    const long long blocks = a.batch + (threads + kThreads - 1) / kThreads;
+    const long long rows = (long long)a.layers * a.batch * a.hkv;
+    const int groups = kThreads / (a.row_bytes >= 256 ? 16 : a.row_bytes / 16);  // norm rows per block
+    const long long blocks = a.batch + (threads + kThreads - 1) / kThreads + (a.norms ? (rows + groups - 1) / groups : 0);
     hipLaunchKernelGGL(append_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }

@@ -45,14 +45,24 @@ __global__ __launch_bounds__(kThreads) void fold_kernel(FoldArgs a) {
             if (a.vnorm) {  // r_groups == hkv: one row per KV head
                 // VNorm: each KV head's group sum times the token's value-norm factor norm / mean norm
                 // (factor 1 where the slab's norms are all zero)
-                const float* nl = a.vnorm + ((size_t)(l * a.batch + b) * a.hkv) * a.n_stride + tok0;
+                // norms in the workspace (stride n_stride, rows padded to 64: 16-byte loads) or in the caller's
+                // norm cache (stride cap, unpadded: the live rows only, one by one)
+                const float* nl = a.vnorm + ((size_t)(l * a.batch + b) * a.hkv) * a.vnorm_stride + tok0;
                 const float* il = a.vnorm_inv_mean + (size_t)(l * a.batch + b) * a.hkv;
+                const bool padded = a.vnorm_stride == a.n_stride;
                 f32x4 plain = {0.0f, 0.0f, 0.0f, 0.0f};
                 for (int g = 0; g < a.hkv; ++g) {
                     const f32x4 rg = *reinterpret_cast<const f32x4*>(rl + (size_t)g * a.n_stride);
                     const float im = il[g];
-                    const f32x4 f = im > 0.0f ? *reinterpret_cast<const f32x4*>(nl + (size_t)g * a.n_stride) * im
-                                              : f32x4{1.0f, 1.0f, 1.0f, 1.0f};
+                    const float* ng = nl + (size_t)g * a.vnorm_stride;
+                    f32x4 nv;
+                    if (padded) {
+                        nv = *reinterpret_cast<const f32x4*>(ng);
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) nv[j] = tok0 + j < a.n ? ng[j] : 0.0f;
+                    }
+                    const f32x4 f = im > 0.0f ? nv * im : f32x4{1.0f, 1.0f, 1.0f, 1.0f};
                     s += rg * f;
                     plain += rg;
                 }

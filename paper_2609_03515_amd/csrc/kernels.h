@@ -129,6 +129,7 @@ struct FoldArgs {
     const float* vnorm;           // nullable: [layers][batch][n_kv][n_stride] value-row l2 norms
     const float* vnorm_inv_mean;  // [layers][batch][n_kv] 1 / mean norm (0: all norms zero, factor 1)
     const float* entropy;         // nullable: [layers][batch] normalised entropy of the layer's attention
+    int vnorm_stride;             // row stride of vnorm: n_stride (workspace) or cap (the caller's norm cache)
     float* raw;                   // nullable: [batch][cap] rank trace's raw score (plain scores, layer mean)
     float raw_scale;              // 1 / (layers * n_q)
     float* u;
@@ -155,14 +156,22 @@ int fold_groups(int n);
 struct VariantArgs {
     const void* v;
     const float* r;
-    float* vnorm;           // [layers][batch][n_kv][n_stride]
-    float* vnorm_inv_mean;  // [layers][batch][n_kv]
+    float* vnorm;           // [layers][batch][n_kv][vnorm_stride]
+    float* vnorm_inv_mean;  // [layers][batch][n_kv] (nullable for launch_vnorm: norms only)
     float* entropy;         // [layers][batch]
     int batch, layers, hkv, cap, n, n_stride;
+    int vnorm_stride;       // n_stride (workspace norms) or cap (the caller's norm cache)
+    int norms_direct;       // launch_vnorm: one 4-byte store per live row (unpadded rows, e.g. the norm cache)
     int r_groups, rblock;  // as in FoldArgs
     float inv_hq;
+    // launch_vnorm_mean: when non-null, row n - 1 is the step's newcomer, not yet cached: its norm is taken
+    // from v_new ([layers][batch][n_kv][d]) and written to the cache before the mean
+    const void* v_new;
 };
+// Norms of rows [0, n) read from V into vnorm, and (when vnorm_inv_mean is set) each slab's n / sum of norms.
 hipError_t launch_vnorm(int dtype, int head_dim, const VariantArgs& a, hipStream_t s);
+// Each slab's n / sum of norms from the norm cache (vnorm, stride cap), with the newcomer's norm from v_new.
+hipError_t launch_vnorm_mean(int dtype, int head_dim, const VariantArgs& a, hipStream_t s);
 hipError_t launch_entropy(const VariantArgs& a, hipStream_t s);
 
 // Rank trace (appendix "Mechanistic Diagnostics"): per-sequence set statistics (the raw step score comes from
@@ -207,6 +216,7 @@ struct MoveArgs {
     int batch, layers, hkv, cap, row_bytes;
     int max_pairs;    // loop bound on pairs per sequence
     int pair_stride;  // row stride of pair_dst / pair_src
+    float* norms;     // nullable: value-norm cache [layers][batch][n_kv][cap], moved with V
 };
 hipError_t launch_move(const MoveArgs& a, hipStream_t s);
 
@@ -220,6 +230,9 @@ struct AppendArgs {
     int32_t* pos;
     int batch, layers, hkv, cap, row_bytes, n_in, new_pos;
     int init_mode;  // 0: zero (refresh step), 1: mean, 2: min of u[0, n_in)
+    float* norms;   // nullable: value-norm cache [layers][batch][n_kv][cap]: the newcomer's norms are written
+                    // where its V rows go
+    int bf16;       // element type of the rows (for the norms)
 };
 hipError_t launch_append(const AppendArgs& a, hipStream_t s);
 // A non-refresh step on a cache of n_in <= budget tokens (init_mode 1 or 2): the newcomer's prior, the single
@@ -245,6 +258,8 @@ struct PlaceArgs {
     uint8_t* keep_out;      // nullable: the decision over the n slots
     int ncand;
     int batch, layers, hkv, cap, row_bytes, n, budget;
+    float* norms;           // nullable: value-norm cache, the newcomer's norms written into its slot
+    int bf16;
 };
 hipError_t launch_place(const PlaceArgs& a, hipStream_t s);
 

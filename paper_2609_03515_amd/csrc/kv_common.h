@@ -164,6 +164,42 @@ struct Elem<bf16_t> {
     }
 };
 
+// l2 norm of one value row, as every producer of VNorm's norms computes it: an aligned group of LPR lanes
+// (LPR = min(16, the row's 16-byte chunks)), lane p squaring and adding the elements of its chunks p, p + LPR,
+// ... in order, then a DPP sum over the group.  The same arithmetic at append time and in a pass over V gives
+// bit-identical norms.  Every lane of the group must call it (the sum crosses lanes).
+template <typename T, int LPR, int CPL>
+__device__ __forceinline__ float row_norm_lanes(const typename Elem<T>::chunk_t (&c)[CPL]) {
+    float ss = 0.0f;
+#pragma unroll
+    for (int cc = 0; cc < CPL; ++cc) {
+        float f[Elem<T>::kPerChunk];
+        Elem<T>::unpack(c[cc], f);
+#pragma unroll
+        for (int x = 0; x < Elem<T>::kPerChunk; ++x) ss = fmaf(f[x], f[x], ss);
+    }
+    return sqrtf(group_allsum<LPR>(ss));
+}
+
+// Lanes per row of row_norm (the group size): min(16, row_bytes / 16).
+__device__ __forceinline__ int norm_lanes(int row_bytes) { return row_bytes >= 256 ? 16 : row_bytes / 16; }
+
+// row_norm_lanes for a row of `row_bytes` bytes (64 or 128 elements of bf16 or f32) at `row`, 16-byte aligned;
+// p = the lane's index in its group of norm_lanes(row_bytes) lanes.
+__device__ __forceinline__ float row_norm(const void* row, int row_bytes, bool bf16, int p) {
+    const u32x4* rp = static_cast<const u32x4*>(row);
+    if (bf16) {
+        const u32x4 c[1] = {rp[p]};
+        return row_bytes == 256 ? row_norm_lanes<bf16_t, 16, 1>(c) : row_norm_lanes<bf16_t, 8, 1>(c);
+    }
+    if (row_bytes == 512) {
+        const f32x4 c[2] = {__builtin_bit_cast(f32x4, rp[p]), __builtin_bit_cast(f32x4, rp[p + 16])};
+        return row_norm_lanes<float, 16, 2>(c);
+    }
+    const f32x4 c[1] = {__builtin_bit_cast(f32x4, rp[p])};
+    return row_norm_lanes<float, 16, 1>(c);
+}
+
 __host__ __device__ constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x >> 1); }
 __host__ __device__ constexpr size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 

@@ -40,7 +40,11 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int p = lane % LPR;
     const int grp = lane / LPR;
-    const __amdgpu_buffer_rsrc_t out = raw_rsrc(a.vnorm + slab * a.n_stride, a.n_stride * 4);
+    // workspace norms (stride n_stride, padded to 64 rows): staged 16-byte stores; the caller's norm cache
+    // (stride cap, no padding): one 4-byte store per live row
+    const bool direct = a.norms_direct != 0;
+    float* nrow = a.vnorm + slab * a.vnorm_stride;
+    const __amdgpu_buffer_rsrc_t out = raw_rsrc(nrow, direct ? 0 : a.n_stride * 4);
     // row of (pass base, k) for this lane: the wave's block, then k-major, row groups innermost
     auto row_of = [&](int base, int k) { return base + wave * RPW + k * GPW + grp; };
     auto load = [&](int base, chunk_t (&c)[kRows][CPL]) {
@@ -56,22 +60,16 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
     auto reduce = [&](int base, const chunk_t (&c)[kRows][CPL]) {
 #pragma unroll
         for (int k = 0; k < kRows; ++k) {
-            float ss = 0.0f;
-#pragma unroll
-            for (int cc = 0; cc < CPL; ++cc) {
-                float f[EPC];
-                E::unpack(c[k][cc], f);
-#pragma unroll
-                for (int x = 0; x < EPC; ++x) ss = fmaf(f[x], f[x], ss);
-            }
-            ss = group_allsum<LPR>(ss);  // DPP inside the row's aligned lane group
+            const float nr = row_norm_lanes<T, LPR, CPL>(c[k]);  // DPP inside the row's aligned lane group
             const int row = row_of(base, k);
             if (p == 0) {
-                const float nrm = row < a.n ? sqrtf(ss) : 0.0f;
+                const float nrm = row < a.n ? nr : 0.0f;
                 stage[wave][k * GPW + grp] = nrm;
                 sum += nrm;
+                if (direct && row < a.n) nrow[row] = nrm;
             }
         }
+        if (direct) return;
         // the wave's RPW consecutive norms, 4 per lane (a group starting below n ends inside the padded stride,
         // a multiple of 64); the wave's own LDS row, so only the wave's order matters
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -91,9 +89,59 @@ __global__ __launch_bounds__(kVThreads) void vnorm_kernel(VariantArgs a) {
     for (int o = 1; o < kWave; o <<= 1) sum += __shfl_xor(sum, o, kWave);
     if (lane == 0) part[wave] = sum;
     __syncthreads();
-    if (threadIdx.x == 0) {
+    if (threadIdx.x == 0 && a.vnorm_inv_mean) {
         float tot = 0.0f;
         for (int w = 0; w < kWavesV; ++w) tot += part[w];
+        a.vnorm_inv_mean[slab] = tot > 0.0f ? (float)a.n / tot : 0.0f;
+    }
+}
+
+// The slab's n / (sum of its n value norms) from the caller's norm cache (VNorm without reading V).  With
+// v_new set, row n - 1 is the step's newcomer, not cached yet: one lane group computes its norm from v_new
+// (row_norm_lanes, as at append) and writes it to the cache, the others add the n - 1 cached norms.  The sum
+// runs in a fixed order (thread-strided partial sums, a fixed butterfly, the waves in order), so the result
+// is deterministic.
+constexpr int kMThreads = 256;
+
+template <typename T, int D>
+__global__ __launch_bounds__(kMThreads) void vnorm_mean_kernel(VariantArgs a) {
+    using chunk_t = typename Elem<T>::chunk_t;
+    constexpr int CH = D / Elem<T>::kPerChunk, LPR = CH >= 16 ? 16 : CH, CPL = CH / LPR;
+    __shared__ float part[kMThreads / kWave];
+    __shared__ float newcomer;
+    const size_t slab = blockIdx.x;
+    float* nb = a.vnorm + slab * a.vnorm_stride;
+    const int m = a.v_new ? a.n - 1 : a.n;  // cached rows whose norms are read
+    if (a.v_new && threadIdx.x < LPR) {
+        const chunk_t* row = reinterpret_cast<const chunk_t*>(static_cast<const T*>(a.v_new) + slab * D);
+        chunk_t c[CPL];
+#pragma unroll
+        for (int cc = 0; cc < CPL; ++cc) c[cc] = row[threadIdx.x + cc * LPR];
+        const float nrm = row_norm_lanes<T, LPR, CPL>(c);
+        if (threadIdx.x == 0) {
+            nb[a.n - 1] = nrm;
+            newcomer = nrm;
+        }
+    }
+    constexpr int kU = 4;  // loads in flight per thread
+    float sum = 0.0f;
+    int i = threadIdx.x;
+    for (; i + (kU - 1) * kMThreads < m; i += kU * kMThreads) {
+        float x[kU];
+#pragma unroll
+        for (int j = 0; j < kU; ++j) x[j] = nb[i + j * kMThreads];
+#pragma unroll
+        for (int j = 0; j < kU; ++j) sum += x[j];
+    }
+    for (; i < m; i += kMThreads) sum += nb[i];
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) sum += __shfl_xor(sum, o, kWave);
+    if ((threadIdx.x & (kWave - 1)) == 0) part[threadIdx.x / kWave] = sum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float tot = 0.0f;
+        for (int w = 0; w < kMThreads / kWave; ++w) tot += part[w];
+        if (a.v_new) tot += newcomer;
         a.vnorm_inv_mean[slab] = tot > 0.0f ? (float)a.n / tot : 0.0f;
     }
 }
@@ -156,6 +204,18 @@ hipError_t launch_vnorm(int dtype, int head_dim, const VariantArgs& a, hipStream
     } else {
         if (head_dim == 64) hipLaunchKernelGGL((vnorm_kernel<bf16_t, 64>), grid, dim3(kVThreads), 0, s, a);
         else hipLaunchKernelGGL((vnorm_kernel<bf16_t, 128>), grid, dim3(kVThreads), 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_vnorm_mean(int dtype, int head_dim, const VariantArgs& a, hipStream_t s) {
+    const dim3 grid((unsigned)((size_t)a.layers * a.batch * a.hkv));
+    if (dtype == 0) {
+        if (head_dim == 64) hipLaunchKernelGGL((vnorm_mean_kernel<float, 64>), grid, dim3(kMThreads), 0, s, a);
+        else hipLaunchKernelGGL((vnorm_mean_kernel<float, 128>), grid, dim3(kMThreads), 0, s, a);
+    } else {
+        if (head_dim == 64) hipLaunchKernelGGL((vnorm_mean_kernel<bf16_t, 64>), grid, dim3(kMThreads), 0, s, a);
+        else hipLaunchKernelGGL((vnorm_mean_kernel<bf16_t, 128>), grid, dim3(kMThreads), 0, s, a);
     }
     return hipGetLastError();
 }

@@ -43,15 +43,15 @@ int main(void) {
     int32_t n_out = -7;
     void* fake = (void*)(uintptr_t)(1u << 20); /* never dereferenced: validation fails first */
     /* no workspace: rejected before anything is queued, n_out untouched */
-    CHECK(kv_evict_step(&s, &p, 2, 3277, 40000, fake, fake, fake, fake, fake, (float*)fake, (int32_t*)fake, &n_out,
+    CHECK(kv_evict_step(&s, &p, 2, 3277, 40000, fake, fake, fake, fake, fake, (float*)fake, (int32_t*)fake, NULL, &n_out,
                         NULL, NULL, NULL, NULL, NULL, 0, NULL) == KV_ERR_WORKSPACE);
     CHECK(n_out == -7);
     p.alpha = 1.0f;
-    CHECK(kv_evict_step(&s, &p, 2, 3277, 40000, fake, fake, fake, fake, fake, (float*)fake, (int32_t*)fake, &n_out,
+    CHECK(kv_evict_step(&s, &p, 2, 3277, 40000, fake, fake, fake, fake, fake, (float*)fake, (int32_t*)fake, NULL, &n_out,
                         NULL, NULL, NULL, NULL, NULL, 0, NULL) == KV_ERR_INVALID_ARG);
     p.alpha = 0.9f;
     p.score_merge = 3; /* not a divisor of the 8 KV heads */
-    CHECK(kv_evict_step(&s, &p, 2, 3277, 40000, fake, fake, fake, fake, fake, (float*)fake, (int32_t*)fake, &n_out,
+    CHECK(kv_evict_step(&s, &p, 2, 3277, 40000, fake, fake, fake, fake, fake, (float*)fake, (int32_t*)fake, NULL, &n_out,
                         NULL, NULL, NULL, NULL, NULL, 0, NULL) == KV_ERR_INVALID_ARG);
     p.score_merge = 0;
     CHECK(kv_attend_score(&s, 30, 3, 3278, fake, fake, fake, (const int32_t*)fake, 40000, 0.5f, 64, 1, fake, NULL, 0,
@@ -74,6 +74,7 @@ int main(void) {
         CHECK(kv_set_exchange_wait_limit(-1) == def);
     }
     (void)KV_FAULT_EXCHANGE_TIMEOUT;
+    CHECK(kv_value_norms(&s, 0, fake, (float*)fake, NULL) == KV_ERR_INVALID_ARG);
 
     CHECK(strcmp(kv_status_string(KV_OK), "ok") == 0);
     CHECK(strlen(kv_status_string(KV_ERR_HIP)) > 0);

@@ -84,3 +84,19 @@ def assert_o(o_gpu, o_ref, scale, dtype, what):
     bad = np.nonzero(err > lim)
     assert len(bad[0]) == 0, (f"{what}: {len(bad[0])} of {err.size} outputs outside tolerance; worst "
                               f"err/scale {np.max(err / (scale + 1e-30)):.3e} at {tuple(b[0] for b in bad)}")
+
+
+def check_norm_cache(B, shape, v_dev, norms, n, v_ref_raw, dtype, what, b=None, v_ref_seq=None):
+    """The value-norm cache's live rows [0, n): bit for bit the norms kv_value_norms recomputes from the GPU's V
+    (one arithmetic produces every cached norm, so appends and moves must have kept each norm beside its row),
+    and within 1e-5 relative of the float64 l2 norms of the oracle's V rows.  v_ref_raw: the oracle's V of the
+    whole batch [K, b, H_kv, cap, d]; or, for sequence b only, v_ref_seq [K, H_kv, cap, d]."""
+    fresh = torch.full_like(norms, -1.0)
+    B.kv_value_norms(shape, n, v_dev, fresh)
+    torch.cuda.synchronize()
+    got = norms[..., :n] if b is None else norms[:, b, :, :n]
+    want = fresh[..., :n] if b is None else fresh[:, b, :, :n]
+    assert torch.equal(got, want), f"{what}: cached norms differ from the norms of the rows beside them"
+    ref = v_ref_raw if b is None else v_ref_seq
+    v64 = to_f64(np.asarray(ref)[..., :n, :], dtype)
+    assert_close(got.cpu().numpy(), np.sqrt((v64 * v64).sum(axis=-1)), f"{what} norms", rel=1e-5)

@@ -105,22 +105,25 @@ def test_select_compact_validation(lib):
     assert L.kv_topk_select(ctypes.byref(s), 10, 0, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == B.KV_ERR_INVALID_ARG
     assert L.kv_topk_select(ctypes.byref(s), 10, 5, None, FAKE, FAKE, FAKE, 1 << 30, None) == B.KV_ERR_INVALID_ARG
     assert L.kv_topk_select(ctypes.byref(s), 10, 5, FAKE, FAKE, FAKE, None, 0, None) == B.KV_ERR_WORKSPACE
-    assert L.kv_compact(ctypes.byref(s), 10, 5, None, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == \
+    assert L.kv_compact(ctypes.byref(s), 10, 5, None, FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == \
         B.KV_ERR_INVALID_ARG
-    assert L.kv_compact(ctypes.byref(s), 10, 5, FAKE, FAKE + 8, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == \
+    assert L.kv_compact(ctypes.byref(s), 10, 5, FAKE, FAKE + 8, FAKE, FAKE, FAKE, None, FAKE, 1 << 30, None) == \
         B.KV_ERR_UNSUPPORTED
     # n <= B is a no-op that still validates the workspace
-    assert L.kv_compact(ctypes.byref(s), 10, 50, FAKE, FAKE, FAKE, FAKE, FAKE, None, 0, None) == B.KV_ERR_WORKSPACE
+    assert L.kv_compact(ctypes.byref(s), 10, 5, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE + 2, FAKE, 1 << 30, None) == \
+        B.KV_ERR_UNSUPPORTED                                      # misaligned norm cache
+    assert L.kv_compact(ctypes.byref(s), 10, 50, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == \
+        B.KV_ERR_WORKSPACE
 
 
 def _step(s, p, t=1, n_in=10, n_out=True, **kw):
-    args = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k=FAKE, v=FAKE, u=FAKE, pos=FAKE, ws=None, ws_bytes=0)
+    args = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k=FAKE, v=FAKE, u=FAKE, pos=FAKE, ws=None, ws_bytes=0, norms=None)
     args.update(kw)
     out = ctypes.c_int32(-7)
     rc = lib_().kv_evict_step(ctypes.byref(s), ctypes.byref(p) if p is not None else None, t, n_in, 5,
                               args["q"], args["k_new"], args["v_new"], args["k"], args["v"], args["u"], args["pos"],
-                              ctypes.byref(out) if n_out else None, None, None, None, args.get("rt"), args["ws"],
-                              args["ws_bytes"], None)
+                              args["norms"], ctypes.byref(out) if n_out else None, None, None, None, args.get("rt"),
+                              args["ws"], args["ws_bytes"], None)
     return rc, out.value
 
 
@@ -167,6 +170,7 @@ def test_step_validation(lib):
     assert _step(s, B.make_params(0.9, 20, score_merge=2))[0] == B.KV_ERR_WORKSPACE
     assert _step(s, good, v_new=None)[0] == B.KV_ERR_INVALID_ARG
     assert _step(s, good, k=FAKE + 2)[0] == B.KV_ERR_UNSUPPORTED
+    assert _step(s, good, norms=FAKE + 2)[0] == B.KV_ERR_UNSUPPORTED
     rc, out = _step(s, good)
     assert rc == B.KV_ERR_WORKSPACE and out == -7                      # nothing written on failure
 
@@ -176,9 +180,9 @@ def test_append_validation(lib):
     good = B.make_params(0.9, 20)
     L = lib_()
 
-    def call(p=good, t=1, n_in=10, new_pos=5, k_new=FAKE, k=FAKE, u=FAKE):
+    def call(p=good, t=1, n_in=10, new_pos=5, k_new=FAKE, k=FAKE, u=FAKE, norms=None):
         return L.kv_append(ctypes.byref(s), ctypes.byref(p) if p is not None else None, t, n_in, new_pos, k_new,
-                           FAKE, k, FAKE, u, FAKE, None)
+                           FAKE, k, FAKE, u, FAKE, norms, None)
     assert call(p=None) == B.KV_ERR_INVALID_ARG
     assert call(p=B.make_params(0.9, 0)) == B.KV_ERR_INVALID_ARG
     assert call(t=0) == B.KV_ERR_INVALID_ARG
@@ -187,6 +191,7 @@ def test_append_validation(lib):
     assert call(k_new=None) == B.KV_ERR_INVALID_ARG
     assert call(k=FAKE + 8) == B.KV_ERR_UNSUPPORTED
     assert call(u=FAKE + 2) == B.KV_ERR_UNSUPPORTED
+    assert call(norms=FAKE + 2) == B.KV_ERR_UNSUPPORTED
 
 
 def test_attend_validation(lib):
@@ -219,7 +224,8 @@ def test_finish_validation(lib):
 
     def call(p=good, t=1, n=10, k=FAKE, n_out=True, ws=None, ws_bytes=0):
         return L.kv_evict_finish(ctypes.byref(s), ctypes.byref(p) if p is not None else None, t, n, k, FAKE, FAKE,
-                                 FAKE, ctypes.byref(out) if n_out else None, None, None, None, ws, ws_bytes, None)
+                                 FAKE, None, ctypes.byref(out) if n_out else None, None, None, None, ws, ws_bytes,
+                                 None)
     assert call(p=None) == B.KV_ERR_INVALID_ARG
     assert call(t=0) == B.KV_ERR_INVALID_ARG
     assert call(n=0) == B.KV_ERR_INVALID_ARG
@@ -282,7 +288,7 @@ def test_static_step_rejects_what_its_scratch_cannot_hold(lib):
     out = ctypes.c_int32(-7)
 
     def call(s, p, t, n_in, new_pos):
-        return lib_().kv_evict_step_static(ctypes.byref(s), ctypes.byref(p), t, n_in, new_pos, *(FAKE,) * 7,
+        return lib_().kv_evict_step_static(ctypes.byref(s), ctypes.byref(p), t, n_in, new_pos, *(FAKE,) * 7, None,
                                            ctypes.byref(out), None, None, None, None, None)
     s = B.make_shape(8, 32, 32, 8, 128, 32769, "bf16")
     assert call(s, B.make_params(0.9, 3277), 1, 32768, 32768) == B.KV_ERR_UNSUPPORTED
@@ -291,3 +297,14 @@ def test_static_step_rejects_what_its_scratch_cannot_hold(lib):
     assert call(s, B.make_params(0.9, 3277), 0, 3277, 40000) == B.KV_ERR_INVALID_ARG   # argument checks as the step
     assert call(s, B.make_params(1.0, 3277), 2, 3277, 40000) == B.KV_ERR_INVALID_ARG
     assert out.value == -7
+
+
+def test_value_norms_validation(lib):
+    s = shape()
+    L = lib_()
+    assert L.kv_value_norms(ctypes.byref(s), 0, FAKE, FAKE, None) == B.KV_ERR_INVALID_ARG
+    assert L.kv_value_norms(ctypes.byref(s), 101, FAKE, FAKE, None) == B.KV_ERR_INVALID_ARG
+    assert L.kv_value_norms(ctypes.byref(s), 10, None, FAKE, None) == B.KV_ERR_INVALID_ARG
+    assert L.kv_value_norms(ctypes.byref(s), 10, FAKE, None, None) == B.KV_ERR_INVALID_ARG
+    assert L.kv_value_norms(ctypes.byref(s), 10, FAKE + 8, FAKE, None) == B.KV_ERR_UNSUPPORTED
+    assert L.kv_value_norms(ctypes.byref(s), 10, FAKE, FAKE + 1, None) == B.KV_ERR_UNSUPPORTED

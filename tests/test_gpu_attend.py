@@ -13,7 +13,7 @@ import pytest
 import torch
 
 from oracle import attention_output, evict_step, layer_scores, refresh_due, to_f64
-from parity import assert_close, assert_o, lockstep_adopter, oracle_cache, oracle_params, to_device
+from parity import assert_close, assert_o, check_norm_cache, lockstep_adopter, oracle_cache, oracle_params, to_device
 from workload import LLAMA8B, LLAMA8B_LAZY, QWEN, TINY, Workload, raw_numpy
 
 pytestmark = pytest.mark.gpu
@@ -32,7 +32,8 @@ def attend_layers(shape, cfg, n, q, k, v, pos, cur_pos, emit, ws, per_layer):
     return o
 
 
-def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False, emit_norms=False, merge=0):
+def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False, emit_norms=False, merge=0,
+                       norm_cache=False):
     w = Workload(cfg)
     cap = max(cfg.prefill_len, cfg.budget) + 1
     st = w.prefill(capacity=cap)
@@ -45,6 +46,10 @@ def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False, emit_n
     op = oracle_params(cfg, vnorm=vnorm, entropy=entropy)
     ws = B.workspace(shape, cap)
     n = st["n"]
+    norms = None
+    if norm_cache:
+        norms = torch.full((cfg.layers, cfg.batch, cfg.n_kv_heads, cap), -1.0, device="cuda")
+        B.kv_value_norms(shape, n, dev["v"], norms)
     flips = 0
     for t in range(1, steps + 1):
         si = w.step_inputs(t)
@@ -52,14 +57,14 @@ def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False, emit_n
         refresh = refresh_due(t, cfg.refresh_period, cfg.score_free)
         print(f"{cfg.name} t={t} refresh={refresh} per_layer={per_layer} n_in={n}", flush=True)
         B.kv_append(shape, params, t, n, si["new_pos"], sig["k_new"], sig["v_new"], dev["k"], dev["v"], dev["u"],
-                    dev["pos"])
+                    dev["pos"], v_norms=norms)
         emit = (B.KV_EMIT_SCORES | (B.KV_EMIT_VNORMS if emit_norms else 0)) if refresh else 0
         o = attend_layers(shape, cfg, n + 1, sig["q"], dev["k"], dev["v"], dev["pos"], si["new_pos"], emit, ws,
                           per_layer)
         keep = torch.zeros(cfg.batch, cap, dtype=torch.uint8, device="cuda")
         s_out = torch.full((cfg.layers, cfg.batch, n + 1), -1.0, device="cuda")
         n_out = B.kv_evict_finish(shape, params, t, n + 1, dev["k"], dev["v"], dev["u"], dev["pos"], ws,
-                                  keep_out=keep, s_out=s_out)
+                                  keep_out=keep, s_out=s_out, v_norms=norms)
         torch.cuda.synchronize()
         keep_g = keep.cpu().numpy()[:, : n + 1].astype(bool)
         step_flips = []
@@ -76,6 +81,8 @@ def run_fused_lockstep(cfg, steps, per_layer, vnorm=False, entropy=False, emit_n
         np.testing.assert_array_equal(dev["pos"][:, :n].cpu().numpy(), oc.pos[:, :n])
         np.testing.assert_array_equal(raw_numpy(dev["k"])[:, :, :, :n], oc.k[:, :, :, :n])
         np.testing.assert_array_equal(raw_numpy(dev["v"])[:, :, :, :n], oc.v[:, :, :, :n])
+        if norms is not None:
+            check_norm_cache(B, shape, dev["v"], norms, n, oc.v, cfg.dtype, f"{cfg.name} t={t}")
     return flips
 
 
@@ -106,6 +113,16 @@ def test_fused_step_scorer_variants(name, emit_norms):
     run_fused_lockstep(cfg, steps, per_layer=True, vnorm=True, entropy=True, emit_norms=emit_norms)
     if emit_norms:
         run_fused_lockstep(cfg, 2, per_layer=False, vnorm=True, entropy=False, emit_norms=True)
+
+
+@pytest.mark.parametrize("per_layer", [True, False], ids=["per_layer", "all_layers"])
+@pytest.mark.parametrize("name", ["tiny", "llama8b_reduced", "llama8b_split_step1", "lazy_r4_min", "qwen_reduced"])
+def test_fused_step_value_norm_cache(name, per_layer):
+    """VNorm + entropy on the fused path with the value-norm cache: kv_append caches the newcomer's norm, the
+    finish reads the cached norms (neither the attention nor the finish reads V for them) and keeps the cache
+    through the placement and the compaction."""
+    cfg, steps = CASES[name]
+    run_fused_lockstep(cfg, steps, per_layer, vnorm=True, entropy=True, norm_cache=True)
 
 
 @pytest.mark.parametrize("name,merge", [("llama8b_reduced", 4), ("llama8b_split_step1", 8), ("qwen_reduced", 2)])

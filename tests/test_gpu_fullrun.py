@@ -19,7 +19,7 @@ import pytest
 import torch
 
 from oracle import Cache, evict_step
-from parity import assert_close, lockstep_adopter, oracle_params
+from parity import assert_close, check_norm_cache, lockstep_adopter, oracle_params
 from workload import LLAMA8B, QWEN, SCOREFREE128K, Workload, raw_numpy
 
 pytestmark = pytest.mark.gpu
@@ -45,18 +45,21 @@ class Run:
                                   cfg.capacity, cfg.dtype)
         self.ws = B.workspace(self.shape, cfg.capacity)
         self.flips = 0
+        self.norms = None   # VNorm's value-norm cache, when a run keeps one
 
     def step(self, t, sched, tag):
         cfg, st = self.cfg, self.st
+        variants = {k: sched.get(k, False) for k in ("vnorm", "entropy")}
         params = B.make_params(cfg.alpha, cfg.budget, sched["refresh_period"], sched["score_free"],
-                               sched["nonrefresh_init"], cfg.recency_bias, cfg.recency_window)
+                               sched["nonrefresh_init"], cfg.recency_bias, cfg.recency_window, **variants)
         op = oracle_params(cfg, **{k: v for k, v in sched.items() if k != "last"})
         si = self.w.step_inputs(t)
         n = st["n"]
         keep = torch.zeros(cfg.batch, cfg.capacity, dtype=torch.uint8, device="cuda")
         s_out = torch.empty((cfg.layers, cfg.batch, n + 1), device="cuda")
         n_out = B.kv_evict_step(self.shape, params, t, n, si["new_pos"], si["q"], si["k_new"], si["v_new"],
-                                st["k"], st["v"], st["u"], st["pos"], self.ws, keep_out=keep, s_out=s_out)
+                                st["k"], st["v"], st["u"], st["pos"], self.ws, keep_out=keep, s_out=s_out,
+                                v_norms=self.norms)
         torch.cuda.synchronize()
         assert n_out == min(cfg.budget, n + 1)
         full = t == 1 or t % self.full_every == 0 or t == sched["last"]
@@ -90,6 +93,10 @@ class Run:
                     got = raw_numpy(st[name][:, b].index_select(2, rows_t))
                 want = getattr(oc, name)[:, 0][:, :, rows]
                 assert np.array_equal(got, want), f"{what}: {name} rows differ ({'all' if full else rows[:8]})"
+        if self.norms is not None and full:
+            for b in self.samples:
+                check_norm_cache(B, self.shape, st["v"], self.norms, n_out, None, cfg.dtype, f"{tag} t={t} seq {b}",
+                                 b=b, v_ref_seq=self.oc[b].v[:, 0])
         st["n"] = n_out
         if t == 1 or t % 16 == 0 or t == sched["last"]:
             print(f"{tag} t={t} ok, n={n_out}, in-band flips so far {self.flips}", flush=True)
@@ -152,6 +159,26 @@ def test_llama8b_32k_all_64_steps(llama_after_step1, period, init):
     sched = _sched(cfg, cfg.steps, refresh_period=period, nonrefresh_init=init, score_free=False)
     for t in range(2, cfg.steps + 1):
         run.step(t, sched, f"8B R={period} {init}")
+
+
+def test_llama8b_32k_vnorm_from_the_norm_cache(llama_after_step1):
+    """VNorm + entropy steps at the 8B / 32k shape with the value-norm cache filled once (kv_value_norms) after
+    the shared step 1: 16 full-refresh steps (the steady step's three kernels plus the norms' mean), then 16
+    Lazy R = 4 steps under the mean prior; the cache itself is checked at every full comparison."""
+    run, snap = llama_after_step1
+    run.restore(snap)
+    cfg = run.cfg
+    run.norms = torch.full((cfg.layers, cfg.batch, cfg.n_kv_heads, cfg.capacity), -1.0, device="cuda")
+    try:
+        B.kv_value_norms(run.shape, run.st["n"], run.st["v"], run.norms)
+        full = _sched(cfg, 33, refresh_period=1, nonrefresh_init="mean", score_free=False, vnorm=True, entropy=True)
+        lazy = _sched(cfg, 33, refresh_period=4, nonrefresh_init="mean", score_free=False, vnorm=True, entropy=True)
+        for t in range(2, 18):
+            run.step(t, full, "8B VNorm norm cache R=1")
+        for t in range(18, 34):
+            run.step(t, lazy, "8B VNorm norm cache R=4 mean")
+    finally:
+        run.norms = None
 
 
 @pytest.fixture(scope="module")

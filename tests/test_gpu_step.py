@@ -10,7 +10,7 @@ import pytest
 import torch
 
 from oracle import evict_step
-from parity import assert_close, lockstep_adopter, oracle_cache, oracle_params, to_device
+from parity import assert_close, check_norm_cache, lockstep_adopter, oracle_cache, oracle_params, to_device
 from workload import LLAMA8B, LLAMA8B_LAZY, QWEN, SCOREFREE128K, TINY, Workload, raw_numpy
 
 pytestmark = pytest.mark.gpu
@@ -18,7 +18,7 @@ pytestmark = pytest.mark.gpu
 B = pytest.importorskip("paper_2609_03515_amd.binding")
 
 
-def run_lockstep(cfg, steps, seed=None, rule="ema", vnorm=False, entropy=False, merge=0):
+def run_lockstep(cfg, steps, seed=None, rule="ema", vnorm=False, entropy=False, merge=0, norm_cache=False):
     w = Workload(cfg, seed=seed)
     cap = max(cfg.prefill_len, cfg.budget) + 1          # room for the cache to grow up to B + 1
     st = w.prefill(capacity=cap)
@@ -31,6 +31,11 @@ def run_lockstep(cfg, steps, seed=None, rule="ema", vnorm=False, entropy=False, 
     op = oracle_params(cfg, rule=rule, vnorm=vnorm, entropy=entropy)
     ws = B.workspace(shape, cap)
     n = st["n"]
+    norms = None
+    if norm_cache:   # VNorm's value-norm cache, filled once from the prefill, then kept by the steps
+        norms = torch.full((cfg.layers, cfg.batch, cfg.n_kv_heads, cap), -1.0, device="cuda")
+        if n > 0:
+            B.kv_value_norms(shape, n, dev["v"], norms)
     flips = 0
     for t in range(1, steps + 1):
         si = w.step_inputs(t)
@@ -38,7 +43,8 @@ def run_lockstep(cfg, steps, seed=None, rule="ema", vnorm=False, entropy=False, 
         keep = torch.zeros(cfg.batch, cap, dtype=torch.uint8, device="cuda")
         s_out = torch.full((cfg.layers, cfg.batch, n + 1), -1.0, device="cuda")
         n_out = B.kv_evict_step(shape, params, t, n, si["new_pos"], sig["q"], sig["k_new"], sig["v_new"],
-                                dev["k"], dev["v"], dev["u"], dev["pos"], ws, keep_out=keep, s_out=s_out)
+                                dev["k"], dev["v"], dev["u"], dev["pos"], ws, keep_out=keep, s_out=s_out,
+                                v_norms=norms)
         torch.cuda.synchronize()
         q_raw, kn_raw, vn_raw = raw_numpy(si["q"]), raw_numpy(si["k_new"]), raw_numpy(si["v_new"])
         keep_g = keep.cpu().numpy()[:, : n + 1].astype(bool)
@@ -54,6 +60,8 @@ def run_lockstep(cfg, steps, seed=None, rule="ema", vnorm=False, entropy=False, 
         np.testing.assert_array_equal(dev["pos"][:, :n].cpu().numpy(), oc.pos[:, :n])
         np.testing.assert_array_equal(raw_numpy(dev["k"])[:, :, :, :n], oc.k[:, :, :, :n])
         np.testing.assert_array_equal(raw_numpy(dev["v"])[:, :, :, :n], oc.v[:, :, :, :n])
+        if norms is not None:
+            check_norm_cache(B, shape, dev["v"], norms, n, oc.v, cfg.dtype, f"{cfg.name} t={t}")
         print(f"{cfg.name} t={t} refresh={ref.refreshed} n={n} in-band flips so far={flips}", flush=True)
     return flips
 
@@ -112,6 +120,33 @@ def test_scorer_variants_lockstep(name, vnorm, entropy):
     """Sec. 5.1 scorer perturbations through kv_evict_step, in lockstep with the oracle."""
     cfg, steps = VARIANT_CASES[name]
     run_lockstep(cfg, steps, vnorm=vnorm, entropy=entropy)
+
+
+NORM_CACHE_CASES = {
+    "tiny": (TINY, 6),
+    "llama8b_reduced": (LLAMA8B.scaled(batch=2, layers=3, prefill_len=1200, budget=120), 5),
+    "llama8b_split_step1": (LLAMA8B.scaled(batch=1, layers=2, prefill_len=6000, budget=600), 3),
+    "qwen_reduced": (QWEN.scaled(batch=2, layers=2, prefill_len=1000, budget=250), 4),
+    "lazy_r4_min": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=800, budget=80), 9),
+    "lazy_r4_mean": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=800, budget=80, nonrefresh_init="mean"), 9),
+    "scorefree_mean": (SCOREFREE128K.scaled(batch=2, layers=2, prefill_len=3000, budget=300,
+                                            nonrefresh_init="mean"), 8),
+    "lazy_under_budget": (LLAMA8B_LAZY.scaled(batch=2, layers=2, prefill_len=40, budget=44, nonrefresh_init="mean"), 9),
+    "empty_start": (TINY.scaled(prefill_len=0, budget=3), 6),
+}
+
+
+@pytest.mark.parametrize("vnorm,entropy", [(True, False), (True, True), (False, False)],
+                         ids=["vnorm", "vnorm_entropy", "plain"])
+@pytest.mark.parametrize("name", list(NORM_CACHE_CASES))
+def test_value_norm_cache_lockstep(name, vnorm, entropy):
+    """VNorm from the value-norm cache (Sec. 5.1; a value row's norm is computed once, when it is cached):
+    kv_evict_step in lockstep with the oracle, the cache checked after every step (every append, placement
+    and compaction keeps each norm beside its row), on steady steps (three kernels plus the norms' mean),
+    first steps, non-refresh steps under both priors and caches under budget; "plain" keeps the cache without
+    VNorm."""
+    cfg, steps = NORM_CACHE_CASES[name]
+    run_lockstep(cfg, steps, vnorm=vnorm, entropy=entropy, norm_cache=True)
 
 
 @pytest.mark.parametrize("init", ["min", "mean"])

@@ -24,11 +24,14 @@ def _copy(st):
     return {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in st.items()}
 
 
-def _compare(cfg, w, st, t, params, what):
+def _compare(cfg, w, st, t, params, what, norm_cache=False):
     cap = st["k"].shape[3]
     shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
     si = w.step_inputs(t)
     n_in = st["n"]
+    if norm_cache:   # the value-norm cache, filled from the cached rows, is part of the state both sides keep
+        st = dict(st, norms=torch.full((cfg.layers, cfg.batch, cfg.n_kv_heads, cap), -1.0, device="cuda"))
+        B.kv_value_norms(shape, n_in, st["v"], st["norms"])
     a, b = _copy(st), _copy(st)
     outs = []
     for side, fn in (("workspace", B.kv_evict_step), ("static", B.kv_evict_step_static)):
@@ -38,9 +41,9 @@ def _compare(cfg, w, st, t, params, what):
         args = (shape, params, t, n_in, si["new_pos"], si["q"], si["k_new"], si["v_new"], d["k"], d["v"], d["u"],
                 d["pos"])
         if side == "workspace":
-            n_out = fn(*args, B.workspace(shape, n_in + 1), keep_out=keep, s_out=s_out)
+            n_out = fn(*args, B.workspace(shape, n_in + 1), keep_out=keep, s_out=s_out, v_norms=d.get("norms"))
         else:
-            n_out = fn(*args, keep_out=keep, s_out=s_out)
+            n_out = fn(*args, keep_out=keep, s_out=s_out, v_norms=d.get("norms"))
         torch.cuda.synchronize()
         outs.append((n_out, keep, s_out))
     assert outs[0][0] == outs[1][0] == min(params.budget, n_in + 1), what
@@ -51,6 +54,8 @@ def _compare(cfg, w, st, t, params, what):
     assert torch.equal(a["pos"][:, :n_out], b["pos"][:, :n_out]), f"{what}: positions"
     assert torch.equal(a["k"][:, :, :, :n_out], b["k"][:, :, :, :n_out]), f"{what}: keys"
     assert torch.equal(a["v"][:, :, :, :n_out], b["v"][:, :, :, :n_out]), f"{what}: values"
+    if norm_cache:
+        assert torch.equal(a["norms"][..., :n_out], b["norms"][..., :n_out]), f"{what}: value norms"
 
 
 def test_static_scratch_matches_workspace_variant_on_two_calls():
@@ -81,6 +86,8 @@ def test_static_scratch_other_step_kinds():
                        entropy=True)
     print("no-alloc: VNorm + entropy refresh step", flush=True)
     _compare(cfg, w, st, 2, vn, "VNorm + entropy step")
+    print("no-alloc: VNorm + entropy refresh step from the value-norm cache", flush=True)
+    _compare(cfg, w, st, 2, vn, "VNorm step, norm cache", norm_cache=True)
     cfg = TINY
     w = Workload(cfg, device="cuda")
     st = w.prefill()
