@@ -10,9 +10,11 @@ scoring, fold, selection and compaction, with every input already resident in HB
 Prints one JSON line: evict-steps/s, the roofline of the dominant kernel (scoring; algorithmic bytes over its
 event-timed duration), Lazy R = 4 / R = 8 step rates on the same trajectory under both new-token priors, whole
 64-step runs (full refresh, Lazy R = 4 / R = 8 under both priors) from the same prefill, and the float64 CPU
-oracle timed on bounded samples of each step type (first step, steady refresh step, non-refresh step).  The events around every timed scoring launch are timing-only
-(hipEventDisableSystemFence): a default event writes back and invalidates the caches when it is recorded, which
-slowed each step by ~5 us (against ~1.4 us), and their readings are taken after the stream is synchronized.
+oracle timed on bounded samples of each step type (first step, steady refresh step, non-refresh step).  The
+throughput comes from blocks of steps with events only around the block; the score kernel's launch durations
+(the roofline) from a further block with timing-only events (hipEventDisableSystemFence) around every scoring
+launch, read after the stream is synchronized: events between a step's kernels lengthen the step, so that block
+is reported apart (`instrumented_steps`).
 """
 from __future__ import annotations
 
@@ -279,17 +281,21 @@ def secondary_workloads(B, dev, K, W):
     cfg = QWEN
     w, st, shape, params, ws = setup(cfg)
     kq = min(K, 100)
-    w_inputs = {t: w.step_inputs(t) for t in range(1, 2 + W + kq)}
+    w_inputs = {t: w.step_inputs(t) for t in range(1, 2 + W + 2 * kq)}
     first = timed_first_step(cfg, w, st, shape, params, ws)
     for t in range(2, 2 + W):
         run(w, st, shape, params, ws, t)
-    pairs = [(B.HipEvent(True), B.HipEvent(True)) for _ in range(kq)]
     torch.cuda.synchronize()
     h0 = time.perf_counter()
-    for i, t in enumerate(range(2 + W, 2 + W + kq)):
-        run(w, st, shape, params, ws, t, trace=B.make_trace({"score": pairs[i]}))
+    for t in range(2 + W, 2 + W + kq):
+        run(w, st, shape, params, ws, t)
     torch.cuda.synchronize()
     host_s = time.perf_counter() - h0
+    # a further block with events around every scoring launch: the score kernel's durations
+    pairs = [(B.HipEvent(True), B.HipEvent(True)) for _ in range(kq)]
+    for i, t in enumerate(range(2 + W + kq, 2 + W + 2 * kq)):
+        run(w, st, shape, params, ws, t, trace=B.make_trace({"score": pairs[i]}))
+    torch.cuda.synchronize()
     score_ms = sum(p[0].elapsed_ms(p[1]) for p in pairs) / kq
     by = step_bytes(cfg, cfg.budget + 1, B.kv_score_merge(shape, cfg.budget + 1, params))
     out["qwen_8k"] = {"config": {"batch": cfg.batch, "layers": cfg.layers, "n_q_heads": cfg.n_q_heads,
@@ -472,7 +478,7 @@ def main():
     ws = B.workspace(shape, cap, device=dev)
     K, W = args.steps, args.warmup
     KF = min(K, 50)   # steps per configuration of the extra measurements (fused attention, variants, trace)
-    total = max(64, 1 + W + 9 * K + 16 * KF)   # step 1, warmup, the timed schedules, the extra rows (15 x KF)
+    total = 64 + W + 10 * K + 16 * KF  # the 64-step runs, warmup, the timed schedules, the extra rows (15 x KF)
     inputs = [w.step_inputs(t) for t in range(1, total + 1)]
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
@@ -488,14 +494,6 @@ def main():
 
     k, v, u, pos = st["k"], st["v"], st["u"], st["pos"]
     n0 = st["n"]
-    # the oracle's first-step sample: sequence 0 of this prefill and its step-1 inputs, as stored bits
-    first_cpu = None
-    if not args.no_cpu:
-        si = inputs[0]
-        first_cpu = {"cache": (raw_numpy(k[:, 0:1]), raw_numpy(v[:, 0:1]),
-                               u[0:1].cpu().numpy().astype("float64"), pos[0:1].cpu().numpy().astype("int64")),
-                     "inputs": (raw_numpy(si["q"][:, 0:1]), raw_numpy(si["k_new"][:, 0:1]),
-                                raw_numpy(si["v_new"][:, 0:1]), si["new_pos"])}
     prefill = [x.clone() for x in (k, v, u, pos)]   # restored before each whole 64-step run
     state = {"n": n0, "t": 0}
 
@@ -527,58 +525,13 @@ def main():
     step1_ms = e0.elapsed_ms(e1)
     step1 = first_step_record(B, cfg, shape, full, n0 + 1, keep1, step1_ms)
     step1["cold_ms"] = round(step1_cold_ms, 3)
-    for _ in range(W):
-        step(full)
-
-    def timed(params):
-        pairs = [(B.HipEvent(True), B.HipEvent(True)) for _ in range(K)]
-        traces = [B.make_trace({"score": p}) for p in pairs]
-        t_first = state["t"] + 1
-        refreshed = [(t - 1) % params.refresh_period == 0 for t in range(t_first, t_first + K)]
-        torch.cuda.synchronize()
-        a, z = B.HipEvent(), B.HipEvent()
-        h0 = time.perf_counter()
-        a.record()
-        for i in range(K):
-            step(params, traces[i])
-        z.record()
-        torch.cuda.synchronize()
-        host_s = time.perf_counter() - h0
-        dev_ms = a.elapsed_ms(z)
-        # non-refresh steps launch no scoring kernel and leave their events unrecorded
-        score = [p[0].elapsed_ms(p[1]) for p, r in zip(pairs, refreshed) if r]
-        return host_s, dev_ms, score
-
-    host_s, dev_ms, score_ms = timed(full)
-    assert state["n"] == cfg.budget
-    steps_per_s = K / host_s
-    ms_per_step = 1e3 * host_s / K
-    lazy_s = {key: timed(p) for key, p in lazy.items()}
-
-    def graphed(params):
-        """K steps captured into one HIP graph (torch.cuda.CUDAGraph on the library's stream) and replayed
-        once: the device-bound rate, without the per-call host cost that dominates non-refresh steps."""
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):  # records the launches of steps t+1 .. t+K; the replay performs them
-            for _ in range(K):
-                step(params)
-        torch.cuda.synchronize()
-        a, z = B.HipEvent(), B.HipEvent()
-        a.record()
-        g.replay()
-        z.record()
-        torch.cuda.synchronize()
-        return a.elapsed_ms(z) / K
-
-    lazy_graph_ms = {key: graphed(p) for key, p in lazy.items()}
-
-    extra = extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, ms_per_step)
-
     n = cfg.budget + 1
     merge = B.kv_score_merge(shape, n, full)
     by = step_bytes(cfg, n, merge)
 
-    # whole 64-step runs from the same prefill (step 1 + 63 steps; inputs of steps 1..64), each timed end to end
+    # whole 64-step runs from the same prefill (step 1 + 63 steps; inputs of steps 1..64), each timed end to
+    # end.  They run first: sustained work before the headline's warmup and timed block (a GPU left idle before
+    # a short timed block runs it below its sustained clocks).
     def run64(params, steps=64):
         for dst, src in zip((k, v, u, pos), prefill):
             dst.copy_(src)
@@ -610,6 +563,69 @@ def main():
         runs[f"lazy_r{R}_{init}"] = run64(p)
     runs["lazy_r4_mean_speedup_vs_full"] = round(runs["lazy_r4_mean"]["steps_per_s"] /
                                                  runs["full_refresh"]["steps_per_s"], 3)
+
+    # the headline: W warmup steps continuing the last run (a steady cache of B tokens), then K timed steps
+    for _ in range(W):
+        step(full)
+
+    def timed(params, score_events=False):
+        """K consecutive steps, host clock and events around the block.  score_events: also a pair of timing
+        events around every step's scoring launch (the score kernel's per-launch durations for the roofline),
+        taken in a block of their own."""
+        pairs = [(B.HipEvent(True), B.HipEvent(True)) for _ in range(K)] if score_events else []
+        traces = [B.make_trace({"score": p}) for p in pairs] if score_events else [None] * K
+        t_first = state["t"] + 1
+        refreshed = [(t - 1) % params.refresh_period == 0 for t in range(t_first, t_first + K)]
+        torch.cuda.synchronize()
+        a, z = B.HipEvent(), B.HipEvent()
+        h0 = time.perf_counter()
+        a.record()
+        for i in range(K):
+            step(params, traces[i])
+        z.record()
+        torch.cuda.synchronize()
+        host_s = time.perf_counter() - h0
+        dev_ms = a.elapsed_ms(z)
+        # non-refresh steps launch no scoring kernel and leave their events unrecorded
+        score = [p[0].elapsed_ms(p[1]) for p, r in zip(pairs, refreshed) if r]
+        return host_s, dev_ms, score, sum(refreshed)
+
+    host_s, dev_ms, _, _ = timed(full)
+    assert state["n"] == cfg.budget
+    steps_per_s = K / host_s
+    ms_per_step = 1e3 * host_s / K
+    ev_host_s, ev_dev_ms, score_ms, _ = timed(full, score_events=True)   # the roofline's launch durations
+    lazy_s = {key: timed(p) for key, p in lazy.items()}
+
+    def graphed(params):
+        """K steps captured into one HIP graph (torch.cuda.CUDAGraph on the library's stream) and replayed
+        once: the device-bound rate, without the per-call host cost that dominates non-refresh steps."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):  # records the launches of steps t+1 .. t+K; the replay performs them
+            for _ in range(K):
+                step(params)
+        torch.cuda.synchronize()
+        a, z = B.HipEvent(), B.HipEvent()
+        a.record()
+        g.replay()
+        z.record()
+        torch.cuda.synchronize()
+        return a.elapsed_ms(z) / K
+
+    lazy_graph_ms = {key: graphed(p) for key, p in lazy.items()}
+
+    extra = extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, ms_per_step)
+
+    # the oracle's first-step sample: sequence 0 of the prefill and its step-1 inputs, as stored bits (copied
+    # to the host only now, after the GPU measurements)
+    first_cpu = None
+    if not args.no_cpu:
+        si = inputs[0]
+        first_cpu = {"cache": (raw_numpy(prefill[0][:, 0:1]), raw_numpy(prefill[1][:, 0:1]),
+                               prefill[2][0:1].cpu().numpy().astype("float64"),
+                               prefill[3][0:1].cpu().numpy().astype("int64")),
+                     "inputs": (raw_numpy(si["q"][:, 0:1]), raw_numpy(si["k_new"][:, 0:1]),
+                                raw_numpy(si["v_new"][:, 0:1]), si["new_pos"])}
     del st, k, v, u, pos, ws, inputs, prefill
     torch.cuda.empty_cache()
     other = secondary_workloads(B, dev, K, W) if not args.no_secondary else {}
@@ -619,10 +635,10 @@ def main():
     step_gbps = by["total"] * steps_per_s / 1e9
 
     def lazy_entry(R, init):
-        hs, _, sc = lazy_s[(R, init)]
+        hs, _, _, nref = lazy_s[(R, init)]
         g = lazy_graph_ms[(R, init)]
         return {"value": round(K / hs, 2), "unit": "evict-steps/s", "ms_per_step": round(1e3 * hs / K, 4),
-                "refresh_steps": len(sc), "speedup_vs_full": round((K / hs) / steps_per_s, 3),
+                "refresh_steps": nref, "speedup_vs_full": round((K / hs) / steps_per_s, 3),
                 "graph_ms_per_step": round(g, 4), "graph_steps_per_s": round(1e3 / g, 1)}
 
     out = {
@@ -646,6 +662,10 @@ def main():
         "pct_peak": round(100 * step_gbps / PEAK_HBM_GBPS, 2),
         "step_bytes": by,
         "device_ms_per_step": round(dev_ms / K, 4),
+        "instrumented_steps": {"what": "K further steps with timing events around every scoring launch (the "
+                                       "roofline's launch durations come from these)",
+                               "ms_per_step": round(1e3 * ev_host_s / K, 4),
+                               "device_ms_per_step": round(ev_dev_ms / K, 4)},
         "roofline": {"kernel": f"score_kernel<bf16, d128, group 4, LDS-resident, {merge} KV heads per workgroup>",
                      "bound": "hbm",
                      "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",

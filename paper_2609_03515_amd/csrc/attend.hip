@@ -148,9 +148,12 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     using KP = KUnit<T, D, GP>;
     constexpr int kNbufK = use_mfma<T, D, GP>() ? 2 : kNbuf;  // K units in flight (16 rows each on MFMA)
 
+    // the waves' partial outputs are added in one step when every wave's slice fits 16 KiB of LDS (GP * D <= 512
+    // floats: groups up to 4 at d = 128), else wave by wave (one barrier each); the sums are the same
+    constexpr bool kWaveSlices = kWaves * GP * D <= 4096;
     extern __shared__ float zs[];
     __shared__ float red_m[kWaves][GP], red_s[kWaves][GP], red_n[kWaves];
-    __shared__ float obuf[kV ? GP * D : 1];
+    __shared__ float obuf[kV ? (kWaveSlices ? kWaves : 1) * GP * D : 1];
     __shared__ int next_unit[2];
 
     const L ln;
@@ -347,19 +350,40 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
             for (int c = 0; c < CPL; ++c)
 #pragma unroll
                 for (int x = 0; x < EPC; ++x) acc[h][c][x] += __shfl_xor(acc[h][c][x], o, kWave);
-    for (int w = 0; w < kWaves; ++w) {
-        if (ln.wave == w && ln.lane < LPR) {
+    if constexpr (kWaveSlices) {
+        // each wave's partial in its own slice; then output idx = ((w0 + w1) + w2) + ... by the thread that later
+        // stores it (the same thread-to-output mapping as the stores below, so no barrier between)
+        if (ln.lane < LPR) {
 #pragma unroll
             for (int h = 0; h < GP; ++h)
 #pragma unroll
                 for (int c = 0; c < CPL; ++c)
 #pragma unroll
-                    for (int x = 0; x < EPC; ++x) {
-                        const int idx = h * D + (ln.p + c * LPR) * EPC + x;
-                        obuf[idx] = w == 0 ? acc[h][c][x] : obuf[idx] + acc[h][c][x];
-                    }
+                    for (int x = 0; x < EPC; ++x)
+                        obuf[ln.wave * GP * D + h * D + (ln.p + c * LPR) * EPC + x] = acc[h][c][x];
         }
         __syncthreads();
+        for (int idx = threadIdx.x; idx < a.group * D; idx += kThreads) {
+            float t = obuf[idx];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) t += obuf[w * GP * D + idx];
+            obuf[idx] = t;
+        }
+    } else {
+        for (int w = 0; w < kWaves; ++w) {
+            if (ln.wave == w && ln.lane < LPR) {
+#pragma unroll
+                for (int h = 0; h < GP; ++h)
+#pragma unroll
+                    for (int c = 0; c < CPL; ++c)
+#pragma unroll
+                        for (int x = 0; x < EPC; ++x) {
+                            const int idx = h * D + (ln.p + c * LPR) * EPC + x;
+                            obuf[idx] = w == 0 ? acc[h][c][x] : obuf[idx] + acc[h][c][x];
+                        }
+            }
+            __syncthreads();
+        }
     }
     auto head_sum = [&](int h) {
         float t = red_s[0][h];
