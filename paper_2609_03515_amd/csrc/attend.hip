@@ -235,12 +235,12 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
     constexpr int kStep = kWaves * kWave;
     const int mine = nunits > ln.wave ? (nunits - ln.wave + kWaves - 1) / kWaves : 0;
     const bool write_z = a.emit && a.nchunk > 1;
-    const __amdgpu_buffer_rsrc_t zrs =
-        raw_rsrc(a.z + ((size_t)lb * a.hq + (size_t)g * a.group + ln.hh) * a.n_stride + row0, nrows * 4);
+    // this lane's head's logit row (lanes of one wave hold different heads: stored by address)
+    float* zrow = a.z + ((size_t)lb * a.hq + (size_t)g * a.group + ln.hh) * a.n_stride + row0;
     float ssum = 0.0f;
     auto expo = [&](float z, int unit) {
         // -inf: padded head or row past the end
-        if (write_z && z != -INFINITY) store_stream(zrs, ln.unit_row(unit) * 4, z);
+        if (write_z && z != -INFINITY) store_stream_at(zrow + ln.unit_row(unit), z);
         return z == -INFINITY ? 0.0f : __expf(z - m);
     };
     int i = 0;

@@ -52,9 +52,17 @@ inline hipError_t raise_lds_limit(const void* kern, std::atomic<bool> (&done)[kM
     return e;
 }
 
-// Raw buffer resource over `bytes` bytes at `base` (reads at offsets >= bytes return zero).
+// Raw buffer resource over `bytes` bytes at `base` (reads at offsets >= bytes return zero).  A resource is
+// wave-uniform: base and size are taken from the wave's first active lane, so every caller passes the same
+// values in all lanes (per-lane differences go into the offsets).  Without the explicit broadcast a value the
+// compiler happens to compute in vector registers (e.g. a size derived from a uniform boolean) makes it wrap
+// every buffer access in a loop over the distinct resources of the wave.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* base, int bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kRsrcConfig);
+    const uint64_t p = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+    void* b = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(b, (short)0, __builtin_amdgcn_readfirstlane(bytes), kRsrcConfig);
 }
 
 // 16- and 4-byte stores at byte offset `off` of a raw buffer resource, with the streaming-result cache policy.
@@ -63,6 +71,12 @@ __device__ __forceinline__ void store_stream(__amdgpu_buffer_rsrc_t rs, int off,
 }
 __device__ __forceinline__ void store_stream(__amdgpu_buffer_rsrc_t rs, int off, float v) {
     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rs, off, 0, kStoreStream);
+}
+// The same 4-byte store by address, for destinations that differ between the lanes of a wave (a resource must
+// be wave-uniform): a relaxed device-scope store, which carries the same device-scope cache policy.
+__device__ __forceinline__ void store_stream_at(float* p, float v) {
+    __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __builtin_bit_cast(uint32_t, v), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <typename T, int D, int GP>
