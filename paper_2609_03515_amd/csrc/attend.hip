@@ -52,15 +52,26 @@ __device__ __forceinline__ void read_probs(const float* src, float (&e)[GP]) {
     }
 }
 
-// Several chunks per slab: one workgroup per slab combines them after the chunks' launch.
-//   o_h = sum_c exp(m_c - M_h) o_c / sum_c exp(m_c - M_h) S_c,  M_h = max_c m_c;
-//   r(row) = sum_{h in group} exp(z_h(row) - M_h) / S_h from the logits the chunks wrote (when emitting).
-// (Electing the last chunk inside the attention kernel instead needs a device-scope release/acquire fence in
-// every chunk, which lowers to a full L2 write-back and invalidate: measured 5x slower per layer.)
+// Several chunks per slab: a combine kernel after the chunks' launch, combine_parts(n) workgroups per slab:
+//   o_h = sum_c exp(m_c - M_h) o_c / sum_c exp(m_c - M_h) S_c,  M_h = max_c m_c   (part 0);
+//   r(row) = sum_{h in group} exp(z_h(row) - M_h) / S_h from the logits the chunks wrote, when emitting (part p:
+//   rows [p kCombineRows, (p + 1) kCombineRows)).
+// The rows are spread over several workgroups because one per slab left the score's rows (52 KB of logits per
+// slab at the 8B shape) to 64 workgroups at one decoder layer's batch.
+// Electing the last chunk of a slab inside the attention kernel instead was measured twice at the 8B shape:
+// with a device-scope release/acquire fence in every chunk (a full L2 write-back and invalidate) 5x slower per
+// layer; with the partials written and read back by device-scope (write-through) accesses and a completion
+// wait before the arrival count, no faster without the score (the chunk's store, count and reload round trips
+// cost what the kernel boundary does) and 9% slower with it (one workgroup per slab takes the score's rows).
+constexpr int kCombineRows = 1024;
+__host__ __device__ constexpr int combine_parts(int n, bool emit) { return emit ? (n + kCombineRows - 1) / kCombineRows : 1; }
+
 template <typename T, int D, int GP>
 __global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
     __shared__ float cm[GP], ci[GP];
-    const int s = blockIdx.x;  // slab: (l * batch + b) * hkv + g, l relative to the call
+    const int parts = combine_parts(a.n, a.emit);
+    const int s = blockIdx.x / parts;  // slab: (l * batch + b) * hkv + g, l relative to the call
+    const int part = blockIdx.x % parts;
     const size_t head0 = (size_t)(s / a.hkv) * a.hq + (size_t)(s % a.hkv) * a.group;
     // The loops over chunks load four chunks' values before using them (the loads are independent; the
     // arithmetic keeps the sequential order, so the result does not depend on the unrolling).
@@ -89,14 +100,14 @@ __global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
         cm[threadIdx.x] = mx;
         ci[threadIdx.x] = tot > 0.0f ? 1.0f / tot : 0.0f;
     }
-    if (a.emit_norms && threadIdx.x == kWave) {  // (another wave than the one filling cm / ci)
+    if (a.emit_norms && part == 0 && threadIdx.x == kWave) {  // (another wave than the one filling cm / ci)
         float tot = 0.0f;
         for (int c = 0; c < a.nchunk; ++c) tot += a.npart[(size_t)s * a.nchunk + c];
         a.vinv[s] = tot > 0.0f ? (float)a.n / tot : 0.0f;
     }
     __syncthreads();
     T* ob = static_cast<T*>(a.o) + head0 * D;
-    for (int idx = threadIdx.x; idx < a.group * D; idx += kThreads) {
+    for (int idx = threadIdx.x; part == 0 && idx < a.group * D; idx += kThreads) {
         const int h = idx / D;
         const float2* pp = a.part + (head0 + h) * a.nchunk;
         const float* op = a.opart + (head0 + h) * a.nchunk * D + idx % D;
@@ -119,7 +130,8 @@ __global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
         // rows are padded to a multiple of 64: 4 rows per thread and pass, rows >= n are scratch
         const float* zb = a.z + head0 * a.n_stride;
         float* rb = a.r + (size_t)s * a.n_stride;
-        for (int row = threadIdx.x * 4; row < a.n; row += kThreads * 4) {
+        const int row_end = min(a.n, (part + 1) * kCombineRows);
+        for (int row = part * kCombineRows + threadIdx.x * 4; row < row_end; row += kThreads * 4) {
             f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
             for (int h = 0; h < a.group; ++h) {
                 const f32x4 z = *reinterpret_cast<const f32x4*>(zb + (size_t)h * a.n_stride + row);
@@ -458,8 +470,8 @@ hipError_t launch_attend_gp(const ScorePlan& plan, const ScoreArgs& a, hipStream
         if (plan.split) {
             hipError_t e = hipGetLastError();
             if (e != hipSuccess) return e;
-            hipLaunchKernelGGL((attend_combine_kernel<T, D, GP>), dim3(plan.grid / plan.nchunk), dim3(kThreads), 0,
-                               s, a);
+            hipLaunchKernelGGL((attend_combine_kernel<T, D, GP>),
+                               dim3(plan.grid / plan.nchunk * combine_parts(a.n, a.emit)), dim3(kThreads), 0, s, a);
         }
         return hipGetLastError();
     }
