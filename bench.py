@@ -9,8 +9,9 @@ scoring, fold, selection and compaction, with every input already resident in HB
 
 Prints one JSON line: evict-steps/s, the roofline of the dominant kernel (scoring; algorithmic bytes over its
 event-timed duration), Lazy R = 4 / R = 8 step rates on the same trajectory under both new-token priors, whole
-64-step runs (full refresh, Lazy R = 4 / R = 8 under both priors) from the same prefill, and the float64 CPU
-oracle timed on bounded samples of each step type (first step, steady refresh step, non-refresh step).  The
+64-step runs (full refresh, Lazy R = 4 / R = 8 under both priors) from the same prefill, the Score-Free 128k,
+Qwen-shaped and Tiny workloads (each in a child process of its own), and the float64 CPU oracle timed on
+bounded samples of each step type (first step, steady refresh step, non-refresh step).  The
 throughput comes from blocks of steps with events only around the block; the score kernel's launch durations
 (the roofline) from a further block with timing-only events (hipEventDisableSystemFence) around every scoring
 launch, read after the stream is synchronized: events between a step's kernels lengthen the step, so that block
@@ -202,10 +203,13 @@ def nonrefresh_bytes(cfg, n):
     return cfg.batch * n * 8 + 2 * 2 * cfg.layers * cfg.batch * cfg.n_kv_heads * cfg.head_dim * e + cfg.batch * 8
 
 
-def secondary_workloads(B, dev, K, W):
-    """The other configurations of the measurement plan, one after another on the freed device:
-    Score-Free at 131,072 tokens (step-1 rate, then non-refresh steps), the Qwen-shaped workload (steady
-    full-refresh steps) and the Tiny workload (launch-bound steps)."""
+SECONDARY = ("scorefree_128k", "qwen_8k", "tiny")
+
+
+def secondary_workloads(B, dev, K, W, which):
+    """One of the other configurations of the measurement plan (`which`): Score-Free at 131,072 tokens (step-1
+    rate, then non-refresh steps), the Qwen-shaped workload (steady full-refresh steps) or the Tiny workload
+    (launch-bound steps).  Each runs in a process of its own (see run_secondary)."""
     import torch
 
     from workload import QWEN, SCOREFREE128K, TINY, Workload
@@ -227,103 +231,131 @@ def secondary_workloads(B, dev, K, W):
                                   st["k"], st["v"], st["u"], st["pos"], ws, keep_out=keep, trace=trace)
 
     def timed_first_step(cfg, w, st, shape, params, ws):
-        keep = torch.zeros(cfg.batch, cfg.capacity, dtype=torch.uint8, device=dev)
-        n = st["n"] + 1
-        torch.cuda.synchronize()
-        a, z = B.HipEvent(), B.HipEvent()
-        a.record()
-        run(w, st, shape, params, ws, 1, keep=keep)
-        z.record()
-        ms = a.elapsed_ms(z)
-        return first_step_record(B, cfg, shape, params, n, keep, ms)
+        """Step 1 once on a copy of the prefill (the process's one-time costs: code-object loading, first touch
+        of the workspace; reported as cold_ms), then on the real state."""
+        def once(state):
+            keep = torch.zeros(cfg.batch, cfg.capacity, dtype=torch.uint8, device=dev)
+            n = state["n"] + 1
+            torch.cuda.synchronize()
+            a, z = B.HipEvent(), B.HipEvent()
+            a.record()
+            run(w, state, shape, params, ws, 1, keep=keep)
+            z.record()
+            return n, keep, a.elapsed_ms(z)
 
-    # Score-Free, 131,072-token prefill, B = 13,107, min prior
-    cfg = SCOREFREE128K
-    w, st, shape, params, ws = setup(cfg)
-    nsteps = min(cfg.steps - 1, K)
-    w_inputs = {t: w.step_inputs(t) for t in range(1, 2 + 4 * nsteps)}
-    first = timed_first_step(cfg, w, st, shape, params, ws)
-    sf = {"config": {"batch": cfg.batch, "layers": cfg.layers, "context": cfg.prefill_len, "budget": cfg.budget},
-          "step1": first, "nonrefresh_steps": nsteps}
-    # the frozen ranking's append-and-evict steps under each new-token prior, continuing the same cache: the
-    # minimum prior (the workload's "lowest frozen utility"), then the paper's mean prior
-    t_next = 2
-    for init in ("min", "mean"):
-        p_init = B.make_params(cfg.alpha, cfg.budget, cfg.refresh_period, cfg.score_free, init, cfg.recency_bias,
-                               cfg.recency_window)
-        torch.cuda.synchronize()
-        h0 = time.perf_counter()
-        for t in range(t_next, t_next + nsteps):
-            run(w, st, shape, p_init, ws, t)
-        torch.cuda.synchronize()
-        host_ms = 1e3 * (time.perf_counter() - h0) / nsteps
-        t_next += nsteps
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
+        copy = {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in st.items()}
+        cold_ms = once(copy)[2]
+        del copy
+        n, keep, ms = once(st)
+        rec = first_step_record(B, cfg, shape, params, n, keep, ms)
+        rec["cold_ms"] = round(cold_ms, 3)
+        return rec
+
+    if which == "scorefree_128k":
+        # Score-Free, 131,072-token prefill, B = 13,107, min prior
+        cfg = SCOREFREE128K
+        w, st, shape, params, ws = setup(cfg)
+        nsteps = min(cfg.steps - 1, K)
+        w_inputs = {t: w.step_inputs(t) for t in range(1, 2 + 4 * nsteps)}
+        first = timed_first_step(cfg, w, st, shape, params, ws)
+        sf = {"config": {"batch": cfg.batch, "layers": cfg.layers, "context": cfg.prefill_len, "budget": cfg.budget},
+              "step1": first, "nonrefresh_steps": nsteps}
+        # the frozen ranking's append-and-evict steps under each new-token prior, continuing the same cache: the
+        # minimum prior (the workload's "lowest frozen utility"), then the paper's mean prior
+        t_next = 2
+        for init in ("min", "mean"):
+            p_init = B.make_params(cfg.alpha, cfg.budget, cfg.refresh_period, cfg.score_free, init, cfg.recency_bias,
+                                   cfg.recency_window)
+            torch.cuda.synchronize()
+            h0 = time.perf_counter()
             for t in range(t_next, t_next + nsteps):
                 run(w, st, shape, p_init, ws, t)
-        t_next += nsteps
+            torch.cuda.synchronize()
+            host_ms = 1e3 * (time.perf_counter() - h0) / nsteps
+            t_next += nsteps
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for t in range(t_next, t_next + nsteps):
+                    run(w, st, shape, p_init, ws, t)
+            t_next += nsteps
+            torch.cuda.synchronize()
+            a, z = B.HipEvent(), B.HipEvent()
+            a.record()
+            g.replay()
+            z.record()
+            graph_ms = a.elapsed_ms(z) / nsteps
+            sf[f"nonrefresh_{init}_prior"] = {"ms_per_step": round(host_ms, 4), "steps_per_s": round(1e3 / host_ms, 1),
+                                              "graph_ms_per_step": round(graph_ms, 4),
+                                              "graph_steps_per_s": round(1e3 / graph_ms, 1)}
+            del g
+        out["scorefree_128k"] = sf
+
+    elif which == "qwen_8k":
+        # Qwen-shaped: batch 32, 28 layers, 28 / 4 heads (G = 7), 8k prefill, B = 2,048, full refresh
+        cfg = QWEN
+        w, st, shape, params, ws = setup(cfg)
+        kq = min(K, 100)
+        sustain = 64  # untimed steady steps first: a GPU left idle runs a short timed block below its clocks
+        w_inputs = {t: w.step_inputs(t) for t in range(1, 2 + sustain + W + 2 * kq)}
+        first = timed_first_step(cfg, w, st, shape, params, ws)
+        for t in range(2, 2 + sustain + W):
+            run(w, st, shape, params, ws, t)
         torch.cuda.synchronize()
-        a, z = B.HipEvent(), B.HipEvent()
-        a.record()
-        g.replay()
-        z.record()
-        graph_ms = a.elapsed_ms(z) / nsteps
-        sf[f"nonrefresh_{init}_prior"] = {"ms_per_step": round(host_ms, 4), "steps_per_s": round(1e3 / host_ms, 1),
-                                          "graph_ms_per_step": round(graph_ms, 4),
-                                          "graph_steps_per_s": round(1e3 / graph_ms, 1)}
-        del g
-    out["scorefree_128k"] = sf
-    del w, st, ws, w_inputs  # kept in torch's cache (see the note at the first step's copies)
+        h0 = time.perf_counter()
+        for t in range(2 + sustain + W, 2 + sustain + W + kq):
+            run(w, st, shape, params, ws, t)
+        torch.cuda.synchronize()
+        host_s = time.perf_counter() - h0
+        # a further block with events around every scoring launch: the score kernel's durations
+        pairs = [(B.HipEvent(True), B.HipEvent(True)) for _ in range(kq)]
+        for i, t in enumerate(range(2 + sustain + W + kq, 2 + sustain + W + 2 * kq)):
+            run(w, st, shape, params, ws, t, trace=B.make_trace({"score": pairs[i]}))
+        torch.cuda.synchronize()
+        score_ms = sum(p[0].elapsed_ms(p[1]) for p in pairs) / kq
+        by = step_bytes(cfg, cfg.budget + 1, B.kv_score_merge(shape, cfg.budget + 1, params))
+        out["qwen_8k"] = {"config": {"batch": cfg.batch, "layers": cfg.layers, "n_q_heads": cfg.n_q_heads,
+                                     "n_kv_heads": cfg.n_kv_heads, "context": cfg.prefill_len, "budget": cfg.budget},
+                          "step1": first, "steady_steps_per_s": round(kq / host_s, 1),
+                          "steady_ms_per_step": round(1e3 * host_s / kq, 4),
+                          "steady_GBps": round(by["total"] * kq / host_s / 1e9, 1),
+                          "score_kernel_ms": round(score_ms, 4),
+                          "score_kernel_GBps": round(by["score"] / (score_ms * 1e-3) / 1e9, 1),
+                          "score_kernel_pct_peak":
+                              round(100 * by["score"] / (score_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 1)}
 
-    # Qwen-shaped: batch 32, 28 layers, 28 / 4 heads (G = 7), 8k prefill, B = 2,048, full refresh
-    cfg = QWEN
-    w, st, shape, params, ws = setup(cfg)
-    kq = min(K, 100)
-    w_inputs = {t: w.step_inputs(t) for t in range(1, 2 + W + 2 * kq)}
-    first = timed_first_step(cfg, w, st, shape, params, ws)
-    for t in range(2, 2 + W):
-        run(w, st, shape, params, ws, t)
-    torch.cuda.synchronize()
-    h0 = time.perf_counter()
-    for t in range(2 + W, 2 + W + kq):
-        run(w, st, shape, params, ws, t)
-    torch.cuda.synchronize()
-    host_s = time.perf_counter() - h0
-    # a further block with events around every scoring launch: the score kernel's durations
-    pairs = [(B.HipEvent(True), B.HipEvent(True)) for _ in range(kq)]
-    for i, t in enumerate(range(2 + W + kq, 2 + W + 2 * kq)):
-        run(w, st, shape, params, ws, t, trace=B.make_trace({"score": pairs[i]}))
-    torch.cuda.synchronize()
-    score_ms = sum(p[0].elapsed_ms(p[1]) for p in pairs) / kq
-    by = step_bytes(cfg, cfg.budget + 1, B.kv_score_merge(shape, cfg.budget + 1, params))
-    out["qwen_8k"] = {"config": {"batch": cfg.batch, "layers": cfg.layers, "n_q_heads": cfg.n_q_heads,
-                                 "n_kv_heads": cfg.n_kv_heads, "context": cfg.prefill_len, "budget": cfg.budget},
-                      "step1": first, "steady_steps_per_s": round(kq / host_s, 1),
-                      "steady_ms_per_step": round(1e3 * host_s / kq, 4),
-                      "steady_GBps": round(by["total"] * kq / host_s / 1e9, 1),
-                      "score_kernel_ms": round(score_ms, 4),
-                      "score_kernel_GBps": round(by["score"] / (score_ms * 1e-3) / 1e9, 1),
-                      "score_kernel_pct_peak": round(100 * by["score"] / (score_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 1)}
-    del w, st, ws, w_inputs  # kept in torch's cache (see the note at the first step's copies)
-
-    # Tiny (parity-sized, launch-bound): 16 full-refresh steps
-    cfg = TINY
-    w, st, shape, params, ws = setup(cfg)
-    st = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in st.items()}
-    w_inputs = {t: {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in w.step_inputs(t).items()}
-                for t in range(1, cfg.steps + 1)}
-    run(w, st, shape, params, ws, 1)
-    torch.cuda.synchronize()
-    h0 = time.perf_counter()
-    for t in range(2, cfg.steps + 1):
-        run(w, st, shape, params, ws, t)
-    torch.cuda.synchronize()
-    tiny_ms = 1e3 * (time.perf_counter() - h0) / (cfg.steps - 1)
-    out["tiny"] = {"steps_per_s": round(1e3 / tiny_ms, 1), "ms_per_step": round(tiny_ms, 4),
-                   "note": "launch-bound: a few kernels of a few microseconds each per step"}
-    del w, st, ws, w_inputs  # kept in torch's cache (see the note at the first step's copies)
+    elif which == "tiny":
+        # Tiny (parity-sized, launch-bound): 16 full-refresh steps
+        cfg = TINY
+        w, st, shape, params, ws = setup(cfg)
+        st = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in st.items()}
+        w_inputs = {t: {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in w.step_inputs(t).items()}
+                    for t in range(1, cfg.steps + 1)}
+        run(w, st, shape, params, ws, 1)
+        torch.cuda.synchronize()
+        h0 = time.perf_counter()
+        for t in range(2, cfg.steps + 1):
+            run(w, st, shape, params, ws, t)
+        torch.cuda.synchronize()
+        tiny_ms = 1e3 * (time.perf_counter() - h0) / (cfg.steps - 1)
+        out["tiny"] = {"steps_per_s": round(1e3 / tiny_ms, 1), "ms_per_step": round(tiny_ms, 4),
+                       "note": "launch-bound: a few kernels of a few microseconds each per step"}
+    else:
+        raise ValueError(which)
     return out
+
+
+def run_secondary(name, K, W):
+    """One secondary workload in a child process of its own, whose one JSON line is read back.  A process's
+    history changes the step times of the workloads it runs later on these systems (the Qwen-shaped steady step
+    measured ~9% slower after the 8B and 128k sections in the same process than alone), so each configuration
+    starts fresh.  The child is started as a new process (not exec'd over this one)."""
+    import subprocess
+
+    cmd = [sys.executable, os.path.abspath(__file__), "--secondary-only", name, "--steps", str(K), "--warmup", str(W)]
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=900)
+    if r.returncode != 0:
+        return {"error": f"exit status {r.returncode}", "stderr_tail": r.stderr[-800:]}
+    return json.loads(r.stdout.strip().splitlines()[-1])[name]
 
 
 def extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, full_ms):
@@ -445,6 +477,9 @@ def main():
                     help="consecutive non-refresh steps the CPU oracle times")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-secondary", action="store_true", help="skip the Score-Free 128k / Qwen / Tiny sections")
+    ap.add_argument("--secondary-only", choices=SECONDARY, default=None,
+                    help="run only that secondary workload and print its record (the benchmark starts one child "
+                         "process per secondary workload this way)")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
                     help="run a plain device copy of this size first (counter calibration)")
     args = ap.parse_args()
@@ -457,6 +492,12 @@ def main():
 
     from paper_2609_03515_amd import binding as B
     from workload import LLAMA8B, Workload, raw_numpy
+
+    if args.secondary_only:
+        dev = torch.device("cuda:0")
+        torch.cuda.set_device(dev)
+        print(json.dumps(secondary_workloads(B, dev, args.steps, args.warmup, args.secondary_only)))
+        return
 
     cfg = LLAMA8B
     dev = torch.device("cuda:0")
@@ -627,7 +668,7 @@ def main():
                      "inputs": (raw_numpy(si["q"][:, 0:1]), raw_numpy(si["k_new"][:, 0:1]),
                                 raw_numpy(si["v_new"][:, 0:1]), si["new_pos"])}
     del st, k, v, u, pos, ws, inputs, prefill
-    other = secondary_workloads(B, dev, K, W) if not args.no_secondary else {}
+    other = {} if args.no_secondary else {name: run_secondary(name, K, W) for name in SECONDARY}
 
     score_avg_ms = sum(score_ms) / len(score_ms)
     achieved = by["score"] / (score_avg_ms * 1e-3) / 1e9
