@@ -8,12 +8,12 @@
 // One workgroup per (layer, sequence, KV head, row chunk):
 //   1. K pass: logits of the chunk's rows for the group's heads into LDS (the scorer's lane machinery and
 //      dynamic unit claiming), running per-head max;
-//   2. e = exp(z - max) in place, per-head sums;
-//   3. V pass: every lane accumulates e_h(row) * v(row) for the GP heads over its 16-byte V chunks, the
-//      probabilities of a row being GP consecutive LDS words;
-//   4. cross-lane / cross-wave reduction in a fixed order (deterministic), then either the normalised
-//      output (one chunk per slab) or the chunk's unnormalised partial output with its per-head (max, sum);
-//   5. when the score is wanted: the group probability sums r of the rows (one chunk), or the raw logits
+//   2. e = exp(z - max) in place with per-head sums (with the score: a pass of its own; without: by the wave
+//      that claims a block in the V pass), then the V pass: every lane accumulates e_h(row) * v(row) for the
+//      GP heads over its 16-byte V chunks, the probabilities of a row being GP consecutive LDS words;
+//   3. cross-lane / cross-wave reduction in a fixed order, then either the normalised output (one chunk per
+//      slab) or the chunk's unnormalised partial output with its per-head (max, sum);
+//   4. when the score is wanted: the group probability sums r of the rows (one chunk), or the raw logits
 //      (several chunks), which a combine kernel turns into outputs and scores.
 // Chunks exist so that one layer's slabs (batch x KV heads, e.g. 64) still occupy all 256 CUs.
 #include "stream_lane.h"
@@ -148,8 +148,17 @@ __global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
 
 // kV = false: score only (no V pass, no output), for scoring long slabs in chunks: the chunks write their
 // logits and per-head (max, sum) for the scorer's finish kernel.
+// Waves per SIMD the compiler must leave room for: bf16 rows of d = 128 with groups of 4 (the 8B shape) are held
+// to 128 registers, i.e. two workgroups per CU, which the all-layer call (2,048 workgroups) uses: uncapped the
+// kernel takes 129 and that call with the score measured 1% slower.  Other instances keep what they need.
 template <typename T, int D, int GP, bool kV>
-__global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
+constexpr int attend_waves_per_eu() {
+    return (kV && GP == 4 && D == 128 && std::is_same<T, bf16_t>::value) ? 4 : 1;
+}
+
+template <typename T, int D, int GP, bool kV>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(attend_waves_per_eu<T, D, GP, kV>())))
+void attend_kernel(ScoreArgs a) {
     using L = Lane<T, D, GP>;
     using E = Elem<T>;
     using chunk_t = typename L::chunk_t;
@@ -235,8 +244,9 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
         }
     }
 
-    // 2. per-head max, exponentials in place, per-head sums; several chunks: the logits go to HBM for the
-    //    score's finish kernel
+    // per-head max, then the exponentials in place with their per-head sums: in a pass of their own when a score
+    // is produced (several chunks: the logits go to HBM on the way, for the finish or combine kernel), else
+    // inside the V pass (below)
     kp.publish_max(mk, red_m[ln.wave]);
     __syncthreads();
     float m = red_m[0][ln.hh];
@@ -255,27 +265,33 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
         if (write_z && z != -INFINITY) store_stream_at(zrow + ln.unit_row(unit), z);
         return z == -INFINITY ? 0.0f : __expf(z - m);
     };
-    int i = 0;
-    for (; i + kEpi <= mine; i += kEpi) {
-        float e[kEpi];
+    // Measured for one decoder layer per call (8B shape): without the score, exponentials inside the V pass
+    // save the pass and its barrier (32 calls 790 -> 769 us); with it the logits' stores would join the V
+    // stream (842 -> 867 us), and one chunk's sums would have to be retaken for the scorer's order.
+    const bool exp_apart = !kV || a.emit;
+    if (exp_apart) {
+        int i = 0;
+        for (; i + kEpi <= mine; i += kEpi) {
+            float e[kEpi];
 #pragma unroll
-        for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
+            for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
 #pragma unroll
-        for (int v = 0; v < kEpi; ++v) {
-            e[v] = expo(e[v], ln.wave + (i + v) * kWaves);
-            ssum += e[v];
-            zl[(i + v) * kStep] = e[v];
+            for (int v = 0; v < kEpi; ++v) {
+                e[v] = expo(e[v], ln.wave + (i + v) * kWaves);
+                ssum += e[v];
+                if (kV) zl[(i + v) * kStep] = e[v];
+            }
         }
-    }
-    for (; i < mine; ++i) {
-        const float e = expo(zl[i * kStep], ln.wave + i * kWaves);
-        ssum += e;
-        zl[i * kStep] = e;
-    }
+        for (; i < mine; ++i) {
+            const float e = expo(zl[i * kStep], ln.wave + i * kWaves);
+            ssum += e;
+            if (kV) zl[i * kStep] = e;
+        }
 #pragma unroll
-    for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
-    if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;
-    __syncthreads();  // also publishes every exponential to the V pass
+        for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
+        if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;
+        __syncthreads();  // also publishes every exponential to the V pass
+    }
     if constexpr (!kV) {
         if (threadIdx.x < a.group) {
             const size_t h = (size_t)lb * a.hq + (size_t)g * a.group + threadIdx.x;
@@ -290,8 +306,11 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
         return;
     } else {
 
-    // 3. V pass: acc[h][c][x] = sum over this lane's rows of e_h(row) * v(row)[(p + c LPR) EPC + x]; with
-    //    emit_norms also the rows' value norms (VNorm), written out and summed
+    // 2. V pass: acc[h][c][x] = sum over this lane's rows of e_h(row) * v(row)[(p + c LPR) EPC + x]; with
+    //    emit_norms also the rows' value norms (VNorm), written out and summed.  Without the score the wave
+    //    that claims a block first turns its logits into exponentials in place (each lane the word it owns) and
+    //    adds them to its sums; the block's probabilities are then read by the wave's own lanes, so no
+    //    workgroup barrier separates the exponentials from the V stream.
     const __amdgpu_buffer_rsrc_t vns =
         raw_rsrc(a.vn + (size_t)s * a.n_stride + row0, a.emit_norms ? nrows * 4 : 0);
     float nsum = 0.0f;
@@ -312,8 +331,15 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
                 ubuf[slot] = claim(1);
                 ln.load_rows(vrs, ubuf[slot], vbuf[slot]);
                 if (more && ubuf[j] < nunits) {
+                    float* eb = zs + ubuf[j] * kWave;
+                    if (!exp_apart) {
+                        const float e = expo(eb[ln.lane], ubuf[j]);
+                        ssum += e;
+                        eb[ln.lane] = e;
+                        __builtin_amdgcn_wave_barrier();  // (the reads below are of words other lanes just wrote)
+                    }
                     // row k * NG + grp of the unit: its GP probabilities are words grp * LPR + k * GP + [0, GP)
-                    const float* eu = zs + ubuf[j] * kWave + ln.grp * LPR;
+                    const float* eu = eb + ln.grp * LPR;
 #pragma unroll
                     for (int k = 0; k < RPG; ++k) {
                         float e[GP];
@@ -352,8 +378,13 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
         for (int o = kWave / 2; o >= 1; o >>= 1) nsum += __shfl_xor(nsum, o, kWave);
         if (ln.lane == 0) red_n[ln.wave] = nsum;  // read after the barriers below
     }
+    if (!exp_apart) {  // the sums the waves took over the blocks they claimed
+#pragma unroll
+        for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
+        if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;  // read after the barriers below
+    }
 
-    // 4. lanes holding the same chunk of different rows (stride LPR), then the waves in order
+    // 3. lanes holding the same chunk of different rows (stride LPR), then the waves in order
 #pragma unroll
     for (int o = LPR; o < kWave; o <<= 1)
 #pragma unroll
@@ -435,13 +466,13 @@ __global__ __launch_bounds__(kThreads) void attend_kernel(ScoreArgs a) {
         return;
     }
 
-    // 5. one chunk: the score's group probability sums, staged in each unit's first RPW words (only this
+    // 4. one chunk: the score's group probability sums, staged in each unit's first RPW words (only this
     //    wave reads its units, and the V pass is over) and written with 16-byte stores
     if (a.emit && a.nchunk == 1) {
         static_assert(RPW % 4 == 0, "the coalesced store moves 4 rows at a time");
         const float tot = head_sum(ln.hh);
         const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
-        for (i = 0; i < mine; ++i) {
+        for (int i = 0; i < mine; ++i) {
             const float sum = group_allsum<GP>(zl[i * kStep] * inv);
             if (ln.hh == 0) zs[(ln.wave + i * kWaves) * kWave + ln.kk * L::NG + ln.grp] = sum;
         }
