@@ -13,8 +13,8 @@
 //      GP heads over its 16-byte V chunks, the probabilities of a row being GP consecutive LDS words;
 //   3. cross-lane / cross-wave reduction in a fixed order, then either the normalised output (one chunk per
 //      slab) or the chunk's unnormalised partial output with its per-head (max, sum);
-//   4. when the score is wanted: the group probability sums r of the rows (one chunk), or the raw logits
-//      (several chunks), which a combine kernel turns into outputs and scores.
+//   4. when the score is wanted: the group probability sums r of the rows (one chunk), or the chunk's
+//      exponentials (several chunks), which a combine kernel turns into outputs and scores.
 // Chunks exist so that one layer's slabs (batch x KV heads, e.g. 64) still occupy all 256 CUs.
 #include "stream_lane.h"
 
@@ -54,8 +54,9 @@ __device__ __forceinline__ void read_probs(const float* src, float (&e)[GP]) {
 
 // Several chunks per slab: a combine kernel after the chunks' launch, combine_parts(n) workgroups per slab:
 //   o_h = sum_c exp(m_c - M_h) o_c / sum_c exp(m_c - M_h) S_c,  M_h = max_c m_c   (part 0);
-//   r(row) = sum_{h in group} exp(z_h(row) - M_h) / S_h from the logits the chunks wrote, when emitting (part p:
-//   rows [p kCombineRows, (p + 1) kCombineRows)).
+//   r(row) = sum_{h in group} exp(z_h(row) - M_h) / S_h = sum_h e_h(row) exp(m_c - M_h) / S_h from the
+//   exponentials e_h = exp(z_h - m_c) the chunks wrote (c: the row's chunk), when emitting (part p: rows
+//   [p kCombineRows, (p + 1) kCombineRows)).
 // The rows are spread over several workgroups because one per slab left the score's rows (52 KB of logits per
 // slab at the 8B shape) to 64 workgroups at one decoder layer's batch.
 // Electing the last chunk of a slab inside the attention kernel instead was measured twice at the 8B shape:
@@ -127,19 +128,22 @@ __global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
         Elem<T>::store(ob + idx, acc * ci[h]);
     }
     if (a.emit) {
-        // rows are padded to a multiple of 64: 4 rows per thread and pass, rows >= n are scratch
+        // the rows hold e_h(row) = exp(z - m_c) of their chunk c (4 rows per thread and pass lie in one chunk: chunks
+        // are a multiple of 4 rows; rows are padded to a multiple of 64, rows >= n are scratch):
+        // r(row) = sum_h e_h(row) exp(m_c - M_h) / S_h
         const float* zb = a.z + head0 * a.n_stride;
         float* rb = a.r + (size_t)s * a.n_stride;
         const int row_end = min(a.n, (part + 1) * kCombineRows);
         for (int row = part * kCombineRows + threadIdx.x * 4; row < row_end; row += kThreads * 4) {
+            const int c = row / a.chunk_rows;
             f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
             for (int h = 0; h < a.group; ++h) {
-                const f32x4 z = *reinterpret_cast<const f32x4*>(zb + (size_t)h * a.n_stride + row);
-                const float m = cm[h], inv = ci[h];
-                acc.x += __expf(z.x - m) * inv;
-                acc.y += __expf(z.y - m) * inv;
-                acc.z += __expf(z.z - m) * inv;
-                acc.w += __expf(z.w - m) * inv;
+                const f32x4 e = *reinterpret_cast<const f32x4*>(zb + (size_t)h * a.n_stride + row);
+                const float f = __expf(a.part[(head0 + h) * a.nchunk + c].x - cm[h]) * ci[h];
+                acc.x += e.x * f;
+                acc.y += e.y * f;
+                acc.z += e.z * f;
+                acc.w += e.w * f;
             }
             *reinterpret_cast<f32x4*>(rb + row) = acc;
         }
@@ -256,7 +260,7 @@ void attend_kernel(ScoreArgs a) {
     float* zl = zs + ln.wave * kWave + ln.lane;
     constexpr int kStep = kWaves * kWave;
     const int mine = nunits > ln.wave ? (nunits - ln.wave + kWaves - 1) / kWaves : 0;
-    const bool write_z = a.emit && a.nchunk > 1;
+    const bool write_z = !kV && a.emit && a.nchunk > 1;  // (with V, a chunk's exponentials are stored later)
     // this lane's head's logit row (lanes of one wave hold different heads: stored by address)
     float* zrow = a.z + ((size_t)lb * a.hq + (size_t)g * a.group + ln.hh) * a.n_stride + row0;
     float ssum = 0.0f;
@@ -265,10 +269,11 @@ void attend_kernel(ScoreArgs a) {
         if (write_z && z != -INFINITY) store_stream_at(zrow + ln.unit_row(unit), z);
         return z == -INFINITY ? 0.0f : __expf(z - m);
     };
-    // Measured for one decoder layer per call (8B shape): without the score, exponentials inside the V pass
-    // save the pass and its barrier (32 calls 790 -> 769 us); with it the logits' stores would join the V
-    // stream (842 -> 867 us), and one chunk's sums would have to be retaken for the scorer's order.
-    const bool exp_apart = !kV || a.emit;
+    // Measured for one decoder layer per call (8B shape): exponentials inside the V pass save the pass and its
+    // barrier (32 calls 790 -> 769 us without the score).  With the score, a slab cut in chunks then stores its
+    // exponentials after the streams (stored during the V pass, with the logits, they had cost 842 -> 867 us);
+    // one chunk per slab keeps the pass, whose sums are the scorer's bit for bit.
+    const bool exp_apart = !kV || (a.emit && a.nchunk == 1);
     if (exp_apart) {
         int i = 0;
         for (; i + kEpi <= mine; i += kEpi) {
@@ -426,6 +431,23 @@ void attend_kernel(ScoreArgs a) {
                         }
             }
             __syncthreads();
+        }
+    }
+    if (a.emit && a.nchunk > 1) {
+        // the chunk's exponentials e_h(row) = exp(z - m_h) (m_h: this chunk's maximum), every block's already in
+        // LDS (the barriers above follow the V pass), to the logit rows for the combine: 4 rows of one head per
+        // thread and 16-byte store; rows past the chunk give 0 (rows are padded to a multiple of 64)
+        float* zc = a.z + ((size_t)lb * a.hq + (size_t)g * a.group) * a.n_stride + row0;
+        const int quads = (nrows + 3) / 4;
+        for (int t = threadIdx.x; t < a.group * quads; t += kThreads) {
+            const int h = t / quads, r0 = t % quads * 4;
+            f32x4 e;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int row = r0 + j, rib = row % RPW;
+                e[j] = row < nrows ? zs[row / RPW * kWave + rib % L::NG * LPR + rib / L::NG * GP + h] : 0.0f;
+            }
+            *reinterpret_cast<f32x4*>(zc + (size_t)h * a.n_stride + r0) = e;
         }
     }
     auto head_sum = [&](int h) {

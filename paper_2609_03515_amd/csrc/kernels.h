@@ -27,7 +27,8 @@ struct ScoreArgs {
     const void* k;
     const int32_t* pos;
     float* r;       // [layers][batch][n_kv][n_stride]
-    float* z;       // split: [layers][batch][n_q][n_stride]
+    float* z;       // split: [layers][batch][n_q][n_stride] logits (score-only chunks) or exponentials relative
+                    // to the chunk's maximum (attention chunks)
     float2* part;   // split: [layers][batch][n_q][nchunk] (max, sum)
     int batch, layers, hq, hkv, group, cap, n, n_stride;
     int recent_from;  // positions >= recent_from receive `bias`
