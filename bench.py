@@ -405,23 +405,31 @@ def extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, full_
         state["n"] = B.kv_evict_step(shape, p, state["t"], state["n"], si["new_pos"], si["q"], si["k_new"],
                                      si["v_new"], k, v, u, pos, ws, rank_trace=rank_trace, v_norms=norms)
 
-    def ms_of(fn, *a, **kw):
+    def ms_of(fn, *a, device=False, **kw):
+        """ms per call of fn by the host clock around KF - 1 calls; device=True: also by events around them
+        (the device's own time, without the host's per-call cost when that exceeds the kernels')."""
         fn(*a, **kw)  # one untimed call (first use of a configuration)
         torch.cuda.synchronize()
+        e0, e1 = B.HipEvent(), B.HipEvent()
         h0 = time.perf_counter()
+        e0.record()
         for _ in range(KF - 1):
             fn(*a, **kw)
+        e1.record()
         torch.cuda.synchronize()
-        return 1e3 * (time.perf_counter() - h0) / (KF - 1)
+        host = 1e3 * (time.perf_counter() - h0) / (KF - 1)
+        return (host, e0.elapsed_ms(e1) / (KF - 1)) if device else host
 
     res = {}
     kv_bytes = 2 * cfg.layers * cfg.batch * cfg.n_kv_heads * (cfg.budget + 1) * cfg.head_dim * 2
     for per_layer in (True, False):
-        a_ms = ms_of(attention_only, per_layer)
+        a_ms, a_dev = ms_of(attention_only, per_layer, device=True)
         f_ms = ms_of(fused_step, per_layer)
         s_ms = ms_of(separate_step, per_layer)
         res["per_layer_calls" if per_layer else "all_layers_one_call"] = {
             "attention_only_ms": round(a_ms, 4), "attention_GBps_K_V": round(kv_bytes / (a_ms * 1e-3) / 1e9, 1),
+            "attention_only_device_ms": round(a_dev, 4),
+            "attention_GBps_K_V_device": round(kv_bytes / (a_dev * 1e-3) / 1e9, 1),
             "fused_decode_step_ms": round(f_ms, 4), "separate_decode_step_ms": round(s_ms, 4),
             "fused_steps_per_s": round(1e3 / f_ms, 2), "separate_steps_per_s": round(1e3 / s_ms, 2),
             "eviction_overhead_fused_pct": round(100 * (f_ms - a_ms) / a_ms, 1),
