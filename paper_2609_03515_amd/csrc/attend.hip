@@ -150,8 +150,6 @@ __global__ __launch_bounds__(kThreads) void attend_combine_kernel(ScoreArgs a) {
     }
 }
 
-// kV = false: score only (no V pass, no output), for scoring long slabs in chunks: the chunks write their
-// logits and per-head (max, sum) for the scorer's finish kernel.
 // Waves per SIMD the compiler must leave room for: bf16 rows of d = 128 with groups of 4 (the 8B shape) are held
 // to 128 registers, i.e. two workgroups per CU, which the all-layer call (2,048 workgroups) uses: uncapped the
 // kernel takes 129 and that call with the score measured 1% slower.  Other instances keep what they need.
@@ -160,6 +158,8 @@ constexpr int attend_waves_per_eu() {
     return (kV && GP == 4 && D == 128 && std::is_same<T, bf16_t>::value) ? 4 : 1;
 }
 
+// kV = false: score only (no V pass, no output), for scoring long slabs in chunks: the chunks write their
+// logits and per-head (max, sum) for the scorer's finish kernel.
 template <typename T, int D, int GP, bool kV>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(attend_waves_per_eu<T, D, GP, kV>())))
 void attend_kernel(ScoreArgs a) {
