@@ -352,10 +352,16 @@ def run_secondary(name, K, W):
     import subprocess
 
     cmd = [sys.executable, os.path.abspath(__file__), "--secondary-only", name, "--steps", str(K), "--warmup", str(W)]
-    r = subprocess.run(cmd, capture_output=True, text=True, timeout=900)
+    try:
+        r = subprocess.run(cmd, capture_output=True, text=True, timeout=300)
+    except subprocess.TimeoutExpired:
+        return {"error": "no result within 300 s"}
     if r.returncode != 0:
         return {"error": f"exit status {r.returncode}", "stderr_tail": r.stderr[-800:]}
-    return json.loads(r.stdout.strip().splitlines()[-1])[name]
+    try:
+        return json.loads(r.stdout.strip().splitlines()[-1])[name]
+    except (IndexError, KeyError, ValueError):
+        return {"error": "no result line", "stdout_tail": r.stdout[-400:], "stderr_tail": r.stderr[-400:]}
 
 
 def extra_measurements(B, cfg, shape, ws, inputs, state, k, v, u, pos, KF, full_ms):
