@@ -288,6 +288,41 @@ def workspace(shape: KvShape, n_max: int, device="cuda") -> torch.Tensor:
     return ws
 
 
+class KvCache:
+    """One cache's device buffers (caller-owned torch tensors) and its cached row count n, for `evict_step`.
+
+    k, v: [layers][batch][n_kv_heads][capacity][head_dim] of the shape's dtype; u: [batch][capacity] f32;
+    pos: [batch][capacity] int32; ws: a workspace of kv_workspace_bytes(shape, capacity) bytes; v_norms: the
+    optional per-row value-norm cache [layers][batch][n_kv_heads][capacity] f32 (VNorm scoring)."""
+
+    def __init__(self, shape: KvShape, k, v, u, pos, n: int, ws, v_norms=None):
+        self.shape, self.k, self.v, self.u, self.pos, self.n, self.ws = shape, k, v, u, pos, int(n), ws
+        self.v_norms = v_norms
+
+    @classmethod
+    def allocate(cls, shape: KvShape, device="cuda", v_norms=False) -> "KvCache":
+        """Zero-filled buffers for `shape` with n = 0; the caller fills the prefill rows and sets n."""
+        dt = torch.float32 if shape.dtype == KV_F32 else torch.bfloat16
+        rows = (shape.layers, shape.batch, shape.n_kv_heads, shape.capacity)
+        return cls(shape, torch.zeros(rows + (shape.head_dim,), dtype=dt, device=device),
+                   torch.zeros(rows + (shape.head_dim,), dtype=dt, device=device),
+                   torch.zeros(shape.batch, shape.capacity, dtype=torch.float32, device=device),
+                   torch.zeros(shape.batch, shape.capacity, dtype=torch.int32, device=device), 0,
+                   workspace(shape, shape.capacity, device),
+                   torch.zeros(rows, dtype=torch.float32, device=device) if v_norms else None)
+
+
+def evict_step(cache: KvCache, q, k_new, v_new, t: int, params: KvParams, new_pos: int, keep_out=None,
+               s_out=None, stream=None) -> int:
+    """One decode step t (1-based) through kv_evict_step on `cache`'s buffers: the newcomer (q, k_new, v_new at
+    position new_pos) is appended, and on refresh steps the cache is scored, folded, selected and compacted to
+    the budget.  Sets cache.n to the new row count and returns it; raises KVError on a non-zero status."""
+    cache.n = kv_evict_step(cache.shape, params, t, cache.n, new_pos, q, k_new, v_new, cache.k, cache.v,
+                            cache.u, cache.pos, cache.ws, keep_out=keep_out, s_out=s_out, stream=stream,
+                            v_norms=cache.v_norms)
+    return cache.n
+
+
 def faults(ws, clear=False) -> int:
     """The workspace's fault word (kv_fault bits), read after synchronising the current stream."""
     out = torch.zeros(1, dtype=torch.int32, device=ws.device)

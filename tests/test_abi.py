@@ -5,6 +5,7 @@ import os
 import re
 
 import pytest
+import torch
 
 from paper_2609_03515_amd import binding as B
 
@@ -308,3 +309,21 @@ def test_value_norms_validation(lib):
     assert L.kv_value_norms(ctypes.byref(s), 10, FAKE, None, None) == B.KV_ERR_INVALID_ARG
     assert L.kv_value_norms(ctypes.byref(s), 10, FAKE + 8, FAKE, None) == B.KV_ERR_UNSUPPORTED
     assert L.kv_value_norms(ctypes.byref(s), 10, FAKE, FAKE + 1, None) == B.KV_ERR_UNSUPPORTED
+
+
+def test_cache_wrapper_raises_and_keeps_n(lib):
+    """evict_step(cache, ...) raises KVError on a rejected call and leaves the cache's row count alone (CPU
+    tensors stand in for the buffers: the host validation rejects both calls before any HIP call)."""
+    s = shape(capacity=16)
+    rows = (3, 2, 2, 16, 128)
+    cache = B.KvCache(s, torch.zeros(rows, dtype=torch.bfloat16), torch.zeros(rows, dtype=torch.bfloat16),
+                      torch.zeros(2, 16), torch.zeros(2, 16, dtype=torch.int32), 5, torch.zeros(256, dtype=torch.uint8))
+    q, kv_new = torch.zeros(2, 8, 128, dtype=torch.bfloat16), torch.zeros(3, 2, 2, 128, dtype=torch.bfloat16)
+    params = B.make_params(0.9, 8)
+    with pytest.raises(B.KVError) as e:
+        B.evict_step(cache, q, kv_new, kv_new, 0, params, new_pos=20, stream=0)     # steps are 1-based
+    assert e.value.status == B.KV_ERR_INVALID_ARG and cache.n == 5
+    cache.n = 16                                                                   # no room for the newcomer
+    with pytest.raises(B.KVError):
+        B.evict_step(cache, q, kv_new, kv_new, 1, params, new_pos=20, stream=0)
+    assert cache.n == 16

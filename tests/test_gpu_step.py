@@ -240,3 +240,29 @@ def test_steps_without_keep_out_leave_identical_caches(cfg):
         for name in ("k", "v"):
             assert torch.equal(st[name][:, :, :, :n1], other[name][:, :, :, :n1]), (t, name)
         print(f"{cfg.name} t={t}: identical with and without keep_out", flush=True)
+
+
+def test_cache_wrapper_matches_entry_point():
+    """evict_step(cache, q, k_new, v_new, t, params) is kv_evict_step on the cache's buffers: over refresh and
+    non-refresh steps (Lazy R = 4, mean prior) both leave bit-identical buffers and row counts."""
+    cfg = LLAMA8B_LAZY.scaled(batch=2, layers=3, prefill_len=800, budget=80, nonrefresh_init="mean")
+    w = Workload(cfg, seed=7)
+    cap = cfg.prefill_len + 1
+    st = w.prefill(capacity=cap)
+    shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
+    params = B.make_params(cfg.alpha, cfg.budget, cfg.refresh_period, cfg.score_free, cfg.nonrefresh_init,
+                           cfg.recency_bias, cfg.recency_window)
+    a, b = to_device(st), to_device(st)
+    cache = B.KvCache(shape, b["k"], b["v"], b["u"], b["pos"], st["n"], B.workspace(shape, cap))
+    ws, n = B.workspace(shape, cap), st["n"]
+    for t in range(1, 7):
+        si = w.step_inputs(t)
+        sig = to_device(si)
+        n = B.kv_evict_step(shape, params, t, n, si["new_pos"], sig["q"], sig["k_new"], sig["v_new"], a["k"],
+                            a["v"], a["u"], a["pos"], ws)
+        assert B.evict_step(cache, sig["q"], sig["k_new"], sig["v_new"], t, params, si["new_pos"]) == n
+        assert cache.n == n <= cfg.budget
+        torch.cuda.synchronize()
+        for key in ("k", "v", "u", "pos"):
+            assert torch.equal(a[key][..., :n] if key in ("u", "pos") else a[key][:, :, :, :n],
+                               b[key][..., :n] if key in ("u", "pos") else b[key][:, :, :, :n]), (t, key)
