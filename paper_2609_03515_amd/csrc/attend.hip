@@ -385,30 +385,50 @@ void attend_kernel(ScoreArgs a) {
     }
     if (!exp_apart) {  // the sums the waves took over the blocks they claimed
 #pragma unroll
-        for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
+        for (int o = GP; o < 16; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
+        ssum = rows_allsum(ssum);
         if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;  // read after the barriers below
     }
 
-    // 3. lanes holding the same chunk of different rows (stride LPR), then the waves in order
+    // 3. lanes holding the same chunk of different rows (stride LPR), then the waves in order.  With 16 lanes
+    //    per row the four rows hold the same chunks: four accumulators at a time are reduced over the rows with
+    //    row swaps, leaving accumulator 4i + r in row r (in the butterfly's order, so the sums are unchanged),
+    //    and every lane stores its share of the wave's slice.  Measured at the 8B shape, one decoder layer per
+    //    call: 24.6 -> 23.4 us; the 64 cross-row shuffles of the butterfly had kept the LDS crossbar busy for
+    //    ~1 us after the V pass.
+    constexpr int kAcc = GP * CPL * EPC;
+    constexpr bool kRowSwaps = kWaveSlices && LPR == 16 && kAcc % 4 == 0;
+    if constexpr (!kRowSwaps) {
 #pragma unroll
-    for (int o = LPR; o < kWave; o <<= 1)
-#pragma unroll
-        for (int h = 0; h < GP; ++h)
-#pragma unroll
-            for (int c = 0; c < CPL; ++c)
-#pragma unroll
-                for (int x = 0; x < EPC; ++x) acc[h][c][x] += __shfl_xor(acc[h][c][x], o, kWave);
-    if constexpr (kWaveSlices) {
-        // each wave's partial in its own slice; then output idx = ((w0 + w1) + w2) + ... by the thread that later
-        // stores it (the same thread-to-output mapping as the stores below, so no barrier between)
-        if (ln.lane < LPR) {
+        for (int o = LPR; o < kWave; o <<= 1)
 #pragma unroll
             for (int h = 0; h < GP; ++h)
 #pragma unroll
                 for (int c = 0; c < CPL; ++c)
 #pragma unroll
-                    for (int x = 0; x < EPC; ++x)
-                        obuf[ln.wave * GP * D + h * D + (ln.p + c * LPR) * EPC + x] = acc[h][c][x];
+                    for (int x = 0; x < EPC; ++x) acc[h][c][x] += __shfl_xor(acc[h][c][x], o, kWave);
+    }
+    if constexpr (kWaveSlices) {
+        // each wave's partial in its own slice; then output idx = ((w0 + w1) + w2) + ... by the thread that later
+        // stores it (the same thread-to-output mapping as the stores below, so no barrier between)
+        float* slice = obuf + ln.wave * GP * D;
+        if constexpr (kRowSwaps) {
+            const float* flat = &acc[0][0][0];  // index (h CPL + c) EPC + x
+            const int r = ln.lane / 16;
+#pragma unroll
+            for (int i = 0; i < kAcc / 4; ++i) {
+                const float t = rows_sum4(flat[4 * i], flat[4 * i + 1], flat[4 * i + 2], flat[4 * i + 3]);
+                const int ai = 4 * i + r;
+                const int h = ai / (CPL * EPC), c = ai / EPC % CPL, x = ai % EPC;
+                slice[h * D + (ln.p + c * LPR) * EPC + x] = t;
+            }
+        } else if (ln.lane < LPR) {
+#pragma unroll
+            for (int h = 0; h < GP; ++h)
+#pragma unroll
+                for (int c = 0; c < CPL; ++c)
+#pragma unroll
+                    for (int x = 0; x < EPC; ++x) slice[h * D + (ln.p + c * LPR) * EPC + x] = acc[h][c][x];
         }
         __syncthreads();
         for (int idx = threadIdx.x; idx < a.group * D; idx += kThreads) {

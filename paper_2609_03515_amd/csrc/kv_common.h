@@ -68,6 +68,46 @@ __device__ __forceinline__ float reduce_scatter(float (&v)[W], int p) {
     return v[0];
 }
 
+// Exchanges between the four 16-lane rows of a wave with gfx950's row swaps, which run on the vector ALU
+// instead of the LDS crossbar that a cross-row shuffle (ds_bpermute) goes through:
+//   v_permlane16_swap a, b: row 1 of a <-> row 0 of b, row 3 of a <-> row 2 of b;
+//   v_permlane32_swap a, b: rows 2, 3 of a <-> rows 0, 1 of b.
+// They are issued from inline assembly with two wait states before (a vector ALU write of an operand just
+// before the swap) and after: the compiler's builtins for these instructions return a wrong second result
+// after its instruction combining (seen in its output: the second half of the swap replaced by the first).
+__device__ __forceinline__ void swap_rows16(float& a, float& b) {
+    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void swap_rows32(float& a, float& b) {
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+
+// Sum over the four rows at the lane's position, (row0 + row1) + (row2 + row3) in every lane: the order of a
+// xor-16-then-xor-32 butterfly, so the result is bit-identical to it.
+__device__ __forceinline__ float rows_allsum(float x) {
+    float a = x, b = x;
+    swap_rows16(a, b);  // a = [x0 x0 x2 x2], b = [x1 x1 x3 x3]
+    float c = a + b, d = c;
+    swap_rows32(c, d);  // c = [x01 x01 x01 x01], d = [x23 x23 x23 x23]
+    return c + d;
+}
+__device__ __forceinline__ float rows_allmax(float x) {
+    float a = x, b = x;
+    swap_rows16(a, b);
+    float c = fmaxf(a, b), d = c;
+    swap_rows32(c, d);
+    return fmaxf(c, d);
+}
+// Four values reduced over the rows at once: row r of the result holds the sum of value r (a, b, e, f for
+// r = 0..3) at the lane's position, again (row0 + row1) + (row2 + row3).
+__device__ __forceinline__ float rows_sum4(float a, float b, float e, float f) {
+    swap_rows16(a, b);  // a = [a0 b0 a2 b2], b = [a1 b1 a3 b3]
+    swap_rows16(e, f);
+    float ab = a + b, ef = e + f;  // [a01 b01 a23 b23], [e01 f01 e23 f23]
+    swap_rows32(ab, ef);           // [a01 b01 e01 f01], [a23 b23 e23 f23]
+    return ab + ef;
+}
+
 // Online-softmax pair (running max, sum of exp(z - max)).
 struct MaxSum {
     float m, s;

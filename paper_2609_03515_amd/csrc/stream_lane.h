@@ -277,10 +277,12 @@ struct KUnit {
         m = fmaxf(m, z);
         zs[u * kWave + ln.lane] = z;
     }
-    // the wave's per-head maxima into red[0, GP)
+    // the wave's per-head maxima into red[0, GP) (lanes of one head: equal lane index mod GP; steps below 16
+    // stay inside a 16-lane row, the rows are combined with row swaps)
     __device__ void publish_max(max_t m, float* red) const {
 #pragma unroll
-        for (int o = GP; o < kWave; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+        for (int o = GP; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, kWave));
+        m = rows_allmax(m);
         if (ln.lane < GP) red[ln.lane] = m;
     }
 };
