@@ -210,42 +210,24 @@ void attend_kernel(ScoreArgs a) {
         return __builtin_amdgcn_readfirstlane(u);
     };
 
-    // 1. K pass (loads of claims past the end read zeros and are not reduced)
+    // 1. K pass
     typename KP::max_t mk = kp.max_init();
     {
         typename KP::buf_t kbuf[kNbufK];
-        int pbuf[kNbufK], ubuf[kNbufK];
-#pragma unroll
-        for (int j = 0; j < kNbufK - 1; ++j) {
-            ubuf[j] = claim(0);
-            kp.load(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
-        }
-        bool more = true;
-        while (more) {
-#pragma unroll
-            for (int j = 0; j < kNbufK; ++j) {
-                const int slot = (j + kNbufK - 1) % kNbufK;
-                ubuf[slot] = claim(0);
-                kp.load(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
-                if (more && ubuf[j] < nku) {
-                    kp.logits(a, kbuf[j], qv, pbuf[j], ubuf[j], nrows, zs, mk);
-                } else {
-                    more = false;
-                }
-            }
-        }
+        int pbuf[kNbufK];
+        claimed_units<kNbufK>(
+            nku, -1, [&]() __attribute__((always_inline)) { return claim(0); },
+            [&](auto slot, int u) __attribute__((always_inline)) { kp.load(krs, prs, u, kbuf[slot], pbuf[slot]); },
+            [&](auto slot, int u) __attribute__((always_inline)) { kp.logits(a, kbuf[slot], qv, pbuf[slot], u, nrows, zs, mk); });
     }
 
     // the V stream's first loads are issued now, so their latency overlaps the K pass's epilogue (barriers
     // wait for LDS only, not for these loads)
     chunk_t vbuf[kNbuf][RPG][CPL];
-    int vunit[kNbuf];
-    if constexpr (kV) {
-#pragma unroll
-        for (int j = 0; j < kNbuf - 1; ++j) {
-            vunit[j] = claim(1);
-            ln.load_rows(vrs, vunit[j], vbuf[j]);
-        }
+    int vfirst = -1;
+    if constexpr (kV && kNbuf == 2) {
+        vfirst = claim(1);
+        ln.load_rows(vrs, vfirst, vbuf[0]);
     }
 
     // per-head max, then the exponentials in place with their per-head sums: in a pass of their own when a score
@@ -327,7 +309,8 @@ void attend_kernel(ScoreArgs a) {
 #pragma unroll
             for (int x = 0; x < EPC; ++x) acc[h][c][x] = 0.0f;
     {
-        int (&ubuf)[kNbuf] = vunit;
+        int ubuf[kNbuf];
+        if constexpr (kNbuf == 2) ubuf[0] = vfirst;
         bool more = true;
         while (more) {
 #pragma unroll

@@ -404,6 +404,50 @@ struct KUnit<T, D, GP, true> {
     }
 };
 
+// Streams the units [0, n) a wave claims (claim() returns the next unclaimed unit, wave-uniform) with NB = 1 or
+// 2 units' loads in flight: load(slot, u) issues the loads of unit u into buffer `slot` (a compile-time
+// std::integral_constant), proc(slot, u) consumes them.  The loop is left as soon as a claim runs past the end,
+// before any load for it is issued, so no load is still in flight when the wave moves on (a load past the
+// end would return zeros, but only after the loads queued ahead of it, and the registers it writes are
+// reused after the loop).  `first`: a unit claimed and, if below n, loaded into slot 0 before the call
+// (NB = 2), or -1.
+template <int NB, class ClaimF, class LoadF, class ProcF>
+__device__ __forceinline__ void claimed_units(int n, int first, ClaimF claim, LoadF load, ProcF proc) {
+    static_assert(NB == 1 || NB == 2, "one or two units in flight");
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    if constexpr (NB == 1) {
+        for (;;) {
+            const int u = claim();
+            if (u >= n) break;
+            load(S0{}, u);
+            proc(S0{}, u);
+        }
+    } else {
+        int ua = first;
+        if (ua < 0) {
+            ua = claim();
+            if (ua < n) load(S0{}, ua);
+        }
+        while (ua < n) {
+            const int ub = claim();
+            if (ub >= n) {
+                proc(S0{}, ua);
+                break;
+            }
+            load(S1{}, ub);
+            proc(S0{}, ua);
+            ua = claim();
+            if (ua >= n) {
+                proc(S1{}, ub);
+                break;
+            }
+            load(S0{}, ua);
+            proc(S1{}, ub);
+        }
+    }
+}
+
 #ifndef IKV_EPI_UNROLL
 #define IKV_EPI_UNROLL 8
 #endif
