@@ -37,13 +37,27 @@ constexpr int score_waves_per_eu() {
     return kMulti && w > 2 * kWaves / 4 ? 2 * kWaves / 4 : w;
 }
 
+// K units in flight per wave: three in the multi-slab form over bf16 keys when a lane's share of a unit is at
+// most four 16-byte chunks and the logits are the vector form (8B steady step, alternating builds in one
+// process: 261.6 against 264.0 us, within the register budget of two workgroups per CU), else the default two
+// (the matrix-core form measured no faster with three; the one-slab form runs three workgroups per CU, and the
+// float32 forms would leave that budget).
+template <typename T, int D, int GP, bool kMulti>
+constexpr int score_nbuf() {
+    using G = Geometry<T, D, GP>;
+    return (IKV_NBUF == 0 && kMulti && std::is_same<T, bf16_t>::value && !use_mfma<T, D, GP>() &&
+            G::kRpg * G::kCpl <= 4)
+               ? 3
+               : G::kNbufLds;
+}
+
 template <typename T, int D, int GP, bool kMulti>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(score_waves_per_eu<T, D, GP, kMulti>())))
 void score_lds_kernel(ScoreArgs a) {
     using L = Lane<T, D, GP>;
     using KP = KUnit<T, D, GP>;
     constexpr int RPW = L::RPW;
-    constexpr int kNbuf = Geometry<T, D, GP>::kNbufLds;
+    constexpr int kNbuf = score_nbuf<T, D, GP, kMulti>();
 
     extern __shared__ float zs[];
     __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
