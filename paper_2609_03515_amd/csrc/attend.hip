@@ -497,9 +497,21 @@ void attend_kernel(ScoreArgs a) {
         static_assert(RPW % 4 == 0, "the coalesced store moves 4 rows at a time");
         const float tot = head_sum(ln.hh);
         const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
-        for (int i = 0; i < mine; ++i) {
+        const int row_in = ln.kk * L::NG + ln.grp;  // this lane's row inside a unit
+        int i = 0;
+        for (; i + kEpi <= mine; i += kEpi) {  // kEpi units' reads in flight at a time
+            float e[kEpi];
+#pragma unroll
+            for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
+#pragma unroll
+            for (int v = 0; v < kEpi; ++v) e[v] = group_allsum<GP>(e[v] * inv);
+            if (ln.hh == 0)
+#pragma unroll
+                for (int v = 0; v < kEpi; ++v) zs[(ln.wave + (i + v) * kWaves) * kWave + row_in] = e[v];
+        }
+        for (; i < mine; ++i) {
             const float sum = group_allsum<GP>(zl[i * kStep] * inv);
-            if (ln.hh == 0) zs[(ln.wave + i * kWaves) * kWave + ln.kk * L::NG + ln.grp] = sum;
+            if (ln.hh == 0) zs[(ln.wave + i * kWaves) * kWave + row_in] = sum;
         }
         __syncthreads();
         const __amdgpu_buffer_rsrc_t rrs = raw_rsrc(a.r + (size_t)s * a.n_stride, a.n_stride * 4);

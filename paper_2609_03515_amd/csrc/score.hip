@@ -200,13 +200,34 @@ void score_lds_kernel(ScoreArgs a) {
                 }
             }
         };
+        // kEpi units at a time: the emitting lanes read the item sums of all of them before adding and storing
+        // (one at a time, each read-add-store waited for its own LDS round trip: 2.5 of the epilogue's 5.4 us
+        // at the 8B step)
+        const int row_in = ln.kk * L::NG + ln.grp;  // this lane's row inside a unit
         i = 0;
         for (; i + kEpi <= mine; i += kEpi) {
             float e[kEpi];
 #pragma unroll
             for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
 #pragma unroll
-            for (int v = 0; v < kEpi; ++v) emit(ln.wave + (i + v) * kWaves, group_allsum<GP>(prob(e[v])));
+            for (int v = 0; v < kEpi; ++v) e[v] = group_allsum<GP>(prob(e[v]));
+            if (ln.hh == 0) {
+                if constexpr (!kMulti) {
+#pragma unroll
+                    for (int v = 0; v < kEpi; ++v) zs[(ln.wave + (i + v) * kWaves) * kWave + row_in] = e[v];
+                } else {
+                    float* acc = racc + (ln.wave + i * kWaves) * RPW + row_in;  // units kWaves apart
+                    if (gi != 0) {
+                        float old[kEpi];
+#pragma unroll
+                        for (int v = 0; v < kEpi; ++v) old[v] = acc[v * kWaves * RPW];
+#pragma unroll
+                        for (int v = 0; v < kEpi; ++v) e[v] = old[v] + e[v];
+                    }
+#pragma unroll
+                    for (int v = 0; v < kEpi; ++v) acc[v * kWaves * RPW] = e[v];
+                }
+            }
         }
         for (; i < mine; ++i) emit(ln.wave + i * kWaves, group_allsum<GP>(prob(zl[i * kStep])));
         __syncthreads();  // also: every read of this slab's logits is done before the next slab's K pass
