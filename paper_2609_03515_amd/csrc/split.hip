@@ -151,7 +151,12 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_
         // in a fixed order (a lane's words, then butterflies over the lanes of the same head)
         uint64_t* xs = xchg + (size_t)cur * C * a.group;  // [chunk][head]
         if (ln.wave == 0) {
-            const int h = ln.lane % GP;
+            // the lane index made opaque for this round: the word addresses below are recomputed here instead of
+            // being hoisted out of the slab loop, whose registers they would overflow (spilled, they came back
+            // from scratch memory on every round's exchange)
+            int lane = ln.lane;
+            asm volatile("" : "+v"(lane));
+            const int h = lane % GP;
             float mh = -INFINITY;  // this chunk's statistics of head h
             if (h < a.group) {
                 float sh = 0.0f;
@@ -169,7 +174,7 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_
             bool done[kMaxWords];
 #pragma unroll
             for (int k = 0; k < kMaxWords; ++k) {
-                const int c = (ln.lane + k * kWave) / GP;
+                const int c = (lane + k * kWave) / GP;
                 cm[k] = -INFINITY;
                 cs[k] = 0.0f;
                 done[k] = !(c < C && h < a.group);
@@ -181,7 +186,7 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_
 #pragma unroll
                 for (int k = 0; k < kMaxWords; ++k) {
                     if (done[k]) continue;
-                    const int c = (ln.lane + k * kWave) / GP;
+                    const int c = (lane + k * kWave) / GP;
                     const uint64_t v = __hip_atomic_load(xs + (size_t)c * a.group + h, __ATOMIC_RELAXED,
                                                          __HIP_MEMORY_SCOPE_AGENT);
                     if ((uint32_t)v != 0u) {
@@ -235,7 +240,9 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_
         // rows [4j, 4j + 4) of the chunk lie in one unit; rows up to the padded stride are scratch
         const __amdgpu_buffer_rsrc_t rrs =
             raw_rsrc(a.r + (size_t)cur * a.n_stride + row0, (a.n_stride - row0) * 4);
-        for (int j = threadIdx.x; j * 4 < rows; j += kThreads) {
+        int tid = threadIdx.x;
+        asm volatile("" : "+v"(tid));  // (as the lane index above: recomputed, not held across the slab loop)
+        for (int j = tid; j * 4 < rows; j += kThreads) {
             const int row = j * 4;
             store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]));
         }
