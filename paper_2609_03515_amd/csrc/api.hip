@@ -255,10 +255,12 @@ ScoreRoute score_route(const kv_shape& s, const Layout& L, int n, const ScorePla
 
 // Scoring (Eq. 1) of rows [0, n) of every layer into the workspace r: [layers][batch][n_kv / merge] rows.
 // k_new (one workgroup per slab only): row n - 1 is the step's newcomer, read from k_new instead of the cache,
-// with position cur_pos.
+// with position cur_pos.  vn_cache (a plan from vnorm_fused_plan only): VNorm applied by the scorer, with the
+// newcomer's V row from v_new.
 kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, const void* k, const int32_t* pos,
                     int cur_pos, float recency_bias, int recency_window, const ScorePlan& splan, void* ws,
-                    hipStream_t st, const void* k_new = nullptr) {
+                    hipStream_t st, const void* k_new = nullptr, const float* vn_cache = nullptr,
+                    const void* v_new = nullptr) {
     ScoreArgs a = score_args(s, L, n, q, k, pos, cur_pos, recency_bias, recency_window, ws);
     ScorePlan plan = splan;
     if (plan.split) {
@@ -304,7 +306,26 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
     a.merge = plan.merge;
     a.k_new = k_new;
     a.new_pos = cur_pos;
+    a.vn_cache = vn_cache;
+    a.v_new = v_new;
     return hip_status(launch_score(s.dtype, s.head_dim, plan, a, st));
+}
+
+// VNorm from the value-norm cache on a steady refresh step is applied by the multi-slab scorer (each KV head's
+// group sums weighted by norm / mean before the item adds them), so the step keeps a merged schedule and needs
+// neither the norms' mean kernel nor the fold's factors: when the logits are the vector form, entropy weighting
+// is off (it is taken over the plain scores), no merge is forced, and the item's norms fit in LDS beside its
+// sums with a merge above one.  8B steady step with VNorm, alternating builds in one process: 308.1 -> 282.0 us
+// (the plain step 263 us).
+bool vnorm_fused_plan(const kv_shape& s, const Layout& L, const kv_params& p, ScorePlan* out) {
+    if (!(p.score_variant & KV_SCORE_VNORM) || (p.score_variant & KV_SCORE_ENTROPY) || p.score_merge != 0)
+        return false;
+    ScorePlan plan = L.plan;
+    if (plan.split || !score_vnorm_fusable(s.dtype, s.head_dim, plan.group_pad)) return false;
+    score_merge(&plan, s.dtype, s.head_dim, s.n_kv_heads, s.layers * s.batch, 0, true);
+    if (plan.merge < 2) return false;
+    *out = plan;
+    return true;
 }
 
 // Scorer perturbations (Sec. 5.1) of a refresh step: value-row norms and entropy factors for the fold.  With
@@ -633,7 +654,9 @@ kv_status evict_step(const kv_shape& s, const kv_params& p, int t, int n_in, int
     }
     const bool vnorm = (p.score_variant & KV_SCORE_VNORM) != 0;
     if (refresh && n_in <= p.budget && !rank_trace && (!vnorm || v_norms)) {
-        const ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
+        ScorePlan plan = scorer_plan(s, L, p.score_variant, p.score_merge);
+        const bool vn_fused = vnorm && vnorm_fused_plan(s, L, p, &plan);
+        const int variant = vn_fused ? (p.score_variant & ~KV_SCORE_VNORM) : p.score_variant;
         if (!plan.split) {
             // A steady refresh step (one eviction, or none while under budget) in three kernels: the scorer
             // takes the newcomer from k_new as row n - 1, the fold gives it the refresh prior and reports each
@@ -644,8 +667,9 @@ kv_status evict_step(const kv_shape& s, const kv_params& p, int t, int n_in, int
             record(trace, 0, true, st);
             record(trace, 0, false, st);
             record(trace, 1, true, st);
-            rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, plan, ws, st, k_new);
-            if (rc == KV_OK) rc = run_variants(s, L, n, v, p.score_variant, r_groups, 1, ws, st, v_norms, v_new);
+            rc = run_score(s, L, n, q, k, pos, new_pos, p.recency_bias, p.recency_window, plan, ws, st, k_new,
+                           vn_fused ? v_norms : nullptr, vn_fused ? v_new : nullptr);
+            if (rc == KV_OK) rc = run_variants(s, L, n, v, variant, r_groups, 1, ws, st, v_norms, v_new);
             record(trace, 1, false, st);
             FoldExtra ex;
             ex.pos = pos;
@@ -653,8 +677,7 @@ kv_status evict_step(const kv_shape& s, const kv_params& p, int t, int n_in, int
             ex.candidates = n > p.budget;
             ex.norms = v_norms;
             if (rc == KV_OK)
-                rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, p.score_variant, r_groups, 1, false, ws, st, trace,
-                              ex);
+                rc = run_fold(s, L, n, u, s_out, p.rule, p.alpha, variant, r_groups, 1, false, ws, st, trace, ex);
             record(trace, 3, true, st);
             if (rc == KV_OK)
                 rc = run_place(s, L, n, p.budget, k_new, v_new, k, v, u, pos, v_norms, keep_out, ws, st);

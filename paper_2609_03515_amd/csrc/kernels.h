@@ -52,6 +52,11 @@ struct ScoreArgs {
     // position new_pos
     const void* k_new;
     int new_pos;
+    // multi-slab scorer with VNorm (Sec. 5.1) applied to the group sums: the caller's value-norm cache
+    // ([layers][batch][n_kv][cap]), read with the K rows, and with k_new the newcomer's V rows
+    // ([layers][batch][n_kv][d]); null: plain attention scores
+    const float* vn_cache;
+    const void* v_new;
 };
 
 struct ScorePlan {
@@ -71,7 +76,10 @@ bool score_plan(int dtype, int head_dim, int group, int n, ScorePlan* plan);
 // layers * batch; `forced` > 0: that many, a divisor of hkv) and grows the plan's LDS by their merged sums;
 // 1 for split plans or when the sums do not fit.  The automatic choice queries the device (CU count, and the
 // merged kernel's occupancy on first use per kernel instance).
-int score_merge(ScorePlan* plan, int dtype, int head_dim, int hkv, int lb_count, int forced);
+// vnorm: the item also keeps its slabs' value norms in LDS (the scorer with VNorm fused)
+int score_merge(ScorePlan* plan, int dtype, int head_dim, int hkv, int lb_count, int forced, bool vnorm = false);
+// the VNorm-fused scorer exists for this shape (vector-form logits)
+bool score_vnorm_fusable(int dtype, int head_dim, int group_pad);
 hipError_t launch_score(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s);
 hipError_t launch_split_finish(const ScoreArgs& a, hipStream_t s);
 

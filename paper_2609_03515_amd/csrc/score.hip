@@ -51,16 +51,23 @@ constexpr int score_nbuf() {
                : G::kNbufLds;
 }
 
-template <typename T, int D, int GP, bool kMulti>
+// kVN (multi-slab, vector-form logits only): VNorm (Sec. 5.1) applied to each slab's group sums before they are
+// added into the item's sums: the sum of row i is multiplied by |v_i| / mean_j |v_j| over the slab's n rows
+// (factor 1 when all norms are zero).  The norms come from the caller's value-norm cache, read with the K rows
+// (each owned row's norm with its position), staged in LDS beside the item sums; the newcomer's (row n - 1, V
+// not cached yet) is computed from v_new with the same arithmetic as the cache's.  The mean is summed in the
+// epilogue in a fixed order (each thread its rows, then the wave, then the waves in order).
+template <typename T, int D, int GP, bool kMulti, bool kVN = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(score_waves_per_eu<T, D, GP, kMulti>())))
 void score_lds_kernel(ScoreArgs a) {
     using L = Lane<T, D, GP>;
     using KP = KUnit<T, D, GP>;
     constexpr int RPW = L::RPW;
     constexpr int kNbuf = score_nbuf<T, D, GP, kMulti>();
+    static_assert(!kVN || (kMulti && !use_mfma<T, D, GP>()), "VNorm is fused into the multi-slab vector form");
 
     extern __shared__ float zs[];
-    __shared__ float red_m[kWaves][GP], red_s[kWaves][GP];
+    __shared__ float red_m[kWaves][GP], red_s[kWaves][GP], red_n[kVN ? kWaves : 1];
     __shared__ int next_unit[2];  // claim counters of the slab being streamed and of the next one
 
     const L ln;
@@ -74,8 +81,10 @@ void score_lds_kernel(ScoreArgs a) {
     const int n = a.n;
     const int nunits = (n + RPW - 1) / RPW;      // LDS blocks of logits
     const int nku = (n + KP::kRows - 1) / KP::kRows;  // claimed units of the K pass
-    // item sums after the logits (sized by the plan: the logits' units rounded up to whole iterations)
+    // item sums after the logits (sized by the plan: the logits' units rounded up to whole iterations), then
+    // with kVN the slab's value norms (as many words)
     float* racc = zs + (size_t)((nunits + kWaves - 1) / kWaves) * kThreads;
+    float* zn = racc + (size_t)((nunits + kWaves - 1) / kWaves) * kWaves * RPW;
     // with the newcomer given apart, rows [0, n - 1) come from the cache and row n - 1 is substituted into the
     // buffers of its unit before its logits are taken (the same arithmetic as a cached row)
     const bool has_new = a.k_new != nullptr;
@@ -88,14 +97,17 @@ void score_lds_kernel(ScoreArgs a) {
         return raw_rsrc(static_cast<const T*>(a.k) + (size_t)sidx * a.cap * D, cached * L::kRowBytes);
     };
     auto new_row = [&](int sidx) { return static_cast<const T*>(a.k_new) + (size_t)sidx * D; };
+    auto n_rsrc = [&](int sidx) { return raw_rsrc(a.vn_cache + (size_t)sidx * a.cap, kVN ? cached * 4 : 0); };
+    typename KP::row_t vn;  // kVN: the newcomer's V row (this lane's chunks)
     auto load_slab_consts = [&](int sidx, typename KP::q_t& qv, typename KP::row_t& kn) {
         kp.load_q(a, (size_t)(sidx / a.hkv), sidx % a.hkv, qv);
         if (has_new) kp.load_row(new_row(sidx), kn);
+        if (kVN && has_new) kp.load_row(static_cast<const T*>(a.v_new) + (size_t)sidx * D, vn);
     };
 
     if (threadIdx.x < 2) next_unit[threadIdx.x] = 0;
     int sidx = slab_at(0);
-    __amdgpu_buffer_rsrc_t krs = k_rsrc(sidx), prs = p_rsrc(sidx);
+    __amdgpu_buffer_rsrc_t krs = k_rsrc(sidx), prs = p_rsrc(sidx), nrs = n_rsrc(sidx);
     typename KP::q_t qv;
     typename KP::row_t kn;
     load_slab_consts(sidx, qv, kn);
@@ -110,11 +122,18 @@ void score_lds_kernel(ScoreArgs a) {
     // every path (claims past the end read zeros), so the wait before a reduction covers only its own buffer.
     typename KP::buf_t kbuf[kNbuf];
     int pbuf[kNbuf], ubuf[kNbuf];
+    float nbuf[kNbuf];  // kVN: the value norm of the row this lane owns in each buffered unit
+    auto load_unit = [&](int slot) {
+        kp.load(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
+        if constexpr (kVN)
+            nbuf[slot] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(nrs, ln.unit_row(ubuf[slot]) * 4, 0, 0));
+    };
     auto prime = [&](int si) {
 #pragma unroll
         for (int j = 0; j < kNbuf - 1; ++j) {
             ubuf[j] = claim(si);
-            kp.load(krs, prs, ubuf[j], kbuf[j], pbuf[j]);
+            load_unit(j);
         }
     };
     prime(0);
@@ -127,10 +146,19 @@ void score_lds_kernel(ScoreArgs a) {
             for (int j = 0; j < kNbuf; ++j) {
                 const int slot = (j + kNbuf - 1) % kNbuf;
                 ubuf[slot] = claim(si);
-                kp.load(krs, prs, ubuf[slot], kbuf[slot], pbuf[slot]);
+                load_unit(slot);
                 if (more && ubuf[j] < nku) {
                     if (ubuf[j] == unit_new) kp.put_row(kbuf[j], pbuf[j], kn, a.new_pos, unit_new, n - 1);
                     kp.logits(a, kbuf[j], qv, pbuf[j], ubuf[j], n, zs, mk);
+                    if constexpr (kVN) {
+                        float nv = nbuf[j];
+                        if (ubuf[j] == unit_new) {  // (every lane: the norm is a sum over the row's lane group)
+                            const float vnew = row_norm_lanes<T, L::LPR, L::CPL>(vn);
+                            if (ln.unit_row(ubuf[j]) == n - 1) nv = vnew;
+                        }
+                        const int row = ln.unit_row(ubuf[j]);
+                        if (ln.hh == 0 && row < n) zn[row] = nv;
+                    }
                 } else {
                     more = false;  // claims only grow: every later unit of this wave is past the end too
                 }
@@ -141,6 +169,7 @@ void score_lds_kernel(ScoreArgs a) {
             sidx = slab_at(si + 1);
             krs = k_rsrc(sidx);
             prs = p_rsrc(sidx);
+            nrs = n_rsrc(sidx);
             prime(si + 1);
         }
 
@@ -179,7 +208,27 @@ void score_lds_kernel(ScoreArgs a) {
 #pragma unroll
         for (int o = GP; o < kWave; o <<= 1) ssum += __shfl_xor(ssum, o, kWave);
         if (ln.lane < GP) red_s[ln.wave][ln.lane] = ssum;
+        const int row_in = ln.kk * L::NG + ln.grp;  // this lane's row inside a unit
+        if constexpr (kVN) {  // the slab's norm sum: a lane per row (hh = 0) over its rows, the wave, the waves
+            float nsum = 0.0f;
+            if (ln.hh == 0)
+                for (int u = 0; u < mine; ++u) {
+                    const int row = (ln.wave + u * kWaves) * RPW + row_in;
+                    if (row < n) nsum += zn[row];
+                }
+            nsum = wave_sum(nsum);
+            if (ln.lane == 0) red_n[ln.wave] = nsum;
+        }
         __syncthreads();
+        float inv_mean = 0.0f;  // kVN: n / (sum of the norms), 0 when every norm is zero (factor 1)
+        if constexpr (kVN) {
+            float t = red_n[0];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) t += red_n[w];
+            inv_mean = t > 0.0f ? (float)n / t : 0.0f;
+        }
+        // VNorm factor of row `row` of this slab (rows past n hold no norm: their sums are zero)
+        auto vfactor = [&](int row) { return (row < n && inv_mean > 0.0f) ? zn[row] * inv_mean : 1.0f; };
         float tot = red_s[0][ln.hh];
 #pragma unroll
         for (int w = 1; w < kWaves; ++w) tot += red_s[w][ln.hh];
@@ -195,6 +244,7 @@ void score_lds_kernel(ScoreArgs a) {
                 if (!kMulti) {
                     zs[unit * kWave + row] = sum;
                 } else {
+                    if constexpr (kVN) sum *= vfactor(unit * RPW + row);
                     float* acc = racc + unit * RPW + row;
                     *acc = gi == 0 ? sum : *acc + sum;
                 }
@@ -203,7 +253,6 @@ void score_lds_kernel(ScoreArgs a) {
         // kEpi units at a time: the emitting lanes read the item sums of all of them before adding and storing
         // (one at a time, each read-add-store waited for its own LDS round trip: 2.5 of the epilogue's 5.4 us
         // at the 8B step)
-        const int row_in = ln.kk * L::NG + ln.grp;  // this lane's row inside a unit
         i = 0;
         for (; i + kEpi <= mine; i += kEpi) {
             float e[kEpi];
@@ -217,6 +266,10 @@ void score_lds_kernel(ScoreArgs a) {
                     for (int v = 0; v < kEpi; ++v) zs[(ln.wave + (i + v) * kWaves) * kWave + row_in] = e[v];
                 } else {
                     float* acc = racc + (ln.wave + i * kWaves) * RPW + row_in;  // units kWaves apart
+                    if constexpr (kVN) {
+#pragma unroll
+                        for (int v = 0; v < kEpi; ++v) e[v] *= vfactor((ln.wave + (i + v) * kWaves) * RPW + row_in);
+                    }
                     if (gi != 0) {
                         float old[kEpi];
 #pragma unroll
@@ -290,9 +343,19 @@ hipError_t launch_lds(const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) 
     const int items = a.layers * a.batch * (a.hkv / a.merge);
     const bool multi = a.merge > 1 || (plan.grid > 0 && plan.grid < items);
     auto kern = multi ? score_lds_kernel<T, D, GP, true> : score_lds_kernel<T, D, GP, false>;
+    int which = multi ? 1 : 0;
+    if (a.vn_cache) {  // VNorm fused: multi-slab vector form only (the planner's choice, checked again here)
+        if constexpr (use_mfma<T, D, GP>()) {
+            return hipErrorInvalidValue;
+        } else {
+            if (!multi) return hipErrorInvalidValue;
+            kern = score_lds_kernel<T, D, GP, true, true>;
+            which = 2;
+        }
+    }
     if (plan.lds_bytes > 64 * 1024) {
-        static std::atomic<bool> raised[2][kMaxDevices];
-        const hipError_t e = raise_lds_limit(reinterpret_cast<const void*>(kern), raised[multi]);
+        static std::atomic<bool> raised[3][kMaxDevices];
+        const hipError_t e = raise_lds_limit(reinterpret_cast<const void*>(kern), raised[which]);
         if (e != hipSuccess) return e;
     }
     const int grid = plan.grid > 0 && plan.grid < items ? plan.grid : items;
@@ -418,11 +481,12 @@ bool score_plan(int dtype, int head_dim, int group, int n, ScorePlan* plan) {
 // the 8B steady step (2,048 slabs, all costs 8): m = 4 285.5 us, m = 2 291.7, m = 8 (one workgroup per CU)
 // 295.0, m = 1 302.8; at the Qwen-shaped step (3,584 slabs): m = 2 (cost 14) 327 us, m = 1 (14) 347, m = 4
 // (16) 347.
-int score_merge(ScorePlan* plan, int dtype, int head_dim, int hkv, int lb_count, int forced) {
+int score_merge(ScorePlan* plan, int dtype, int head_dim, int hkv, int lb_count, int forced, bool vnorm) {
     plan->merge = 1;
     plan->grid = 0;
     if (plan->split) return 1;
-    const size_t racc = (size_t)plan->chunk_rows * sizeof(float);  // an item's sums
+    // an item's sums (and with VNorm fused its slab's value norms)
+    const size_t racc = (size_t)plan->chunk_rows * sizeof(float) * (vnorm ? 2 : 1);
     const size_t lds1 = plan->lds_bytes, ldsm = lds1 + racc;
     int best = 1;
     if (forced > 0) {
@@ -453,6 +517,10 @@ int score_merge(ScorePlan* plan, int dtype, int head_dim, int hkv, int lb_count,
     plan->merge = best;
     if (best > 1) plan->lds_bytes = ldsm;
     return best;
+}
+
+bool score_vnorm_fusable(int dtype, int head_dim, int group_pad) {
+    return !(dtype == 1 && (group_pad == 8 || group_pad == 16) && head_dim * 2 / 16 >= group_pad);
 }
 
 hipError_t launch_score(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, hipStream_t s) {
