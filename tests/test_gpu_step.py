@@ -149,6 +149,20 @@ def test_value_norm_cache_lockstep(name, vnorm, entropy):
     run_lockstep(cfg, steps, vnorm=vnorm, entropy=entropy, norm_cache=True)
 
 
+def test_vnorm_fused_into_the_merged_scorer_lockstep():
+    """VNorm applied inside the multi-slab scorer (Sec. 5.1): a steady step given the value-norm cache, with the
+    planned merge above one (1,024 slabs over 256 CUs plan two KV heads per workgroup), weights each KV head's
+    group sums by norm / mean before the item adds them; in lockstep with the oracle over the first step (the
+    five-kernel path) and four steady steps, the norm cache checked after every step."""
+    cfg = LLAMA8B.scaled(batch=4, layers=32, prefill_len=400, budget=300)
+    cap = cfg.prefill_len + 1
+    shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
+    plain = B.make_params(cfg.alpha, cfg.budget, 1, False, "mean", cfg.recency_bias, cfg.recency_window)
+    if B.kv_score_merge(shape, cfg.budget + 1, plain) < 2:
+        pytest.skip("this device plans one KV head per scoring workgroup at this shape")
+    run_lockstep(cfg, 5, vnorm=True, norm_cache=True)
+
+
 @pytest.mark.parametrize("init", ["min", "mean"])
 def test_nonrefresh_newcomer_kept_on_position_tie(init):
     """Non-refresh step where the newcomer survives: under the min prior it ties the lowest utility, and the
