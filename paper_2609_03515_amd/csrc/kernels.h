@@ -19,9 +19,10 @@ constexpr uint32_t kFaultExchangeTimeout = 1u;  // a first-step scoring chunk ga
 int device_cus();
 
 // Scoring of one step (Eq. 1).  One workgroup streams a whole (layer, sequence, KV head) slab and keeps its
-// logits in LDS, writing the group probability sums r.  Slabs too long for that are cut into chunks
-// (launch_score_chunks): the chunks write logits z and per-head partial (max, sum) pairs, and a finish kernel
-// turns them into r.
+// logits in LDS, writing the group probability sums r.  Slabs too long for that are cut into chunks: the chunks
+// of a slab exchange their per-head (max, sum) pairs and write r themselves (launch_score_coop), or, when the
+// exchange words would not fit, write logits z and partial (max, sum) pairs (launch_score_chunks) that a finish
+// kernel turns into r.
 struct ScoreArgs {
     const void* q;
     const void* k;

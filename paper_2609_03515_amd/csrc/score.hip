@@ -13,8 +13,9 @@
 //
 // One workgroup per slab keeps the slab's logits in LDS; after the per-head (max, sum) reduction it writes
 // r(row) = sum over the group's heads of exp(z - max) / sum.  Slabs too long for one workgroup's LDS (long
-// first steps) are scored in chunks by the attention kernel's K pass (attend.hip), which writes logits and
-// per-chunk (max, sum); the finish kernel below combines them.
+// first steps) are scored in chunks that exchange their softmax statistics (split.hip); where the exchange
+// words would not fit, by the attention kernel's K pass (attend.hip), which writes logits and per-chunk
+// (max, sum), combined by the finish kernel below.
 #include <algorithm>
 
 #include "stream_lane.h"
