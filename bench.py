@@ -160,17 +160,17 @@ def cpu_baseline(cfg, seqs: int, steps: int, nonrefresh_steps: int, first_step=N
             "cpu_model": _cpu_model()}
 
 
-def step1_bytes(cfg, n, holes, path):
+def step1_bytes(cfg, n, holes, path, merge=1):
     """Algorithmic HBM bytes of decode step 1 on n tokens with `holes` rows moved per sequence: K read once,
-    queries and positions, the group sums (written by the scorer and read by the fold), the fold's utilities,
-    the selection's reads, and the compaction's moves (K and V rows of every layer and KV head read and
-    written, with their utility and position).  Only the scorer path that writes logits (KV_PATH_LOGITS) also
-    moves them: written and read back once; the chunk-exchange path keeps them in LDS."""
+    queries and positions, the group sums (one row per `merge` KV heads, written by the scorer and read by the
+    fold), the fold's utilities, the selection's reads, and the compaction's moves (K and V rows of every layer
+    and KV head read and written, with their utility and position).  Only the scorer path that writes logits
+    (KV_PATH_LOGITS) also moves them: written and read back once; the chunk-exchange path keeps them in LDS."""
     e = 2 if cfg.dtype == "bf16" else 4
     L, b, hq, hkv, d = cfg.layers, cfg.batch, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     score = L * b * hkv * n * d * e + L * b * hq * d * e + b * n * 4
     logits = 2 * L * b * hq * n * 4 if path == 2 else 0
-    sums = 2 * L * b * hkv * n * 4
+    sums = 2 * L * b * (hkv // merge) * n * 4
     fold = 2 * b * n * 4
     select = 2 * b * n * 4
     moves = sum(holes) * (2 * 2 * L * hkv * d * e + 4 * 4)
@@ -183,7 +183,7 @@ def first_step_bytes(B, cfg, shape, params, n, keep):
     the rows moved per sequence (read from the step's decision)."""
     info = B.kv_score_plan(shape, n, params)
     holes = (keep[:, : cfg.budget] == 0).sum(dim=1).tolist()
-    return step1_bytes(cfg, n, holes, info.path), info, holes
+    return step1_bytes(cfg, n, holes, info.path, info.merge), info, holes
 
 
 def first_step_record(B, cfg, shape, params, n, keep, ms):
@@ -192,6 +192,7 @@ def first_step_record(B, cfg, shape, params, n, keep, ms):
     by, info, holes = first_step_bytes(B, cfg, shape, params, n, keep)
     return {"ms": round(ms, 3), "n_scored": n,
             "scorer_path": {0: "lds", 1: "exchange", 2: "logits"}[info.path], "chunks_per_slab": info.chunks,
+            "kv_heads_per_sum_row": info.merge,
             "algorithmic_bytes": by, "GBps": round(by / (ms * 1e-3) / 1e9, 1),
             "pct_peak": round(100 * by / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 1), "rows_moved_per_seq": holes}
 

@@ -161,11 +161,12 @@ kv_status kv_rank_trace_state_bytes(int32_t batch, int32_t max_pos, size_t* byte
 kv_status kv_workspace_bytes(const kv_shape* shape, int32_t n_max, size_t* bytes);
 
 /* The params->score_merge that kv_evict_step resolves for a refresh step over n cached tokens (after the
- * append) on the current device: KV heads whose group sums one scoring workgroup adds (1 for VNorm and for
- * slabs scored in chunks; a positive params->score_merge is returned as given when it applies).  Exception: a
- * steady VNorm step given the value-norm cache, without entropy weighting and without a forced merge, weights
- * the sums inside the scorer and keeps a planned merge where its shape allows (vector-form logits, LDS room);
- * this call reports 1 for it.  Host only; the automatic choice reads the device's CU count.
+ * append) on the current device: KV heads whose group sums one scoring workgroup (or one team of chunks that
+ * exchange their statistics, path KV_PATH_EXCHANGE below) adds, in KV-head order (1 for VNorm and for slabs
+ * scored by chunks that write logits; a positive params->score_merge is returned as given when it applies).
+ * Exception: a steady VNorm step given the value-norm cache, without entropy weighting and without a forced
+ * merge, weights the sums inside the scorer and keeps a planned merge where its shape allows (vector-form
+ * logits, LDS room); this call reports 1 for it.  Host only; the automatic choice reads the device's CU count.
  * KV_ERR_INVALID_ARG as kv_evict_step for bad params. */
 kv_status kv_score_merge(const kv_shape* shape, int32_t n, const kv_params* params, int32_t* merge);
 

@@ -46,12 +46,19 @@ constexpr size_t kSplitLogitBytes = (size_t)IKV_SPLIT_LOGIT_MIB << 20;
 #define IKV_COOP_SPLIT 1
 #endif
 constexpr bool kCoopSplit = IKV_COOP_SPLIT != 0;
+// KV heads whose group sums a team of exchanging chunks adds by default (the largest divisor of n_kv up to
+// this): fewer rows of r written while K streams, and fewer for the fold to read.
+#ifndef IKV_COOP_MERGE
+#define IKV_COOP_MERGE 4
+#endif
+constexpr int kCoopMerge = IKV_COOP_MERGE;
 
 // The workspace's first 256 bytes hold the sticky fault word (kv_fault bits), at the same place for every n.
 constexpr size_t kFaultBytes = 256;
 static_assert(kFaultExchangeTimeout == (uint32_t)KV_FAULT_EXCHANGE_TIMEOUT, "fault bits of the kernels and the ABI");
 
 struct Layout {
+    int n;  // cached tokens the layout serves
     int n_stride;
     int max_pairs;
     ScorePlan plan;
@@ -87,6 +94,7 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 // chunk partials or attention partials), for the allocation-free variant.
 Layout layout_for(const kv_shape& s, int n, bool step_lds_only = false) {
     Layout L{};
+    L.n = n;
     L.n_stride = (n + 63) / 64 * 64;
     L.max_pairs = n;
     const int group = s.n_q_heads / s.n_kv_heads;
@@ -99,11 +107,16 @@ Layout layout_for(const kv_shape& s, int n, bool step_lds_only = false) {
     // chunk partials of long slabs (scorer) and of the attention
     size_t part_bytes = (size_t)ab.chunk_layers * s.batch * s.n_q_heads * sizeof(float2);
     if (L.plan.split && !step_lds_only) {
+        // the logits path's (max, sum) pairs and the exchange path's words (8 bytes each per query head and
+        // chunk); merged teams cut slabs into more chunks (their LDS also holds the item sums)
+        const int slabs = s.layers * s.batch * s.n_kv_heads;
         ScorePlan cp;
-        if (attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &cp, kScoreChunkLds)) {
-            const size_t sp = heads * cp.nchunk * sizeof(float2);
-            if (sp > part_bytes) part_bytes = sp;
-        }
+        int chunks = 0;
+        if (attend_plan(s.dtype, s.head_dim, group, n, slabs, &cp, kScoreChunkLds)) chunks = cp.nchunk;
+        for (int m = 1; m <= 2; ++m)
+            if (coop_plan(s.dtype, s.head_dim, group, n, slabs, m, &cp) && cp.nchunk > chunks) chunks = cp.nchunk;
+        const size_t sp = heads * chunks * sizeof(uint64_t);
+        if (sp > part_bytes) part_bytes = sp;
     }
     size_t off = kFaultBytes;
     L.r_off = off;
@@ -198,16 +211,6 @@ ScoreArgs score_args(const kv_shape& s, const Layout& L, int n, const void* q, c
     return a;
 }
 
-// The scorer's plan for a refresh step with these scorer variants: KV heads of one (layer, sequence) share a
-// workgroup and add their group sums (`merge` of them: 0 = planned) unless VNorm needs each KV head's sums
-// apart (it weights them per head).
-ScorePlan scorer_plan(const kv_shape& s, const Layout& L, int variant, int merge) {
-    ScorePlan plan = L.plan;
-    score_merge(&plan, s.dtype, s.head_dim, s.n_kv_heads, s.layers * s.batch,
-                (variant & KV_SCORE_VNORM) ? 1 : merge);
-    return plan;
-}
-
 // How a refresh step's scorer runs over n rows: one workgroup per slab with its logits in LDS; or, for slabs
 // too long for that, chunks that exchange their softmax statistics and write the group sums directly (on a
 // grid the device holds at once); or chunks that write logits for a finish kernel (slabs with more exchange
@@ -230,19 +233,21 @@ static_assert((int)ScoreRoute::kLds == KV_PATH_LDS && (int)ScoreRoute::kExchange
                   (int)ScoreRoute::kLogits == KV_PATH_LOGITS,
               "scorer paths of the planner and the ABI");
 
+// plan.merge > 1 (split plans): the exchange route with teams that add that many KV heads' sums, else the
+// logits route (whose finish writes one row per KV head, so a plan only carries such a merge when the
+// exchange route takes it: scorer_plan).
 ScoreRoute score_route(const kv_shape& s, const Layout& L, int n, const ScorePlan& plan) {
     ScoreRoute r{ScoreRoute::kLds, plan, 0};
     if (!plan.split) return r;
     r.kind = ScoreRoute::kLogits;
     const int group = s.n_q_heads / s.n_kv_heads;
+    const long slabs = (long)s.layers * s.batch * s.n_kv_heads;
     ScorePlan xp;
-    if (kCoopSplit &&
-        attend_plan(s.dtype, s.head_dim, group, n, s.layers * s.batch * s.n_kv_heads, &xp,
-                    coop_chunk_lds(plan.group_pad)) &&
-        xp.split && xp.nchunk * xp.group_pad <= kCoopMaxWords) {
-        const long slabs = (long)s.layers * s.batch * s.n_kv_heads;
+    if (kCoopSplit && coop_plan(s.dtype, s.head_dim, group, n, (int)slabs, plan.merge, &xp) && xp.split &&
+        xp.nchunk * xp.group_pad <= kCoopMaxWords) {
+        const long items = slabs / xp.merge;
         long grid = coop_workgroups(s.dtype, s.head_dim, xp) / xp.nchunk * xp.nchunk;
-        if (grid > slabs * xp.nchunk) grid = slabs * xp.nchunk;
+        if (grid > items * xp.nchunk) grid = items * xp.nchunk;
         if (grid >= xp.nchunk &&
             (size_t)s.layers * s.batch * s.n_q_heads * xp.nchunk * sizeof(uint64_t) <= L.opart_off - L.part_off) {
             r.kind = ScoreRoute::kExchange;
@@ -251,6 +256,29 @@ ScoreRoute score_route(const kv_shape& s, const Layout& L, int n, const ScorePla
         }
     }
     return r;
+}
+
+// The scorer's plan for a refresh step with these scorer variants: KV heads of one (layer, sequence) share a
+// workgroup (or, for slabs scored in exchanging chunks, a team of chunks) and add their group sums (`merge`
+// of them: 0 = planned) unless VNorm needs each KV head's sums apart (it weights them per head).  Slabs scored
+// by the logits route keep one row per KV head.
+ScorePlan scorer_plan(const kv_shape& s, const Layout& L, int variant, int merge) {
+    ScorePlan plan = L.plan;
+    const bool vnorm = (variant & KV_SCORE_VNORM) != 0;
+    score_merge(&plan, s.dtype, s.head_dim, s.n_kv_heads, s.layers * s.batch, vnorm ? 1 : merge);
+    if (plan.split && !vnorm) {
+        int m = merge;
+        if (m <= 0) {
+            m = kCoopMerge < kMaxMerge ? kCoopMerge : kMaxMerge;
+            while (m > 1 && s.n_kv_heads % m) --m;
+        }
+        if (m > 1) {
+            ScorePlan t = plan;
+            t.merge = m;
+            if (score_route(s, L, L.n, t).kind == ScoreRoute::kExchange) plan.merge = m;
+        }
+    }
+    return plan;
 }
 
 // Scoring (Eq. 1) of rows [0, n) of every layer into the workspace r: [layers][batch][n_kv / merge] rows.
@@ -270,12 +298,14 @@ kv_status run_score(const kv_shape& s, const Layout& L, int n, const void* q, co
             a.v = k;
             a.chunk_rows = route.xp.chunk_rows;
             a.nchunk = route.xp.nchunk;
+            a.merge = route.xp.merge;
             a.emit = 1;
             return hip_status(launch_score_coop(s.dtype, s.head_dim, route.xp, a, at<uint64_t>(ws, L.part_off),
                                                 (int)route.grid, at<uint32_t>(ws, 0), st));
         }
         // LDS-resident chunks of the attention kernel's K pass that write logits, then the finish kernel, per
-        // group of layers
+        // group of layers (one row of r per KV head: scorer_plan merges only for the exchange route)
+        if (plan.merge != 1) return KV_ERR_UNSUPPORTED;
         const int lg = logit_layer_group(s, L);
         const size_t e = (size_t)esize(s);
         for (int l0 = 0; l0 < s.layers; l0 += lg) {

@@ -67,7 +67,7 @@ struct ScorePlan {
     int rows_per_iter; // rows one workgroup covers per loop iteration
     int chunk_rows;    // rows per workgroup
     int nchunk;        // workgroups per slab
-    int merge;         // KV heads per workgroup (LDS-resident scorer; set by score_merge)
+    int merge;         // KV heads whose group sums one workgroup adds (score_merge; coop_plan for chunks)
     size_t lds_bytes;  // dynamic LDS per workgroup (fast path)
     int grid;
 };
@@ -96,10 +96,21 @@ bool attend_plan(int dtype, int head_dim, int group, int n, int slabs, ScorePlan
 #define IKV_SCORE_CHUNK_LDS (52 * 1024)
 #endif
 constexpr size_t kScoreChunkLds = IKV_SCORE_CHUNK_LDS;
-// Logit LDS of one chunk of the chunk-exchange scorer: padded groups of 8 and 16 (matrix-core logits) hold two
+// LDS of one chunk of the chunk-exchange scorer: padded groups of 8 and 16 (matrix-core logits) hold two
 // workgroups per CU by their registers anyway, so their chunks take the fast-path maximum of 80 KiB (fewer,
-// longer chunks: fewer exchange rounds; Qwen-shaped step 1 2.47 -> 2.45 ms).
-constexpr size_t coop_chunk_lds(int group_pad) { return group_pad >= 8 ? 80 * 1024 : kScoreChunkLds; }
+// longer chunks: fewer exchange rounds; Qwen-shaped step 1 2.47 -> 2.45 ms).  Smaller groups: 52 KiB of
+// logits, three workgroups per CU; with merged teams 42.5 KiB of logits and item sums.  Step 1 with teams of
+// 4 KV heads, builds alternating in one process (8B 32k / Score-Free 128k / Qwen-shaped, ms): one KV head
+// per row at 52 KiB 3.996 / 4.185 / 2.412; merged at 40 KiB 3.798 / 4.156 (65 chunks of the 128k slab: too
+// many words to exchange, so unmerged) / 2.356; 42.5 KiB 3.828 / 3.801 / 2.347; 46 KiB 3.748 / 3.962 / 2.355.
+// Another run (unmerged at 52 KiB 4.007 / 4.181): merged at 52 KiB 4.006 / 4.007, 64 KiB (two per CU) 3.802 /
+// 3.938, 80 KiB 3.784 / 4.165.
+#ifndef IKV_COOP_MERGED_LDS
+#define IKV_COOP_MERGED_LDS (42 * 1024 + 512)
+#endif
+constexpr size_t coop_chunk_lds(int group_pad, bool merged) {
+    return group_pad >= 8 ? 80 * 1024 : merged ? (size_t)IKV_COOP_MERGED_LDS : kScoreChunkLds;
+}
 // Workspace bound over every call of 1..layers layers on n rows: the largest (layers of the call) x nchunk,
 // and whether any such call splits.
 struct AttendBound {
@@ -116,7 +127,12 @@ hipError_t launch_score_chunks(int dtype, int head_dim, const ScorePlan& plan, c
 // multiple of nchunk no larger than coop_workgroups() (the workgroups the device holds at once).  xchg: zeroed
 // here, then one 64-bit word per (layer, sequence, query head, chunk).  A chunk whose peers' words do not all
 // arrive within the wait limit sets its group sums to NaN and ORs kFaultExchangeTimeout into *faults.
+// With merge > 1 (a divisor of n_kv) the chunks of one team score the merge KV heads of a (layer, sequence)
+// in consecutive rounds and add their group sums in LDS (a.merge; r: [layers][batch][n_kv / merge] rows).
 constexpr int kCoopMaxWords = 4 * 64;
+// The chunk plan of the exchange scorer for `merge`: attend_plan's chunks under the LDS cap coop_chunk_lds(),
+// which with merge > 1 also holds the item sums (4 bytes per row); lds_bytes is the kernel's whole dynamic LDS.
+bool coop_plan(int dtype, int head_dim, int group, int n, int slabs, int merge, ScorePlan* plan);
 int coop_workgroups(int dtype, int head_dim, const ScorePlan& plan);
 hipError_t launch_score_coop(int dtype, int head_dim, const ScorePlan& plan, const ScoreArgs& a, uint64_t* xchg,
                              int grid, uint32_t* faults, hipStream_t s);

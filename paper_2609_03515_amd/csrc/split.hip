@@ -9,11 +9,17 @@
 // scales its chunk's exponentials by exp(m - M) / S and writes the chunk's group sums r directly: no logits
 // round trip through memory.
 //
+// With merge > 1 a team of chunks scores the `merge` consecutive KV heads of one (layer, sequence) in
+// consecutive rounds and adds their group sums in LDS (in KV-head order, as the multi-slab scorer does),
+// writing one row of r per item instead of one per KV head.  Those writes, made while the rest of the grid
+// streams K, had cost more than their bytes: the 8B first step with only every fourth KV head's sums written
+// (a timing probe) took 3.825 instead of 3.994 ms.
+//
 // The grid is persistent and no larger than the workgroups the chip holds at once: workgroup w always takes
-// chunk w % C of slabs w / C, w / C + P, ... (P = grid / C slabs per round), so the C chunks of a slab are
-// consecutive workgroups that are dispatched together and only ever wait for one another.  That holds only
-// while the grid has the device to itself: work of other streams or processes that holds CUs can keep a
-// slab's later chunks from being dispatched while its earlier ones wait.  Every wait is therefore bounded
+// chunk w % C of the slabs of items w / C, w / C + P, ... (P = grid / C items at a time), so the C chunks of a
+// slab are consecutive workgroups that are dispatched together and only ever wait for one another.  That
+// holds only while the grid has the device to itself: work of other streams or processes that holds CUs can
+// keep a slab's later chunks from being dispatched while its earlier ones wait.  Every wait is therefore bounded
 // (a limit of ~64-clock sleeps, about 0.1 s by default); a chunk that gives up sets its group sums to NaN
 // and raises KV_FAULT_EXCHANGE_TIMEOUT in the workspace's fault word, so the failure is visible to the caller
 // (kv_fault_status) instead of folding a softmax that misses part of the slab.  The exchange words are zeroed
@@ -38,7 +44,7 @@ constexpr int coop_waves_per_eu() {
 
 template <typename T, int D, int GP>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(coop_waves_per_eu<T, D, GP>())))
-void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_t* faults, int spin_limit) {
+void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int items_per_round, uint32_t* faults, int spin_limit) {
     using L = Lane<T, D, GP>;
     using KP = KUnit<T, D, GP>;
     constexpr int RPW = L::RPW;
@@ -52,12 +58,15 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_
     const L ln;
     const KP kp;
     const int n = a.n, C = a.nchunk;
-    const int slabs = a.layers * a.batch * a.hkv;
+    const int merge = a.merge;  // KV heads per item: their group sums are added, one row of r per item
+    const int items = a.layers * a.batch * a.hkv / merge;
     const int cw = blockIdx.x % C;  // this workgroup's chunk of every slab it scores
     const int row0 = cw * a.chunk_rows;
     const int rows = min(a.chunk_rows, n - row0);
     const int nunits = (rows + RPW - 1) / RPW;          // LDS blocks of logits
     const int nku = (rows + KP::kRows - 1) / KP::kRows;  // claimed units of the K pass
+    // merge > 1: the item's sums of this chunk's rows after the logits (units rounded up to whole iterations)
+    float* racc = zs + (size_t)((nunits + kWaves - 1) / kWaves) * kThreads;
     auto k_rsrc = [&](int slab) {
         return raw_rsrc(static_cast<const T*>(a.k) + ((size_t)slab * a.cap + row0) * D, rows * L::kRowBytes);
     };
@@ -65,8 +74,9 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_
         return raw_rsrc(a.pos + (size_t)(slab / a.hkv % a.batch) * a.cap + row0, rows * 4);
     };
 
-    int slab = (int)blockIdx.x / C;
-    if (slab >= slabs) return;
+    int item = (int)blockIdx.x / C, gi = 0;  // the item being scored and the place of its slab in it
+    if (item >= items) return;
+    int slab = item * merge;
     if (threadIdx.x < 2) next_unit[threadIdx.x] = 0;
     __amdgpu_buffer_rsrc_t krs = k_rsrc(slab), prs = p_rsrc(slab);
     typename KP::q_t qv;
@@ -88,7 +98,7 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_
     };
     prime(0);
     for (int si = 0;; ++si) {
-        const int cur = slab;
+        const int cur = slab, cur_item = item, cur_gi = gi;
         typename KP::max_t mk = kp.max_init();
         bool more = true;
         while (more) {
@@ -104,8 +114,12 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_
                 }
             }
         }
-        slab += slabs_per_round;
-        const bool next = slab < slabs;
+        if (++gi == merge) {
+            gi = 0;
+            item += items_per_round;
+        }
+        slab = item * merge + gi;
+        const bool next = item < items;
         if (next) {  // the next slab's first loads overlap this chunk's epilogue and exchange
             krs = k_rsrc(slab);
             prs = p_rsrc(slab);
@@ -222,10 +236,20 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_
         }
         __syncthreads();
 
-        // group sums of the normalised probabilities, staged in the first RPW words of each unit's block
+        // group sums of the normalised probabilities: one slab per item, staged in the first RPW words of each
+        // unit's block (only this wave reads that block, and it has read the words); several, added to the
+        // item's sums (kEpi units read before they are added and stored)
         const float f = fh[ln.hh];
+        const int row_in = ln.kk * L::NG + ln.grp;  // this lane's row inside a unit
         auto emit = [&](int unit, float sum) {
-            if (ln.hh == 0) zs[unit * kWave + ln.kk * L::NG + ln.grp] = sum;
+            if (ln.hh == 0) {
+                if (merge == 1) {
+                    zs[unit * kWave + row_in] = sum;
+                } else {
+                    float* acc = racc + unit * RPW + row_in;
+                    *acc = cur_gi == 0 ? sum : *acc + sum;
+                }
+            }
         };
         i = 0;
         for (; i + kEpi <= mine; i += kEpi) {
@@ -233,18 +257,37 @@ void score_coop_kernel(ScoreArgs a, uint64_t* xchg, int slabs_per_round, uint32_
 #pragma unroll
             for (int v = 0; v < kEpi; ++v) e[v] = zl[(i + v) * kStep];
 #pragma unroll
-            for (int v = 0; v < kEpi; ++v) emit(ln.wave + (i + v) * kWaves, group_allsum<GP>(e[v] * f));
+            for (int v = 0; v < kEpi; ++v) e[v] = group_allsum<GP>(e[v] * f);
+            if (merge == 1) {
+#pragma unroll
+                for (int v = 0; v < kEpi; ++v) emit(ln.wave + (i + v) * kWaves, e[v]);
+            } else if (ln.hh == 0) {
+                float* acc = racc + (ln.wave + i * kWaves) * RPW + row_in;  // units kWaves apart
+                if (cur_gi != 0) {
+                    float old[kEpi];
+#pragma unroll
+                    for (int v = 0; v < kEpi; ++v) old[v] = acc[v * kWaves * RPW];
+#pragma unroll
+                    for (int v = 0; v < kEpi; ++v) e[v] = old[v] + e[v];
+                }
+#pragma unroll
+                for (int v = 0; v < kEpi; ++v) acc[v * kWaves * RPW] = e[v];
+            }
         }
         for (; i < mine; ++i) emit(ln.wave + i * kWaves, group_allsum<GP>(zl[i * kStep] * f));
         __syncthreads();
-        // rows [4j, 4j + 4) of the chunk lie in one unit; rows up to the padded stride are scratch
-        const __amdgpu_buffer_rsrc_t rrs =
-            raw_rsrc(a.r + (size_t)cur * a.n_stride + row0, (a.n_stride - row0) * 4);
-        int tid = threadIdx.x;
-        asm volatile("" : "+v"(tid));  // (as the lane index above: recomputed, not held across the slab loop)
-        for (int j = tid; j * 4 < rows; j += kThreads) {
-            const int row = j * 4;
-            store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(&zs[(row / RPW) * kWave + row % RPW]));
+        if (cur_gi == merge - 1) {
+            // the item's row of r for this chunk's rows: rows [4j, 4j + 4) lie in one unit; rows up to the
+            // padded stride are scratch
+            const __amdgpu_buffer_rsrc_t rrs =
+                raw_rsrc(a.r + (size_t)cur_item * a.n_stride + row0, (a.n_stride - row0) * 4);
+            int tid = threadIdx.x;
+            asm volatile("" : "+v"(tid));  // (as the lane index above: recomputed, not held across the slab loop)
+            for (int j = tid; j * 4 < rows; j += kThreads) {
+                const int row = j * 4;
+                const float* src = merge == 1 ? &zs[(row / RPW) * kWave + row % RPW] : &racc[row];
+                store_stream(rrs, row * 4, *reinterpret_cast<const f32x4*>(src));
+            }
         }
         if (!next) break;
         __syncthreads();  // every thread has read its staged sums before the next chunk's logits land
@@ -342,6 +385,36 @@ int coop_occupancy_d(int gp, size_t lds) {
 }
 
 }  // namespace
+
+bool coop_plan(int dtype, int head_dim, int group, int n, int slabs, int merge, ScorePlan* plan) {
+    ScorePlan p;
+    if (merge < 1 || !score_plan(dtype, head_dim, group, 1, &p)) return false;
+    const size_t budget = coop_chunk_lds(p.group_pad, merge > 1);
+    const size_t block = kWave * sizeof(float);  // one LDS block of logits: rpw rows
+    const int rpw = kWave / p.group_pad;
+    // the kernel's LDS: the chunk's blocks of logits, then with merge > 1 the item sums of its rows (blocks
+    // rounded up to whole iterations of kWaves blocks)
+    auto lds_of = [&](int rows) {
+        const size_t units = (size_t)(rows + rpw - 1) / rpw;
+        if (merge == 1) return units * block;
+        const size_t whole = (units + kWaves - 1) / kWaves * kWaves;
+        return whole * block + whole * rpw * sizeof(float);
+    };
+    // the logits take group_pad / (group_pad + 1) of the budget when the sums share it
+    size_t cap = merge == 1 ? budget : budget * p.group_pad / (p.group_pad + 1);
+    for (;;) {
+        if (!attend_plan(dtype, head_dim, group, n, slabs, plan, cap)) return false;
+        const size_t need = lds_of(plan->chunk_rows);
+        if (need <= budget) {
+            plan->lds_bytes = need;
+            break;
+        }
+        if (cap <= kWaves * block) return false;
+        cap -= kWaves * block;
+    }
+    plan->merge = merge;
+    return true;
+}
 
 int coop_workgroups(int dtype, int head_dim, const ScorePlan& plan) {
     int occ = 0;

@@ -52,6 +52,9 @@ def test_first_step_bytes_charge_logits_only_on_the_logits_path():
     # every moved row: K and V of every layer and KV head read and written, its utility and position
     fewer = bench.step1_bytes(cfg, n, [holes[0] - 1, holes[1]], 1)
     assert exchange - fewer == 2 * 2 * cfg.layers * cfg.n_kv_heads * cfg.head_dim * 2 + 16
+    # group sums of 4 KV heads added by the scorer: a quarter of the rows written and read back
+    merged = bench.step1_bytes(cfg, n, holes, 1, merge=4)
+    assert exchange - merged == 2 * cfg.layers * cfg.batch * (cfg.n_kv_heads - cfg.n_kv_heads // 4) * n * 4
 
 
 def test_nonrefresh_bytes():

@@ -220,9 +220,27 @@ MERGE_CASES = {
     ("tiny", 2, False)])
 def test_merged_scoring_lockstep(name, merge, entropy):
     """Scoring workgroups that cover several KV heads of one (layer, sequence) and add their group sums in
-    LDS before writing them (the first step of the split case scores in chunks, one row per KV head)."""
+    LDS before writing them (the first step of the split case: teams of chunks exchanging their statistics
+    that add the sums of 8 KV heads over consecutive rounds)."""
     cfg, steps = MERGE_CASES[name]
     run_lockstep(cfg, steps, entropy=entropy, merge=merge)
+
+
+@pytest.mark.parametrize("merge", [0, 1, 2, 4, 8])
+def test_first_step_exchange_teams_lockstep(merge):
+    """A first step over slabs too long for one workgroup: chunks that exchange their softmax statistics, in
+    teams that score `merge` KV heads of a (layer, sequence) in consecutive rounds and add their group sums in
+    LDS (0: the planned merge, 4 for 8 KV heads), then a steady step; in lockstep with the oracle."""
+    cfg = LLAMA8B.scaled(batch=2, layers=3, prefill_len=12000, budget=1200)
+    cap = cfg.prefill_len + 1
+    shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
+    params = B.make_params(cfg.alpha, cfg.budget, 1, False, "mean", cfg.recency_bias, cfg.recency_window,
+                           score_merge=merge)
+    info = B.kv_score_plan(shape, cap, params)
+    assert info.path == B.KV_PATH_EXCHANGE and info.chunks > 1, (info.path, info.chunks)
+    assert info.merge == (merge or 4)
+    assert B.kv_score_merge(shape, cap, params) == info.merge
+    run_lockstep(cfg, 2, merge=merge)
 
 
 @pytest.mark.parametrize("cfg", [LLAMA8B.scaled(batch=2, layers=3, prefill_len=300, budget=60),
