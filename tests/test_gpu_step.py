@@ -226,21 +226,22 @@ def test_merged_scoring_lockstep(name, merge, entropy):
     run_lockstep(cfg, steps, entropy=entropy, merge=merge)
 
 
-@pytest.mark.parametrize("merge", [0, 1, 2, 4, 8])
-def test_first_step_exchange_teams_lockstep(merge):
+@pytest.mark.parametrize("merge,entropy", [(0, False), (1, False), (2, False), (4, False), (8, False), (0, True)])
+def test_first_step_exchange_teams_lockstep(merge, entropy):
     """A first step over slabs too long for one workgroup: chunks that exchange their softmax statistics, in
     teams that score `merge` KV heads of a (layer, sequence) in consecutive rounds and add their group sums in
-    LDS (0: the planned merge, 4 for 8 KV heads), then a steady step; in lockstep with the oracle."""
+    LDS (0: the planned merge, 4 for 8 KV heads), then a steady step; in lockstep with the oracle (also with
+    entropy weighting, taken from the merged rows)."""
     cfg = LLAMA8B.scaled(batch=2, layers=3, prefill_len=12000, budget=1200)
     cap = cfg.prefill_len + 1
     shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
     params = B.make_params(cfg.alpha, cfg.budget, 1, False, "mean", cfg.recency_bias, cfg.recency_window,
-                           score_merge=merge)
+                           entropy=entropy, score_merge=merge)
     info = B.kv_score_plan(shape, cap, params)
     assert info.path == B.KV_PATH_EXCHANGE and info.chunks > 1, (info.path, info.chunks)
     assert info.merge == (merge or 4)
     assert B.kv_score_merge(shape, cap, params) == info.merge
-    run_lockstep(cfg, 2, merge=merge)
+    run_lockstep(cfg, 2, entropy=entropy, merge=merge)
 
 
 @pytest.mark.parametrize("cfg", [LLAMA8B.scaled(batch=2, layers=3, prefill_len=300, budget=60),
