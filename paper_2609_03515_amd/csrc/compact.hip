@@ -16,7 +16,9 @@ constexpr int kThreads = 256;
 // kMoveUnroll loads before its stores (the rows are disjoint), so several loads are in flight per lane.
 // Rows are read and written once: non-temporal loads and stores.  Step 1 at the 8B shape, same process: 4.20
 // ms with cached accesses and 4 rows per thread, 4.13 ms non-temporal; then 1 / 2 / 3 / 4 / 6 rows per thread:
-// 4.14 / 4.05 / 4.08 / 4.13 / 4.35 ms (8: 5.36 ms).
+// 4.14 / 4.05 / 4.08 / 4.13 / 4.35 ms (8: 5.36 ms).  Later (same method): 512-thread workgroups 3.893 and a grid
+// whose first dimension runs over the slabs 3.986 against 3.808 ms (Qwen-shaped step 1: 2.379 / 2.357 against
+// 2.386 ms).
 constexpr int kMoveUnroll = 2;
 
 __global__ __launch_bounds__(kThreads) void move_kernel(MoveArgs a) {
