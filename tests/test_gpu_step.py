@@ -244,6 +244,19 @@ def test_first_step_exchange_teams_lockstep(merge, entropy):
     run_lockstep(cfg, 2, entropy=entropy, merge=merge)
 
 
+def test_first_step_exchange_teams_several_items_each():
+    """Exchange teams that score more than one item: 40,001 tokens make 19 chunks per slab, so an MI355X holds
+    768 / 19 = 40 teams at once for the 48 items of 4 KV heads (2 sequences x 12 layers x 2 blocks); eight
+    teams go on to a second item.  In lockstep with the oracle."""
+    cfg = LLAMA8B.scaled(batch=2, layers=12, prefill_len=40000, budget=4000)
+    cap = cfg.prefill_len + 1
+    shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cap, cfg.dtype)
+    params = B.make_params(cfg.alpha, cfg.budget, 1, False, "mean", cfg.recency_bias, cfg.recency_window)
+    info = B.kv_score_plan(shape, cap, params)
+    assert (info.path, info.merge) == (B.KV_PATH_EXCHANGE, 4) and info.chunks >= 16, (info.path, info.chunks)
+    run_lockstep(cfg, 2)
+
+
 @pytest.mark.parametrize("cfg", [LLAMA8B.scaled(batch=2, layers=3, prefill_len=300, budget=60),
                                  QWEN.scaled(batch=3, layers=2, prefill_len=200, budget=50)],
                          ids=["llama8b_reduced", "qwen_reduced"])
