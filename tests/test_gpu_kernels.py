@@ -41,6 +41,8 @@ SCORE_CASES = [
     ("bf16", 128, 10, 2, 701, 1, 2, True),    # group 5: three padded heads in the matrix-core tile
     ("bf16", 128, 24, 2, 509, 1, 2, False),   # group 12 (padded group 16)
     ("bf16", 64, 12, 2, 20001, 1, 1, True),   # group 6, d = 64: one line per row, chunks exchanging statistics
+    ("f32", 128, 8, 4, 12000, 2, 2, True),    # f32 chunks exchanging statistics in teams of 4 KV heads
+    ("bf16", 128, 16, 8, 15001, 1, 3, False),  # group 2, teams of 4 KV heads over a ragged last chunk
 ]
 
 
