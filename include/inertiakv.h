@@ -113,19 +113,21 @@ typedef struct {
     int32_t recency_window; /* positions p >= new_pos - (window - 1) get the bias                   */
     int32_t rule;           /* kv_rule                                                             */
     int32_t score_variant;  /* kv_score_variant bits (0 = the attention score of Eq. 1)             */
-    int32_t score_merge;    /* performance only, results are unchanged: KV heads of one (layer,
-                               sequence) whose group sums one scoring workgroup adds before writing
-                               them.  0 = chosen from the shape and the device; else a divisor of
-                               n_kv_heads, at most 8, and 1 with VNorm.  Applies to slabs scored in
-                               one workgroup (not to long slabs scored in chunks).  kv_evict_finish
-                               must be given the value the separate step would use.               */
+    int32_t score_merge;    /* performance only (the same sums added in another order: results agree
+                               to rounding): KV heads of one (layer, sequence) whose group sums one
+                               scoring workgroup, or one team of chunks exchanging their statistics,
+                               adds before writing them.  0 = chosen from the shape and the device;
+                               else a divisor of n_kv_heads, at most 8, and 1 with VNorm.  Long slabs
+                               scored by chunks that write logits keep 1.  kv_evict_finish must be
+                               given the value the separate step would use.                        */
 } kv_params;
 
 /* Optional timing hooks: when an entry is non-NULL, kv_evict_step records that hipEvent_t on its stream
  * immediately before (begin) / after (end) the kernels of the phase.  Phases: 0 append, 1 score, 2 fold,
- * 3 select, 4 compact.  On a refresh step over a cache of at most B tokens (without VNorm or a rank trace) the
- * newcomer is scored from k_new and written once, into the slot it takes: phase 3 then times the selection
- * with that placement, and phases 0 and 4 record their events back to back. */
+ * 3 select, 4 compact.  On a refresh step over a cache of at most B tokens (without a rank trace, and with
+ * the value-norm cache when VNorm is on) the newcomer is scored from k_new and written once, into the slot it
+ * takes: phase 3 then times the selection with that placement, and phases 0 and 4 record their events back
+ * to back. */
 #define KV_PHASES 5
 typedef struct {
     void* begin[KV_PHASES];
