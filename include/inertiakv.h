@@ -268,7 +268,9 @@ kv_status kv_evict_step_static(const kv_shape* shape, const kv_params* params, i
  * dominant per-step cost, appendix "Hook-level profiling").  A step t is
  *     kv_append(t) ; kv_attend_score(layers ...) over every layer, emit_scores = refresh step ;
  *     kv_evict_finish(t)
- * and leaves the cache, u and pos exactly as kv_evict_step would (same scores, same fold, same selection).
+ * and leaves the cache, u and pos as kv_evict_step would: bit for bit when each slab of an attention call is
+ * one workgroup (the scorer's arithmetic in its order, e.g. all layers of a steady step in one call), else with
+ * scores that agree to rounding (a slab cut into row chunks whose statistics a second kernel combines).
  * All three calls of a step use the same workspace (the group sums of each layer live in it between the
  * attention calls and the finish), sized by kv_workspace_bytes for at least n_in + 1 tokens.
  *
