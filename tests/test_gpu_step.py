@@ -244,6 +244,20 @@ def test_first_step_exchange_teams_lockstep(merge, entropy):
     run_lockstep(cfg, 2, entropy=entropy, merge=merge)
 
 
+@pytest.mark.parametrize("cfg,chunks,merge", [(LLAMA8B, 16, 4), (SCOREFREE128K, 61, 4), (QWEN, 4, 4)],
+                         ids=["llama8b_32k", "scorefree_128k", "qwen_8k"])
+def test_first_step_plans_of_the_benchmark_shapes(cfg, chunks, merge):
+    """The planner's first-step choices at the benchmark's shapes on an MI355X (256 CUs): the exchange path,
+    42.5 KiB chunks of logits and item sums for groups of 4 (16 chunks per 32k slab, 61 per 128k slab), 80 KiB
+    for Qwen's padded group of 8, and teams of 4 KV heads; VNorm keeps one row per KV head (52 KiB chunks)."""
+    n = cfg.prefill_len + 1
+    shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.capacity, cfg.dtype)
+    info = B.kv_score_plan(shape, n, B.make_params(cfg.alpha, cfg.budget, 1))
+    assert (info.path, info.chunks, info.merge) == (B.KV_PATH_EXCHANGE, chunks, merge)
+    vn = B.kv_score_plan(shape, n, B.make_params(cfg.alpha, cfg.budget, 1, vnorm=True))
+    assert vn.path == B.KV_PATH_EXCHANGE and vn.merge == 1
+
+
 def test_first_step_exchange_teams_several_items_each():
     """Exchange teams that score more than one item: 40,001 tokens make 19 chunks per slab, so an MI355X holds
     768 / 19 = 40 teams at once for the 48 items of 4 KV heads (2 sequences x 12 layers x 2 blocks); eight
