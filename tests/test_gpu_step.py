@@ -258,6 +258,16 @@ def test_first_step_plans_of_the_benchmark_shapes(cfg, chunks, merge):
     assert vn.path == B.KV_PATH_EXCHANGE and vn.merge == 1
 
 
+@pytest.mark.parametrize("cfg,merge", [(LLAMA8B, 4), (QWEN, 2)], ids=["llama8b_32k", "qwen_8k"])
+def test_steady_step_plans_of_the_benchmark_shapes(cfg, merge):
+    """The planner's steady-step choices at the benchmark's shapes on an MI355X: one workgroup per item of
+    `merge` KV heads with its logits in LDS (8B: 512 items of 4, two per CU; Qwen-shaped: 1,792 items of 2)."""
+    n = cfg.budget + 1
+    shape = B.make_shape(cfg.batch, cfg.layers, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, n, cfg.dtype)
+    info = B.kv_score_plan(shape, n, B.make_params(cfg.alpha, cfg.budget, 1))
+    assert (info.path, info.chunks, info.merge) == (B.KV_PATH_LDS, 1, merge)
+
+
 def test_first_step_exchange_teams_several_items_each():
     """Exchange teams that score more than one item: 40,001 tokens make 19 chunks per slab, so an MI355X holds
     768 / 19 = 40 teams at once for the 48 items of 4 KV heads (2 sequences x 12 layers x 2 blocks); eight
