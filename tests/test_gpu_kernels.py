@@ -104,6 +104,8 @@ SELECT_CASES = [
     # long sequences in a small batch: the multi-workgroup selection (slices of every sequence)
     (4, 20000, 2000, "ties"), (2, 131073, 13107, "random"), (8, 32769, 3277, "equal"), (1, 16384, 16382, "random"),
     (3, 50000, 100, "tiny"), (2, 20000, 19998, "ties"),
+    # the edges of that choice: 128 sequences still slice (4 per sequence), 129 do not; 16,383 tokens do not
+    (128, 16384, 1638, "ties"), (129, 16384, 1638, "random"), (5, 16383, 1000, "random"), (5, 16384, 1000, "equal"),
 ]
 
 
