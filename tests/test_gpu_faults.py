@@ -48,7 +48,7 @@ def test_exchange_give_up_is_reported_by_kv_score_ema():
     p = B.make_params(0.9, cfg.budget)
     info = B.kv_score_plan(shape, n, p)
     # chunks in teams that add the group sums of the 4 KV heads: one give-up poisons the team's whole row
-    assert info.path == B.KV_PATH_EXCHANGE and info.chunks > 1 and info.merge == 4, (info.path, info.chunks, info.merge)
+    assert (info.path, info.merge) == (B.KV_PATH_EXCHANGE, 4) and info.chunks > 1, (info.path, info.chunks)
     print(f"fault case: n={n}, {info.chunks} chunks per slab, teams of {info.merge} KV heads", flush=True)
     ws = B.workspace(shape, n)
     si = w.step_inputs(1)
